@@ -1,0 +1,192 @@
+/*
+ * libjpi — C ABI of an MI355X (gfx950) flow-matching action-expert denoiser.
+ *
+ * The operation (paper: "Jetson-PI: Towards Onboard Real-Time Robot Control
+ * via Foresight-Aligned Asynchronous Inference"):
+ *   - Background section and Appendix "Model Architecture of pi series
+ *     Models": the VLM passes its per-layer KV cache to the action expert,
+ *     a DiT whose input is random action noise; at each layer the action
+ *     tokens attend with their own queries to keys/values formed by
+ *     concatenating the LLM layer's KV cache with the action tokens' own;
+ *     a fixed number of flow-matching denoising steps refines the noise
+ *     into an action chunk.
+ *   - Algorithm 1 ("confidence-based scheduling"): the call f_act(h, B_kv)
+ *     is made on every scheduler iteration; it is what jpi_denoise runs.
+ *   - Section "System Design": the computation graph is built once and
+ *     reused (fixed token length), intermediates stay in fixed-size
+ *     GPU-resident buffers, and all denoising steps are unrolled into one
+ *     graph.  libjpi captures the whole N-step loop once per shape into a
+ *     HIP graph over context-owned buffers.
+ *
+ * Semantics fixed where the paper is silent (also in the oracle's header):
+ *   flow from noise at t=1 to actions at t=0, t_k = 1 - k/N, explicit Euler
+ *   x <- x + dt v(x, t_k) with dt = -1/N; adaRMSNorm y = rms(h)(1+scale)+shift
+ *   with (scale, shift, gate) = Linear(swish(T2 swish(T1 emb(t) + b1) + b2)),
+ *   residual h += gate * sublayer(y); tanh-GELU GeGLU MLP; one KV head shared
+ *   by all query heads; RoPE (base rope_base, half-split pairs) on action
+ *   queries/keys at positions prefix_len + i; prefix K already rotated;
+ *   each action query sees prefix slots j < prefix_len and all action keys;
+ *   rows i < n_fixed are committed actions, never updated.
+ *
+ * Conventions
+ *   - Every call returns a jpi_status; nothing throws or aborts.  The text of
+ *     the last failure on a context is jpi_last_error(ctx).
+ *   - "device" pointers are HIP device pointers on the context's device;
+ *     "host" pointers are ordinary CPU memory.  The library never frees or
+ *     keeps caller memory beyond the stream order of the call that used it.
+ *   - Streams are hipStream_t values passed as void* (NULL = null stream).
+ *     Work is enqueued asynchronously; synchronise the stream (or call
+ *     jpi_sync) before reading outputs on the host.
+ *   - A context is not thread-safe; use one context per stream.
+ *   - Matrices are row-major [out][in] (y = x W^T); activation rows are
+ *     m = b*horizon + i.  bf16 data is passed as raw 16-bit patterns.
+ */
+#ifndef JPI_H_
+#define JPI_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define JPI_ABI_VERSION 1
+
+typedef enum {
+  JPI_OK = 0,
+  JPI_ERR_ARG = 1,          /* NULL pointer, value out of range, unknown name */
+  JPI_ERR_SHAPE = 2,        /* element count or size does not match the config */
+  JPI_ERR_DTYPE = 3,        /* wrong element type for this tensor */
+  JPI_ERR_STATE = 4,        /* call made in the wrong order (e.g. no weights yet) */
+  JPI_ERR_OOM = 5,          /* device allocation failed */
+  JPI_ERR_HIP = 6,          /* a HIP runtime call failed (text in jpi_last_error) */
+  JPI_ERR_UNSUPPORTED = 7   /* valid request this version does not implement */
+} jpi_status;
+
+typedef enum { JPI_F32 = 0, JPI_BF16 = 1 } jpi_dtype;
+
+typedef struct {
+  int n_layers;     /* L   (pi0.5 expert: 18, Table "pi_architecture") */
+  int width;        /* W   (1024) */
+  int n_heads;      /* query heads (8) */
+  int n_kv_heads;   /* KV heads; this version requires 1 */
+  int head_dim;     /* Dh  (256); multiple of 32 */
+  int mlp_dim;      /* F   GeGLU hidden width (4096) */
+  int action_dim;   /* A   (32) */
+  int horizon;      /* H   action tokens per chunk (50) */
+  int max_batch;    /* rollouts per call, upper bound for resident buffers */
+  int max_prefix;   /* prefix tokens per rollout, upper bound */
+  jpi_dtype dtype;  /* storage type of matrices, prefix KV and activations */
+  float rms_eps;    /* 1e-6 */
+  float rope_base;  /* 1e4 */
+} jpi_config;
+
+typedef struct jpi_ctx jpi_ctx;
+
+/* ABI version of the loaded library (JPI_ABI_VERSION it was built with). */
+int jpi_abi_version(void);
+
+/* Static description of a status code.  Never NULL. */
+const char* jpi_status_str(jpi_status s);
+
+/* Text of the last failure on ctx ("" if none; a static message if ctx is NULL). */
+const char* jpi_last_error(const jpi_ctx* ctx);
+
+/* Create a context on HIP device `device`.  The config is validated on the
+ * host before any HIP call: dims must be positive, n_kv_heads == 1,
+ * n_heads % n_kv_heads == 0, head_dim a multiple of 32, width a multiple of
+ * 64, mlp_dim a multiple of 64 (JPI_ERR_ARG otherwise).  All resident buffers
+ * (max_batch x max_prefix prefix KV, activations, partial sums, weights) are
+ * allocated here and owned by the context (Section "System Design":
+ * GPU-resident intermediate buffers).  On failure *out is NULL. */
+jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out);
+
+/* Free everything the context owns.  NULL is accepted. */
+jpi_status jpi_destroy(jpi_ctx* ctx);
+
+/* Copy one named expert tensor into the context (packed for the kernels).
+ * Names and shapes ([out][in] for matrices):
+ *   action_in.w [W][A]  action_in.b [W]
+ *   time_mlp.0.w [W][W] time_mlp.0.b [W]  time_mlp.1.w [W][W] time_mlp.1.b [W]
+ *   layers.{l}.attn_mod.w [3W][W]  .attn_mod.b [3W]   (scale | shift | gate)
+ *   layers.{l}.q.w [nH*Dh][W]  .k.w [Dh][W]  .v.w [Dh][W]  .o.w [W][nH*Dh]
+ *   layers.{l}.mlp_mod.w [3W][W]  .mlp_mod.b [3W]
+ *   layers.{l}.gate.w [F][W]  .up.w [F][W]  .down.w [W][F]
+ *   final_mod.w [2W][W]  final_mod.b [2W]           (scale | shift)
+ *   action_out.w [A][W]  action_out.b [A]
+ * Matrices must have dt == cfg.dtype, vectors dt == JPI_F32.  `data` is a
+ * device pointer if is_device != 0, else a host pointer; the caller keeps
+ * ownership.  The copy is complete when the call returns (the stream is
+ * synchronised).  Errors: JPI_ERR_ARG (unknown name / NULL), JPI_ERR_SHAPE
+ * (n_elems), JPI_ERR_DTYPE.  Setting a weight invalidates cached tables and
+ * graphs. */
+jpi_status jpi_set_weight(jpi_ctx* ctx, const char* name, const void* data, int64_t n_elems,
+                          jpi_dtype dt, int is_device, void* stream);
+
+/* Check that every tensor has been set (JPI_ERR_STATE names the first
+ * missing one) and mark the weights ready. */
+jpi_status jpi_finalize_weights(jpi_ctx* ctx, void* stream);
+
+/* Zero-copy producer path: the context's resident prefix K and V buffers,
+ * each [L][max_batch][max_prefix][Dh] of cfg.dtype.  A producer (the VLM
+ * prefill) may write rollout b, layer l, token j at
+ * ((l*max_batch + b)*max_prefix + j)*Dh and then call jpi_bind_prefix with
+ * k == *k_out, v == *v_out and prefix == max_prefix (no copy is made). */
+jpi_status jpi_prefix_buffers(jpi_ctx* ctx, void** k_out, void** v_out);
+
+/* Bind the per-layer prefix KV cache (Appendix: keys/values of the LLM layer).
+ * k, v: device pointers, [L][batch][prefix][Dh] of cfg.dtype, prefix K already
+ * rotated.  They are copied (stream-ordered) into the resident buffers unless
+ * they are those buffers.  prefix_len_host: host array [batch] of valid
+ * lengths in [0, prefix] (NULL = all `prefix`); slots j >= prefix_len are
+ * never read.  Errors: JPI_ERR_ARG (NULL), JPI_ERR_SHAPE (batch outside
+ * [1, max_batch], prefix outside [0, max_prefix], prefix_len out of range). */
+jpi_status jpi_bind_prefix(jpi_ctx* ctx, const void* k, const void* v, const int32_t* prefix_len_host,
+                           int batch, int prefix, void* stream);
+
+/* Bind the per-call state besides the prefix: n_fixed committed action rows
+ * (Algorithm 1: actions already committed for execution while the next chunk
+ * is inferred).  committed_dev: device [batch][n_fixed][A] fp32 (may be NULL
+ * if n_fixed == 0), copied stream-ordered.  n_fixed in [0, horizon).  The
+ * correction tokens (corr_tokens, n_corr) are reserved; n_corr must be 0
+ * (JPI_ERR_UNSUPPORTED otherwise).  Must follow jpi_bind_prefix (batch). */
+jpi_status jpi_bind_state(jpi_ctx* ctx, const float* committed_dev, int n_fixed, const void* corr_tokens,
+                          int n_corr, void* stream);
+
+/* Denoise one action chunk per rollout: x starts at noise (rows < n_fixed
+ * take the committed values), then n_steps Euler steps of the velocity field
+ * run, and x is written to actions_dev.  noise_dev, actions_dev: device
+ * [batch][H][A] fp32 (may alias).  Stream-ordered and asynchronous.  The first
+ * call per (batch, prefix, n_steps, n_fixed, prefix lengths) builds the
+ * modulation tables for the N step times and captures the N-step loop into a
+ * HIP graph; later calls replay it.  Errors: JPI_ERR_STATE (weights not
+ * finalized or no prefix bound), JPI_ERR_ARG (NULL, n_steps < 1). */
+jpi_status jpi_denoise(jpi_ctx* ctx, const float* noise_dev, int n_steps, float* actions_dev, void* stream);
+
+/* Synchronise `stream` and report asynchronous HIP errors as JPI_ERR_HIP. */
+jpi_status jpi_sync(jpi_ctx* ctx, void* stream);
+
+/* ---- kernel-level entry points used by the parity tests ------------------ */
+
+/* C[M][N] (fp32) = A[M][K] . W[N][K]^T with the library's GEMM kernel.
+ * A, W: device, dtype dt (JPI_BF16 -> bf16 MFMA with fp32 accumulation,
+ * JPI_F32 -> fp32 MFMA).  splitk >= 1 splits K across workgroups with a
+ * fixed-order reduction.  Errors: JPI_ERR_ARG (NULL, sizes < 1, K not a
+ * multiple of 32*splitk). */
+jpi_status jpi_debug_gemm(const void* A, const void* W, float* C, int M, int N, int K, jpi_dtype dt,
+                          int splitk, void* stream);
+
+/* Prefix+self attention of one layer for `batch` rollouts with one shared KV
+ * head, as used inside jpi_denoise (queries already rotated):
+ *   q  [batch][n_heads][H][Dh], ks/vs [batch][H][Dh], kp/vp [batch][P][Dh]
+ *   (all dtype dt, device), prefix_len_host [batch] host,
+ *   out [batch*H][n_heads*Dh] fp32 device.
+ * Errors: JPI_ERR_ARG. */
+jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, const void* kp, const void* vp,
+                               const int32_t* prefix_len_host, int batch, int n_heads, int H, int P,
+                               int Dh, jpi_dtype dt, float* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* JPI_H_ */

@@ -61,9 +61,14 @@ TIME_MAX_PERIOD = 1.0e4
 def widen(a: np.ndarray) -> np.ndarray:
     """fp64 copy of an input array; uint16 arrays are bf16 bit patterns."""
     a = np.asarray(a)
+    out = np.empty(a.shape, dtype=np.float64)
     if a.dtype == np.uint16:
-        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-    return a.astype(np.float64)
+        bits = a.astype(np.uint32)
+        np.left_shift(bits, 16, out=bits)
+        out[...] = bits.view(np.float32)
+    else:
+        out[...] = a
+    return out
 
 
 class Expert:

@@ -1,0 +1,886 @@
+// libjpi runtime: context, weight packing, resident buffers, the modulation
+// table cache and the HIP-graph cache, behind the C ABI of include/jpi.h.
+//
+// Packed weight layout on the device (dtype = cfg.dtype, row-major [out][in]):
+//   per layer, contiguous:  QKV [(nH+2)Dh][W] | O [W][nH Dh] | GU [2F][W] | D [W][F]
+//   QKV rows: q heads then k then v.  Inside each q head and inside k, 32-row
+//   group t holds original rows 16t..16t+15 followed by Dh/2+16t..Dh/2+16t+15,
+//   so a GEMM output tile sees each RoPE pair (d, d + Dh/2) in one lane.
+//   GU rows: 32-row group t holds gate rows 16t..16t+15 then up rows
+//   16t..16t+15, so GeGLU pairs also land in one lane.
+//   Modulation: all attn_mod / mlp_mod / final_mod rows stacked into one
+//   [(6L+2)W][W] matrix; row block 2l is layer l's attention norm, 2l+1 its
+//   MLP norm, 2L the final norm (scale | shift | gate, W rows each).
+//
+// Per denoise step k the modulation depends only on t_k = 1 - k/N, so the
+// table [N][(6L+2)W] of all (scale, shift, gate) is computed once per
+// (weights, N) and read by the step kernels.
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "jpi_internal.h"
+
+using namespace jpi;
+
+namespace {
+
+enum TensorKind {
+  T_IN_W, T_IN_B, T_TIME0_W, T_TIME0_B, T_TIME1_W, T_TIME1_B, T_ATTN_MOD_W, T_ATTN_MOD_B, T_Q, T_K, T_V, T_O,
+  T_MLP_MOD_W, T_MLP_MOD_B, T_GATE, T_UP, T_DOWN, T_FINAL_MOD_W, T_FINAL_MOD_B, T_OUT_W, T_OUT_B, T_NKINDS
+};
+
+const char* kind_suffix[T_NKINDS] = {"action_in.w", "action_in.b", "time_mlp.0.w", "time_mlp.0.b", "time_mlp.1.w",
+                                     "time_mlp.1.b", "attn_mod.w", "attn_mod.b", "q.w", "k.w", "v.w", "o.w",
+                                     "mlp_mod.w", "mlp_mod.b", "gate.w", "up.w", "down.w", "final_mod.w",
+                                     "final_mod.b", "action_out.w", "action_out.b"};
+
+bool kind_is_layer(int k) { return k >= T_ATTN_MOD_W && k <= T_DOWN; }
+bool kind_is_matrix(int k) {
+  return k == T_IN_W || k == T_TIME0_W || k == T_TIME1_W || k == T_ATTN_MOD_W || k == T_Q || k == T_K || k == T_V ||
+         k == T_O || k == T_MLP_MOD_W || k == T_GATE || k == T_UP || k == T_DOWN || k == T_FINAL_MOD_W ||
+         k == T_OUT_W;
+}
+
+struct GraphKey {
+  int batch, prefix, n_steps, n_fixed;
+  bool operator<(const GraphKey& o) const {
+    return std::tie(batch, prefix, n_steps, n_fixed) < std::tie(o.batch, o.prefix, o.n_steps, o.n_fixed);
+  }
+};
+
+__global__ void k_scatter_rows(const char* __restrict__ src, char* __restrict__ dst, const int* __restrict__ map,
+                               int rows, int row_bytes) {
+  const int r = blockIdx.x;
+  if (r >= rows) return;
+  const char* s = src + (size_t)r * row_bytes;
+  char* d = dst + (size_t)map[r] * row_bytes;
+  for (int i = threadIdx.x * 4; i < row_bytes; i += blockDim.x * 4) *reinterpret_cast<int*>(d + i) = *reinterpret_cast<const int*>(s + i);
+}
+
+}  // namespace
+
+struct jpi_ctx {
+  jpi_config cfg;
+  int device = 0, n_cu = 0;
+  std::string err;
+  int L, W, nH, Dh, F, A, H, Bmax, Pmax, Mmax;
+  jpi_dtype dt;
+  size_t esz;
+  int R;  // modulation rows (6L+2)W
+  // packed weights
+  void* w_layers = nullptr;
+  size_t layer_elems = 0, off_o = 0, off_gu = 0, off_d = 0;
+  void *w_in = nullptr, *w_t0 = nullptr, *w_t1 = nullptr, *w_mod = nullptr, *w_out = nullptr;
+  float *b_in = nullptr, *b_t0 = nullptr, *b_t1 = nullptr, *b_mod = nullptr, *b_out = nullptr;
+  std::vector<char> have;  // per (kind, layer)
+  bool finalized = false;
+  // prefix and state
+  void *kp = nullptr, *vp = nullptr;
+  int* d_prefix_len = nullptr;
+  int* h_prefix_len = nullptr;  // pinned staging
+  int batch = 0, prefix = 0;
+  bool prefix_bound = false;
+  float2* rope_tab = nullptr;
+  float* committed = nullptr;
+  int n_fixed = 0;
+  // activations
+  float *x = nullptr, *h = nullptr;
+  void *y = nullptr, *q = nullptr, *ks = nullptr, *vs = nullptr, *o = nullptr, *z = nullptr;
+  float* partial = nullptr;
+  size_t partial_cap = 0;
+  unsigned* counters = nullptr;
+  size_t counters_cap = 0;
+  float *opart = nullptr, *mlpart = nullptr;
+  size_t attn_cap = 0;
+  // caches
+  std::map<int, float*> tables;
+  std::map<GraphKey, hipGraphExec_t> graphs;
+  hipStream_t cap_stream = nullptr;
+};
+
+namespace {
+
+thread_local std::string g_noctx_err;
+
+jpi_status fail(jpi_ctx* c, jpi_status st, const std::string& msg) {
+  if (c) c->err = msg;
+  else g_noctx_err = msg;
+  return st;
+}
+
+#define HIPCHK(c, expr)                                                                     \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail((c), e_ == hipErrorOutOfMemory ? JPI_ERR_OOM : JPI_ERR_HIP,               \
+                  std::string(#expr) + ": " + hipGetErrorString(e_));                       \
+  } while (0)
+
+jpi_status dmalloc(jpi_ctx* c, void** p, size_t bytes) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return fail(c, JPI_ERR_OOM, "hipMalloc of " + std::to_string(bytes) + " bytes failed: " + hipGetErrorString(e));
+  }
+  return JPI_OK;
+}
+
+#define TRY(expr)                    \
+  do {                               \
+    jpi_status st_ = (expr);         \
+    if (st_ != JPI_OK) return st_;   \
+  } while (0)
+
+void drop_graphs(jpi_ctx* c) {
+  for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
+  c->graphs.clear();
+}
+
+void drop_tables(jpi_ctx* c) {
+  for (auto& kv : c->tables) (void)hipFree(kv.second);
+  c->tables.clear();
+}
+
+int64_t expected_elems(const jpi_ctx* c, int k) {
+  const int64_t W = c->W, A = c->A, Dh = c->Dh, nH = c->nH, F = c->F;
+  switch (k) {
+    case T_IN_W: return W * A;
+    case T_IN_B: return W;
+    case T_TIME0_W: case T_TIME1_W: return W * W;
+    case T_TIME0_B: case T_TIME1_B: return W;
+    case T_ATTN_MOD_W: case T_MLP_MOD_W: return 3 * W * W;
+    case T_ATTN_MOD_B: case T_MLP_MOD_B: return 3 * W;
+    case T_Q: return nH * Dh * W;
+    case T_K: case T_V: return Dh * W;
+    case T_O: return W * nH * Dh;
+    case T_GATE: case T_UP: return F * W;
+    case T_DOWN: return W * F;
+    case T_FINAL_MOD_W: return 2 * W * W;
+    case T_FINAL_MOD_B: return 2 * W;
+    case T_OUT_W: return A * W;
+    case T_OUT_B: return A;
+  }
+  return -1;
+}
+
+// Parse "layers.{l}.<suffix>" or a global name.  Returns false if unknown.
+bool parse_name(const jpi_ctx* c, const char* name, int* kind, int* layer) {
+  *layer = -1;
+  const char* pre = "layers.";
+  if (strncmp(name, pre, 7) == 0) {
+    const char* p = name + 7;
+    if (*p < '0' || *p > '9') return false;
+    char* end = nullptr;
+    long l = strtol(p, &end, 10);
+    if (!end || *end != '.' || l < 0 || l >= c->L) return false;
+    for (int k = T_ATTN_MOD_W; k <= T_DOWN; ++k)
+      if (strcmp(end + 1, kind_suffix[k]) == 0) {
+        *kind = k;
+        *layer = (int)l;
+        return true;
+      }
+    return false;
+  }
+  for (int k = 0; k < T_NKINDS; ++k)
+    if (!kind_is_layer(k) && strcmp(name, kind_suffix[k]) == 0) {
+      *kind = k;
+      return true;
+    }
+  return false;
+}
+
+int have_index(const jpi_ctx* c, int kind, int layer) {
+  return kind_is_layer(kind) ? T_NKINDS + layer * T_NKINDS + kind : kind;
+}
+
+// packed row of source row r for q / k (RoPE pairs (d, d + Dh/2) in one 32-row group)
+int rope_pack_row(int r, int Dh) {
+  const int half = Dh / 2;
+  const int dd = r % Dh, head = r / Dh;
+  const int hi = dd >= half ? 1 : 0;
+  const int d = dd - hi * half;
+  return head * Dh + (d / 16) * 32 + hi * 16 + (d % 16);
+}
+
+}  // namespace
+
+extern "C" {
+
+int jpi_abi_version(void) { return JPI_ABI_VERSION; }
+
+const char* jpi_status_str(jpi_status s) {
+  switch (s) {
+    case JPI_OK: return "ok";
+    case JPI_ERR_ARG: return "invalid argument";
+    case JPI_ERR_SHAPE: return "shape mismatch";
+    case JPI_ERR_DTYPE: return "dtype mismatch";
+    case JPI_ERR_STATE: return "invalid call order";
+    case JPI_ERR_OOM: return "device out of memory";
+    case JPI_ERR_HIP: return "HIP runtime error";
+    case JPI_ERR_UNSUPPORTED: return "unsupported";
+  }
+  return "unknown status";
+}
+
+const char* jpi_last_error(const jpi_ctx* ctx) { return ctx ? ctx->err.c_str() : g_noctx_err.c_str(); }
+
+jpi_status jpi_destroy(jpi_ctx* c) {
+  if (!c) return JPI_OK;
+  (void)hipSetDevice(c->device);
+  (void)hipDeviceSynchronize();
+  drop_graphs(c);
+  drop_tables(c);
+  void* bufs[] = {c->w_layers, c->w_in, c->w_t0, c->w_t1, c->w_mod, c->w_out, c->b_in, c->b_t0, c->b_t1, c->b_mod,
+                  c->b_out, c->kp, c->vp, c->d_prefix_len, c->rope_tab, c->committed, c->x, c->h, c->y, c->q, c->ks,
+                  c->vs, c->o, c->z, c->partial, c->counters, c->opart, c->mlpart};
+  for (void* p : bufs)
+    if (p) (void)hipFree(p);
+  if (c->h_prefix_len) (void)hipHostFree(c->h_prefix_len);
+  if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
+  delete c;
+  return JPI_OK;
+}
+
+jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
+  if (!out) return fail(nullptr, JPI_ERR_ARG, "jpi_create: out is NULL");
+  *out = nullptr;
+  if (!cfg) return fail(nullptr, JPI_ERR_ARG, "jpi_create: cfg is NULL");
+  const jpi_config& g = *cfg;
+  if (g.n_layers < 1 || g.width < 1 || g.n_heads < 1 || g.n_kv_heads < 1 || g.head_dim < 1 || g.mlp_dim < 1 ||
+      g.action_dim < 1 || g.horizon < 1 || g.max_batch < 1 || g.max_prefix < 0)
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: every dimension must be positive");
+  if (g.n_kv_heads != 1 || g.n_heads % g.n_kv_heads != 0)
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: this version implements exactly one shared KV head");
+  if (g.head_dim != 64 && g.head_dim != 128 && g.head_dim != 256)
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: head_dim must be 64, 128 or 256");
+  if (g.width % 64 != 0 || g.mlp_dim % 64 != 0 || (g.n_heads * g.head_dim) % 64 != 0)
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: width, mlp_dim and n_heads*head_dim must be multiples of 64");
+  if (g.dtype != JPI_F32 && g.dtype != JPI_BF16) return fail(nullptr, JPI_ERR_ARG, "jpi_create: bad dtype");
+  if (!(g.rms_eps > 0.f) || !(g.rope_base > 1.f))
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: rms_eps must be > 0 and rope_base > 1");
+  if ((long long)g.max_batch * g.horizon > (1 << 20) || g.max_prefix > (1 << 20))
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: max_batch*horizon or max_prefix too large");
+
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev) {
+    (void)hipGetLastError();
+    return fail(nullptr, JPI_ERR_HIP, "jpi_create: no HIP device " + std::to_string(device));
+  }
+  jpi_ctx* c = new jpi_ctx();
+  c->cfg = g;
+  c->device = device;
+  c->L = g.n_layers;
+  c->W = g.width;
+  c->nH = g.n_heads;
+  c->Dh = g.head_dim;
+  c->F = g.mlp_dim;
+  c->A = g.action_dim;
+  c->H = g.horizon;
+  c->Bmax = g.max_batch;
+  c->Pmax = g.max_prefix;
+  c->Mmax = g.max_batch * g.horizon;
+  c->dt = g.dtype;
+  c->esz = g.dtype == JPI_BF16 ? 2 : 4;
+  c->R = (6 * c->L + 2) * c->W;
+  c->have.assign(T_NKINDS + (size_t)c->L * T_NKINDS, 0);
+
+  auto cleanup_fail = [&](jpi_status st) {
+    std::string msg = c->err;
+    jpi_destroy(c);
+    return fail(nullptr, st, msg);
+  };
+  if (hipSetDevice(device) != hipSuccess) {
+    (void)hipGetLastError();
+    return cleanup_fail(fail(c, JPI_ERR_HIP, "hipSetDevice failed"));
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, device) != hipSuccess) return cleanup_fail(fail(c, JPI_ERR_HIP, "props"));
+  c->n_cu = prop.multiProcessorCount;
+  if (hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess)
+    return cleanup_fail(fail(c, JPI_ERR_HIP, "stream create failed"));
+
+  const size_t es = c->esz;
+  const size_t W = c->W, Dh = c->Dh, nH = c->nH, F = c->F, A = c->A, M = c->Mmax;
+  c->layer_elems = (nH + 2) * Dh * W + W * nH * Dh + 2 * F * W + W * F;
+  c->off_o = (nH + 2) * Dh * W;
+  c->off_gu = c->off_o + W * nH * Dh;
+  c->off_d = c->off_gu + 2 * F * W;
+  jpi_status st;
+#define ALLOC(ptr, bytes)                                          \
+  st = dmalloc(c, (void**)&(ptr), (bytes));                        \
+  if (st != JPI_OK) return cleanup_fail(st);
+  ALLOC(c->w_layers, c->layer_elems * c->L * es);
+  ALLOC(c->w_in, W * A * es);
+  ALLOC(c->b_in, W * 4);
+  ALLOC(c->w_t0, W * W * es);
+  ALLOC(c->w_t1, W * W * es);
+  ALLOC(c->b_t0, W * 4);
+  ALLOC(c->b_t1, W * 4);
+  ALLOC(c->w_mod, (size_t)c->R * W * es);
+  ALLOC(c->b_mod, (size_t)c->R * 4);
+  ALLOC(c->w_out, A * W * es);
+  ALLOC(c->b_out, A * 4);
+  const size_t kv_elems = (size_t)c->L * c->Bmax * (size_t)c->Pmax * Dh;
+  ALLOC(c->kp, kv_elems * es);
+  ALLOC(c->vp, kv_elems * es);
+  ALLOC(c->d_prefix_len, c->Bmax * 4);
+  ALLOC(c->rope_tab, M * (Dh / 2) * sizeof(float2));
+  ALLOC(c->committed, M * A * 4);
+  ALLOC(c->x, M * A * 4);
+  ALLOC(c->h, M * W * 4);
+  ALLOC(c->y, M * W * es);
+  ALLOC(c->q, M * nH * Dh * es);
+  ALLOC(c->ks, M * Dh * es);
+  ALLOC(c->vs, M * Dh * es);
+  ALLOC(c->o, M * nH * Dh * es);
+  ALLOC(c->z, M * F * es);
+#undef ALLOC
+  if (hipHostMalloc((void**)&c->h_prefix_len, c->Bmax * sizeof(int)) != hipSuccess) {
+    (void)hipGetLastError();
+    c->h_prefix_len = nullptr;
+    return cleanup_fail(fail(c, JPI_ERR_OOM, "pinned prefix_len staging"));
+  }
+  *out = c;
+  return JPI_OK;
+}
+
+jpi_status jpi_set_weight(jpi_ctx* c, const char* name, const void* data, int64_t n_elems, jpi_dtype dt,
+                          int is_device, void* stream) {
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_set_weight: ctx is NULL");
+  if (!name || !data) return fail(c, JPI_ERR_ARG, "jpi_set_weight: name or data is NULL");
+  int kind, layer;
+  if (!parse_name(c, name, &kind, &layer)) return fail(c, JPI_ERR_ARG, std::string("unknown tensor name: ") + name);
+  const int64_t want = expected_elems(c, kind);
+  if (n_elems != want)
+    return fail(c, JPI_ERR_SHAPE, std::string(name) + ": expected " + std::to_string(want) + " elements, got " +
+                                       std::to_string(n_elems));
+  const bool mat = kind_is_matrix(kind);
+  const jpi_dtype want_dt = mat ? c->dt : JPI_F32;
+  if (dt != want_dt)
+    return fail(c, JPI_ERR_DTYPE, std::string(name) + (mat ? ": matrices must have the context dtype"
+                                                           : ": vectors must be JPI_F32"));
+  HIPCHK(c, hipSetDevice(c->device));
+  hipStream_t s = (hipStream_t)stream;
+  const size_t es = mat ? c->esz : 4;
+  const size_t bytes = (size_t)n_elems * es;
+  const size_t W = c->W, Dh = c->Dh, nH = c->nH;
+
+  // destination base and row map (rows of length `cols`)
+  char* base = nullptr;
+  int rows = 0, cols = 0;
+  std::vector<int> map;
+  char* lay = layer >= 0 ? (char*)c->w_layers + (size_t)layer * c->layer_elems * c->esz : nullptr;
+  auto identity = [&](char* dst, int r, int cl) {
+    base = dst;
+    rows = r;
+    cols = cl;
+  };
+  switch (kind) {
+    case T_IN_W: identity((char*)c->w_in, c->W, c->A); break;
+    case T_IN_B: identity((char*)c->b_in, 1, c->W); break;
+    case T_TIME0_W: identity((char*)c->w_t0, c->W, c->W); break;
+    case T_TIME0_B: identity((char*)c->b_t0, 1, c->W); break;
+    case T_TIME1_W: identity((char*)c->w_t1, c->W, c->W); break;
+    case T_TIME1_B: identity((char*)c->b_t1, 1, c->W); break;
+    case T_ATTN_MOD_W: identity((char*)c->w_mod + (size_t)(2 * layer) * 3 * W * W * c->esz, 3 * c->W, c->W); break;
+    case T_ATTN_MOD_B: identity((char*)(c->b_mod + (size_t)(2 * layer) * 3 * W), 1, 3 * c->W); break;
+    case T_MLP_MOD_W:
+      identity((char*)c->w_mod + (size_t)(2 * layer + 1) * 3 * W * W * c->esz, 3 * c->W, c->W);
+      break;
+    case T_MLP_MOD_B: identity((char*)(c->b_mod + (size_t)(2 * layer + 1) * 3 * W), 1, 3 * c->W); break;
+    case T_FINAL_MOD_W: identity((char*)c->w_mod + (size_t)(6 * c->L) * W * W * c->esz, 2 * c->W, c->W); break;
+    case T_FINAL_MOD_B: identity((char*)(c->b_mod + (size_t)(6 * c->L) * W), 1, 2 * c->W); break;
+    case T_OUT_W: identity((char*)c->w_out, c->A, c->W); break;
+    case T_OUT_B: identity((char*)c->b_out, 1, c->A); break;
+    case T_O: identity(lay + c->off_o * c->esz, c->W, (int)(nH * Dh)); break;
+    case T_DOWN: identity(lay + c->off_d * c->esz, c->W, c->F); break;
+    case T_Q:
+    case T_K:
+    case T_V: {
+      base = lay;
+      cols = c->W;
+      const int r0 = kind == T_Q ? 0 : kind == T_K ? (int)(nH * Dh) : (int)((nH + 1) * Dh);
+      rows = kind == T_Q ? (int)(nH * Dh) : (int)Dh;
+      map.resize(rows);
+      for (int r = 0; r < rows; ++r) map[r] = r0 + (kind == T_V ? r : rope_pack_row(r, (int)Dh));
+      break;
+    }
+    case T_GATE:
+    case T_UP: {
+      base = lay + c->off_gu * c->esz;
+      cols = c->W;
+      rows = c->F;
+      map.resize(rows);
+      for (int f = 0; f < rows; ++f) map[f] = (f / 16) * 32 + (kind == T_UP ? 16 : 0) + (f % 16);
+      break;
+    }
+  }
+  if (map.empty()) {
+    HIPCHK(c, hipMemcpyAsync(base, data, bytes, is_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, s));
+  } else {
+    void* src = const_cast<void*>(data);
+    void* tmp = nullptr;
+    int* dmap = nullptr;
+    TRY(dmalloc(c, (void**)&dmap, map.size() * sizeof(int)));
+    if (!is_device) {
+      jpi_status st2 = dmalloc(c, &tmp, bytes);
+      if (st2 != JPI_OK) {
+        (void)hipFree(dmap);
+        return st2;
+      }
+      HIPCHK(c, hipMemcpyAsync(tmp, data, bytes, hipMemcpyHostToDevice, s));
+      src = tmp;
+    }
+    HIPCHK(c, hipMemcpyAsync(dmap, map.data(), map.size() * sizeof(int), hipMemcpyHostToDevice, s));
+    hipLaunchKernelGGL(k_scatter_rows, dim3(rows), dim3(256), 0, s, (const char*)src, base, (const int*)dmap, rows,
+                       (int)(cols * es));
+    HIPCHK(c, hipGetLastError());
+    HIPCHK(c, hipStreamSynchronize(s));
+    (void)hipFree(dmap);
+    if (tmp) (void)hipFree(tmp);
+  }
+  HIPCHK(c, hipStreamSynchronize(s));
+  c->have[have_index(c, kind, layer)] = 1;
+  c->finalized = false;
+  drop_graphs(c);
+  drop_tables(c);
+  return JPI_OK;
+}
+
+jpi_status jpi_finalize_weights(jpi_ctx* c, void* stream) {
+  (void)stream;
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_finalize_weights: ctx is NULL");
+  for (int k = 0; k < T_NKINDS; ++k) {
+    if (kind_is_layer(k)) {
+      for (int l = 0; l < c->L; ++l)
+        if (!c->have[have_index(c, k, l)])
+          return fail(c, JPI_ERR_STATE, "missing tensor layers." + std::to_string(l) + "." + kind_suffix[k]);
+    } else if (!c->have[have_index(c, k, -1)]) {
+      return fail(c, JPI_ERR_STATE, std::string("missing tensor ") + kind_suffix[k]);
+    }
+  }
+  drop_graphs(c);
+  drop_tables(c);
+  c->finalized = true;
+  return JPI_OK;
+}
+
+jpi_status jpi_prefix_buffers(jpi_ctx* c, void** k_out, void** v_out) {
+  if (!c || !k_out || !v_out) return fail(c, JPI_ERR_ARG, "jpi_prefix_buffers: NULL argument");
+  *k_out = c->kp;
+  *v_out = c->vp;
+  return JPI_OK;
+}
+
+jpi_status jpi_bind_prefix(jpi_ctx* c, const void* k, const void* v, const int32_t* prefix_len_host, int batch,
+                           int prefix, void* stream) {
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_bind_prefix: ctx is NULL");
+  if ((!k || !v) && prefix > 0) return fail(c, JPI_ERR_ARG, "jpi_bind_prefix: k or v is NULL");
+  if (batch < 1 || batch > c->Bmax)
+    return fail(c, JPI_ERR_SHAPE, "jpi_bind_prefix: batch " + std::to_string(batch) + " outside [1, max_batch=" +
+                                       std::to_string(c->Bmax) + "]");
+  if (prefix < 0 || prefix > c->Pmax)
+    return fail(c, JPI_ERR_SHAPE, "jpi_bind_prefix: prefix " + std::to_string(prefix) + " outside [0, max_prefix=" +
+                                       std::to_string(c->Pmax) + "]");
+  std::vector<int> lens(batch, prefix);
+  if (prefix_len_host)
+    for (int b = 0; b < batch; ++b) {
+      if (prefix_len_host[b] < 0 || prefix_len_host[b] > prefix)
+        return fail(c, JPI_ERR_SHAPE, "jpi_bind_prefix: prefix_len[" + std::to_string(b) + "] = " +
+                                           std::to_string(prefix_len_host[b]) + " outside [0, prefix]");
+      lens[b] = prefix_len_host[b];
+    }
+  HIPCHK(c, hipSetDevice(c->device));
+  hipStream_t s = (hipStream_t)stream;
+  HIPCHK(c, hipStreamSynchronize(s));  // staging buffer and resident KV are free to overwrite
+  const size_t es = c->esz, Dh = c->Dh;
+  const bool in_place = (k == c->kp && v == c->vp);
+  if (in_place && prefix != c->Pmax)
+    return fail(c, JPI_ERR_SHAPE, "jpi_bind_prefix: the resident buffers must be bound with prefix == max_prefix");
+  if (!in_place && prefix > 0) {
+    for (int l = 0; l < c->L; ++l) {
+      const size_t dst_off = (size_t)l * c->Bmax * c->Pmax * Dh * es;
+      const size_t src_off = (size_t)l * batch * prefix * Dh * es;
+      HIPCHK(c, hipMemcpy2DAsync((char*)c->kp + dst_off, c->Pmax * Dh * es, (const char*)k + src_off, prefix * Dh * es,
+                                 prefix * Dh * es, batch, hipMemcpyDeviceToDevice, s));
+      HIPCHK(c, hipMemcpy2DAsync((char*)c->vp + dst_off, c->Pmax * Dh * es, (const char*)v + src_off, prefix * Dh * es,
+                                 prefix * Dh * es, batch, hipMemcpyDeviceToDevice, s));
+    }
+  }
+  memcpy(c->h_prefix_len, lens.data(), batch * sizeof(int));
+  HIPCHK(c, hipMemcpyAsync(c->d_prefix_len, c->h_prefix_len, batch * sizeof(int), hipMemcpyHostToDevice, s));
+  HIPCHK(c, launch_rope_table(c->d_prefix_len, c->rope_tab, batch, c->H, c->Dh, c->cfg.rope_base, s));
+  if (c->batch != batch) c->n_fixed = 0;  // committed rows were bound for another batch
+  c->batch = batch;
+  c->prefix = prefix;
+  c->prefix_bound = true;
+  return JPI_OK;
+}
+
+jpi_status jpi_bind_state(jpi_ctx* c, const float* committed_dev, int n_fixed, const void* corr_tokens, int n_corr,
+                          void* stream) {
+  (void)corr_tokens;
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_bind_state: ctx is NULL");
+  if (n_corr != 0) return fail(c, JPI_ERR_UNSUPPORTED, "jpi_bind_state: correction tokens are not supported yet");
+  if (!c->prefix_bound) return fail(c, JPI_ERR_STATE, "jpi_bind_state: bind the prefix first (it sets the batch)");
+  if (n_fixed < 0 || n_fixed >= c->H)
+    return fail(c, JPI_ERR_ARG, "jpi_bind_state: n_fixed must be in [0, horizon)");
+  if (n_fixed > 0 && !committed_dev) return fail(c, JPI_ERR_ARG, "jpi_bind_state: committed is NULL");
+  HIPCHK(c, hipSetDevice(c->device));
+  if (n_fixed > 0)
+    HIPCHK(c, hipMemcpyAsync(c->committed, committed_dev, (size_t)c->batch * n_fixed * c->A * sizeof(float),
+                             hipMemcpyDeviceToDevice, (hipStream_t)stream));
+  c->n_fixed = n_fixed;
+  return JPI_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+jpi_status ensure_table(jpi_ctx* c, int n_steps, hipStream_t s, float** out) {
+  auto it = c->tables.find(n_steps);
+  if (it != c->tables.end()) {
+    *out = it->second;
+    return JPI_OK;
+  }
+  const size_t W = c->W;
+  float *tab = nullptr, *tmp = nullptr;
+  TRY(dmalloc(c, (void**)&tab, (size_t)n_steps * c->R * sizeof(float)));
+  jpi_status st = dmalloc(c, (void**)&tmp, (size_t)3 * n_steps * W * sizeof(float));
+  if (st != JPI_OK) {
+    (void)hipFree(tab);
+    return st;
+  }
+  float *emb = tmp, *c1 = tmp + n_steps * W, *cond = tmp + 2 * n_steps * W;
+  hipError_t e = launch_time_embed(nullptr, emb, n_steps, c->W, s);
+  if (e == hipSuccess) e = launch_rowdot(c->dt, emb, c->w_t0, c->b_t0, c1, n_steps, c->W, c->W, 1, s);
+  if (e == hipSuccess) e = launch_rowdot(c->dt, c1, c->w_t1, c->b_t1, cond, n_steps, c->W, c->W, 1, s);
+  if (e == hipSuccess) e = launch_rowdot(c->dt, cond, c->w_mod, c->b_mod, tab, n_steps, c->R, c->W, 0, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  (void)hipFree(tmp);
+  if (e != hipSuccess) {
+    (void)hipFree(tab);
+    return fail(c, JPI_ERR_HIP, std::string("modulation table: ") + hipGetErrorString(e));
+  }
+  c->tables[n_steps] = tab;
+  *out = tab;
+  return JPI_OK;
+}
+
+struct StepGemms {
+  int M;
+  int s_qkv, s_o, s_gu, s_d;
+};
+
+StepGemms plan_gemms(const jpi_ctx* c, int batch) {
+  StepGemms p;
+  p.M = batch * c->H;
+  const int qkvN = (c->nH + 2) * c->Dh;
+  p.s_qkv = gemm_pick_splitk(c->dt, p.M, qkvN, c->W, c->n_cu);
+  p.s_o = gemm_pick_splitk(c->dt, p.M, c->W, c->nH * c->Dh, c->n_cu);
+  p.s_gu = gemm_pick_splitk(c->dt, p.M, 2 * c->F, c->W, c->n_cu);
+  p.s_d = gemm_pick_splitk(c->dt, p.M, c->W, c->F, c->n_cu);
+  return p;
+}
+
+jpi_status ensure_scratch(jpi_ctx* c, int batch, int prefix) {
+  const StepGemms p = plan_gemms(c, batch);
+  const size_t M = p.M;
+  const size_t qkvN = (size_t)(c->nH + 2) * c->Dh;
+  size_t need = 0, tiles = 0;
+  auto acc = [&](int s, size_t N) {
+    if (s > 1) need = std::max(need, (size_t)s * M * N);
+    tiles = std::max(tiles, gemm_tiles(c->dt, (int)M, (int)N));
+  };
+  acc(p.s_qkv, qkvN);
+  acc(p.s_o, c->W);
+  acc(p.s_gu, 2 * (size_t)c->F);
+  acc(p.s_d, c->W);
+  bool changed = false;
+  if (need > c->partial_cap) {
+    if (c->partial) (void)hipFree(c->partial);
+    c->partial = nullptr;
+    c->partial_cap = 0;
+    TRY(dmalloc(c, (void**)&c->partial, need * sizeof(float)));
+    c->partial_cap = need;
+    changed = true;
+  }
+  if (tiles > c->counters_cap) {
+    if (c->counters) (void)hipFree(c->counters);
+    c->counters = nullptr;
+    c->counters_cap = 0;
+    TRY(dmalloc(c, (void**)&c->counters, tiles * sizeof(unsigned)));
+    HIPCHK(c, hipMemset(c->counters, 0, tiles * sizeof(unsigned)));
+    c->counters_cap = tiles;
+    changed = true;
+  }
+  const size_t nch = attn_n_chunks(c->dt, prefix, c->H);
+  const size_t attn = (size_t)batch * c->nH * nch * c->H * (c->Dh + 2);
+  if (attn > c->attn_cap) {
+    if (c->opart) (void)hipFree(c->opart);
+    c->opart = nullptr;
+    c->attn_cap = 0;
+    TRY(dmalloc(c, (void**)&c->opart, attn * sizeof(float)));
+    c->attn_cap = attn;
+    changed = true;
+  }
+  if (changed) drop_graphs(c);  // captured graphs point at the old scratch
+  return JPI_OK;
+}
+
+// Enqueue the whole N-step loop on stream s (eagerly or under capture).
+hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_t s) {
+  const int batch = c->batch, prefix = c->prefix, H = c->H;
+  const StepGemms p = plan_gemms(c, batch);
+  const int M = p.M, W = c->W, Dh = c->Dh, nH = c->nH, F = c->F, L = c->L;
+  const size_t es = c->esz;
+  const int nch = attn_n_chunks(c->dt, prefix, H);
+  const float eps = c->cfg.rms_eps;
+  const float dt_step = -1.0f / (float)n_steps;
+  hipError_t e;
+#define ENQ(x)                      \
+  do {                              \
+    e = (x);                        \
+    if (e != hipSuccess) return e;  \
+  } while (0)
+  for (int k = 0; k < n_steps; ++k) {
+    const float* tk = table + (size_t)k * c->R;
+    ENQ(launch_inproj(c->dt, c->x, c->w_in, c->b_in, c->h, M, W, c->A, s));
+    for (int l = 0; l < L; ++l) {
+      const char* lay = (const char*)c->w_layers + (size_t)l * c->layer_elems * es;
+      const float* am = tk + (size_t)(2 * l) * 3 * W;
+      const float* mm = tk + (size_t)(2 * l + 1) * 3 * W;
+      ENQ(launch_rmsnorm_mod(c->dt, c->h, am, am + W, c->y, M, W, eps, s));
+      GemmLaunch g{};
+      g.partial = c->partial;
+      g.counters = c->counters;
+      g.M = M;
+      // QKV + RoPE
+      g.A = c->y;
+      g.W = lay;
+      g.N = (nH + 2) * Dh;
+      g.K = W;
+      g.splitk = p.s_qkv;
+      g.epi = EPI_QKV;
+      g.ep.q = c->q;
+      g.ep.ks = c->ks;
+      g.ep.vs = c->vs;
+      g.ep.rope = c->rope_tab;
+      g.ep.n_heads = nH;
+      g.ep.head_dim = Dh;
+      g.ep.horizon = H;
+      ENQ(launch_gemm(c->dt, g, s));
+      // attention
+      AttnLaunch a{};
+      a.q = c->q;
+      a.ks = c->ks;
+      a.vs = c->vs;
+      a.kp = (const char*)c->kp + (size_t)l * c->Bmax * c->Pmax * Dh * es;
+      a.vp = (const char*)c->vp + (size_t)l * c->Bmax * c->Pmax * Dh * es;
+      a.kp_bstride = (int64_t)c->Pmax * Dh;
+      a.prefix_len = c->d_prefix_len;
+      a.B = batch;
+      a.nH = nH;
+      a.H = H;
+      a.P = prefix;
+      a.Dh = Dh;
+      a.opart = c->opart;
+      a.mpart = c->opart + (size_t)batch * nH * nch * H * Dh;
+      a.lpart = a.mpart + (size_t)batch * nH * nch * H;
+      a.out = c->o;
+      a.out_f32 = 0;
+      ENQ(launch_attention(c->dt, a, s));
+      // O projection + gated residual
+      g.A = c->o;
+      g.W = lay + c->off_o * es;
+      g.N = W;
+      g.K = nH * Dh;
+      g.splitk = p.s_o;
+      g.epi = EPI_RESID;
+      g.ep.h = c->h;
+      g.ep.gate = am + 2 * W;
+      ENQ(launch_gemm(c->dt, g, s));
+      // MLP
+      ENQ(launch_rmsnorm_mod(c->dt, c->h, mm, mm + W, c->y, M, W, eps, s));
+      g.A = c->y;
+      g.W = lay + c->off_gu * es;
+      g.N = 2 * F;
+      g.K = W;
+      g.splitk = p.s_gu;
+      g.epi = EPI_GEGLU;
+      g.ep.z = c->z;
+      g.ep.mlp_dim = F;
+      ENQ(launch_gemm(c->dt, g, s));
+      g.A = c->z;
+      g.W = lay + c->off_d * es;
+      g.N = W;
+      g.K = F;
+      g.splitk = p.s_d;
+      g.epi = EPI_RESID;
+      g.ep.h = c->h;
+      g.ep.gate = mm + 2 * W;
+      ENQ(launch_gemm(c->dt, g, s));
+    }
+    const float* fm = tk + (size_t)(6 * L) * W;
+    ENQ(launch_final_euler(c->dt, c->h, fm, fm + W, c->w_out, c->b_out, c->x, M, W, c->A, H, c->n_fixed, dt_step,
+                           eps, s));
+  }
+#undef ENQ
+  return hipSuccess;
+}
+
+bool eager_mode() {
+  const char* e = getenv("JPI_EAGER");
+  return e && e[0] == '1';
+}
+
+}  // namespace
+
+extern "C" {
+
+jpi_status jpi_denoise(jpi_ctx* c, const float* noise_dev, int n_steps, float* actions_dev, void* stream) {
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_denoise: ctx is NULL");
+  if (!noise_dev || !actions_dev) return fail(c, JPI_ERR_ARG, "jpi_denoise: noise or actions is NULL");
+  if (n_steps < 1) return fail(c, JPI_ERR_ARG, "jpi_denoise: n_steps must be >= 1");
+  if (!c->finalized) return fail(c, JPI_ERR_STATE, "jpi_denoise: weights are not finalized");
+  if (!c->prefix_bound) return fail(c, JPI_ERR_STATE, "jpi_denoise: no prefix bound");
+  HIPCHK(c, hipSetDevice(c->device));
+  hipStream_t s = (hipStream_t)stream;
+  float* table = nullptr;
+  TRY(ensure_table(c, n_steps, s, &table));
+  TRY(ensure_scratch(c, c->batch, c->prefix));
+  HIPCHK(c, launch_init_x(noise_dev, c->committed, c->x, c->batch, c->H, c->A, c->n_fixed, s));
+  if (eager_mode()) {
+    HIPCHK(c, enqueue_steps(c, table, n_steps, s));
+  } else {
+    const GraphKey key{c->batch, c->prefix, n_steps, c->n_fixed};
+    auto it = c->graphs.find(key);
+    if (it == c->graphs.end()) {
+      hipGraph_t graph = nullptr;
+      HIPCHK(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
+      hipError_t e = enqueue_steps(c, table, n_steps, c->cap_stream);
+      hipError_t e2 = hipStreamEndCapture(c->cap_stream, &graph);
+      if (e != hipSuccess || e2 != hipSuccess) {
+        if (graph) (void)hipGraphDestroy(graph);
+        (void)hipGetLastError();
+        return fail(c, JPI_ERR_HIP, std::string("graph capture: ") + hipGetErrorString(e != hipSuccess ? e : e2));
+      }
+      hipGraphExec_t exec = nullptr;
+      hipError_t e3 = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      if (e3 != hipSuccess) return fail(c, JPI_ERR_HIP, std::string("graph instantiate: ") + hipGetErrorString(e3));
+      it = c->graphs.emplace(key, exec).first;
+    }
+    HIPCHK(c, hipGraphLaunch(it->second, s));
+  }
+  HIPCHK(c, hipMemcpyAsync(actions_dev, c->x, (size_t)c->batch * c->H * c->A * sizeof(float),
+                           hipMemcpyDeviceToDevice, s));
+  return JPI_OK;
+}
+
+jpi_status jpi_sync(jpi_ctx* c, void* stream) {
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_sync: ctx is NULL");
+  HIPCHK(c, hipSetDevice(c->device));
+  HIPCHK(c, hipStreamSynchronize((hipStream_t)stream));
+  HIPCHK(c, hipGetLastError());
+  return JPI_OK;
+}
+
+jpi_status jpi_debug_gemm(const void* A, const void* Wt, float* C, int M, int N, int K, jpi_dtype dt, int splitk,
+                          void* stream) {
+  if (!A || !Wt || !C) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_gemm: NULL pointer");
+  if (M < 1 || N < 1 || K < 1 || splitk < 1) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_gemm: sizes must be >= 1");
+  if (dt != JPI_F32 && dt != JPI_BF16) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_gemm: bad dtype");
+  const int BK = dt == JPI_BF16 ? 64 : 32;
+  if (K % (BK * splitk) != 0)
+    return fail(nullptr, JPI_ERR_ARG, "jpi_debug_gemm: K must be a multiple of " + std::to_string(BK) + "*splitk");
+  hipStream_t s = (hipStream_t)stream;
+  GemmLaunch g{};
+  g.A = A;
+  g.W = Wt;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.splitk = splitk;
+  g.epi = EPI_STORE_F32;
+  g.ep.out_f32 = C;
+  const size_t tiles = gemm_tiles(dt, M, N);
+  hipError_t ea = hipMalloc((void**)&g.counters, tiles * sizeof(unsigned));
+  if (ea != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(nullptr, ea == hipErrorOutOfMemory ? JPI_ERR_OOM : JPI_ERR_HIP,
+                std::string("jpi_debug_gemm: counters: ") + hipGetErrorString(ea));
+  }
+  hipError_t e = hipMemsetAsync(g.counters, 0, tiles * sizeof(unsigned), s);
+  if (e == hipSuccess && splitk > 1) e = hipMalloc((void**)&g.partial, (size_t)splitk * M * N * sizeof(float));
+  if (e == hipSuccess) e = launch_gemm(dt, g, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (g.partial) (void)hipFree(g.partial);
+  (void)hipFree(g.counters);
+  if (e != hipSuccess) return fail(nullptr, JPI_ERR_HIP, std::string("jpi_debug_gemm: ") + hipGetErrorString(e));
+  return JPI_OK;
+}
+
+jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, const void* kp, const void* vp,
+                               const int32_t* prefix_len_host, int batch, int n_heads, int H, int P, int Dh,
+                               jpi_dtype dt, float* out, void* stream) {
+  if (!q || !ks || !vs || !out || !prefix_len_host || ((!kp || !vp) && P > 0))
+    return fail(nullptr, JPI_ERR_ARG, "jpi_debug_attention: NULL pointer");
+  if (batch < 1 || n_heads < 1 || H < 1 || P < 0 || (Dh != 64 && Dh != 128 && Dh != 256))
+    return fail(nullptr, JPI_ERR_ARG, "jpi_debug_attention: bad sizes");
+  if (dt != JPI_F32 && dt != JPI_BF16) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_attention: bad dtype");
+  for (int b = 0; b < batch; ++b)
+    if (prefix_len_host[b] < 0 || prefix_len_host[b] > P)
+      return fail(nullptr, JPI_ERR_ARG, "jpi_debug_attention: prefix_len out of range");
+  hipStream_t s = (hipStream_t)stream;
+  const int nch = attn_n_chunks(dt, P, H);
+  int* dlen = nullptr;
+  float* part = nullptr;
+  const size_t np = (size_t)batch * n_heads * nch * H * (Dh + 2);
+  hipError_t ea = hipMalloc((void**)&dlen, batch * sizeof(int));
+  if (ea == hipSuccess) ea = hipMalloc((void**)&part, np * sizeof(float));
+  if (ea != hipSuccess) {
+    (void)hipGetLastError();
+    if (dlen) (void)hipFree(dlen);
+    return fail(nullptr, ea == hipErrorOutOfMemory ? JPI_ERR_OOM : JPI_ERR_HIP,
+                std::string("jpi_debug_attention: scratch: ") + hipGetErrorString(ea));
+  }
+  AttnLaunch a{};
+  a.q = q;
+  a.ks = ks;
+  a.vs = vs;
+  a.kp = kp ? kp : ks;
+  a.vp = vp ? vp : vs;
+  a.kp_bstride = (int64_t)P * Dh;
+  a.prefix_len = dlen;
+  a.B = batch;
+  a.nH = n_heads;
+  a.H = H;
+  a.P = P;
+  a.Dh = Dh;
+  a.opart = part;
+  a.mpart = part + (size_t)batch * n_heads * nch * H * Dh;
+  a.lpart = a.mpart + (size_t)batch * n_heads * nch * H;
+  a.out = out;
+  a.out_f32 = 1;
+  hipError_t e = hipMemcpyAsync(dlen, prefix_len_host, batch * sizeof(int), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = launch_attention(dt, a, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  (void)hipFree(dlen);
+  (void)hipFree(part);
+  if (e != hipSuccess) return fail(nullptr, JPI_ERR_HIP, std::string("jpi_debug_attention: ") + hipGetErrorString(e));
+  return JPI_OK;
+}
+
+}  // extern "C"

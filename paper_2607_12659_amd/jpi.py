@@ -1,0 +1,172 @@
+"""ctypes binding of libjpi (include/jpi.h).
+
+Argument marshalling only: every function here has the name of the C entry
+point it calls and forwards plain pointers and sizes.  Tensors may be given
+as torch tensors (device memory), numpy arrays (host memory) or raw integer
+addresses; streams as torch.cuda.Stream objects, raw hipStream_t integers or
+None (the null stream).  There is no fallback: if libjpi.so is missing the
+import of this module fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libjpi.so")
+
+JPI_OK, JPI_ERR_ARG, JPI_ERR_SHAPE, JPI_ERR_DTYPE, JPI_ERR_STATE, JPI_ERR_OOM, JPI_ERR_HIP, JPI_ERR_UNSUPPORTED = range(8)
+JPI_F32, JPI_BF16 = 0, 1
+
+EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create", "jpi_destroy", "jpi_set_weight",
+            "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
+            "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention"]
+
+
+class jpi_config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int), ("width", ctypes.c_int), ("n_heads", ctypes.c_int),
+                ("n_kv_heads", ctypes.c_int), ("head_dim", ctypes.c_int), ("mlp_dim", ctypes.c_int),
+                ("action_dim", ctypes.c_int), ("horizon", ctypes.c_int), ("max_batch", ctypes.c_int),
+                ("max_prefix", ctypes.c_int), ("dtype", ctypes.c_int), ("rms_eps", ctypes.c_float),
+                ("rope_base", ctypes.c_float)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libjpi.so is not built (run paper_2607_12659_amd/build.py); there is no fallback path")
+# PyTorch-ROCm bundles its own HIP runtime (SONAME libamdhip64.so.7).  Map it
+# before libjpi so that libjpi's dependency resolves to that same copy: two
+# HIP runtimes in one process do not share devices, memory or streams.
+try:
+    import torch  # noqa: F401
+except ImportError:
+    pass
+_lib = ctypes.CDLL(LIB_PATH)
+
+_vp, _i, _i64, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float
+_sig = {
+    "jpi_abi_version": (_i, []),
+    "jpi_status_str": (ctypes.c_char_p, [_i]),
+    "jpi_last_error": (ctypes.c_char_p, [_vp]),
+    "jpi_create": (_i, [ctypes.POINTER(jpi_config), _i, ctypes.POINTER(_vp)]),
+    "jpi_destroy": (_i, [_vp]),
+    "jpi_set_weight": (_i, [_vp, ctypes.c_char_p, _vp, _i64, _i, _i, _vp]),
+    "jpi_finalize_weights": (_i, [_vp, _vp]),
+    "jpi_prefix_buffers": (_i, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp)]),
+    "jpi_bind_prefix": (_i, [_vp, _vp, _vp, _vp, _i, _i, _vp]),
+    "jpi_bind_state": (_i, [_vp, _vp, _i, _vp, _i, _vp]),
+    "jpi_denoise": (_i, [_vp, _vp, _i, _vp, _vp]),
+    "jpi_sync": (_i, [_vp, _vp]),
+    "jpi_debug_gemm": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "jpi_debug_attention": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
+}
+for _name, (_res, _args) in _sig.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+
+def addr(t) -> int | None:
+    """Address of a torch tensor / numpy array / int / None."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if hasattr(t, "data_ptr"):
+        return t.data_ptr()
+    if hasattr(t, "ctypes"):
+        return t.ctypes.data
+    raise TypeError("cannot take the address of %r" % type(t))
+
+
+def stream_handle(s) -> int | None:
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _i32_host(a):
+    if a is None:
+        return None
+    import numpy as np
+    arr = np.ascontiguousarray(a, dtype=np.int32)
+    return arr
+
+
+# ---------------------------------------------------------------------------
+# same-named wrappers (return the jpi_status, plus outputs where the C call has them)
+# ---------------------------------------------------------------------------
+def jpi_abi_version() -> int:
+    return _lib.jpi_abi_version()
+
+
+def jpi_status_str(status: int) -> str:
+    return _lib.jpi_status_str(status).decode()
+
+
+def jpi_last_error(ctx) -> str:
+    return _lib.jpi_last_error(ctx).decode()
+
+
+def jpi_create(cfg: jpi_config, device: int = 0):
+    out = _vp()
+    st = _lib.jpi_create(ctypes.byref(cfg), device, ctypes.byref(out))
+    return st, out.value
+
+
+def jpi_destroy(ctx) -> int:
+    return _lib.jpi_destroy(ctx)
+
+
+def jpi_set_weight(ctx, name: str, data, n_elems: int, dtype: int, is_device: int, stream=None) -> int:
+    return _lib.jpi_set_weight(ctx, name.encode(), addr(data), n_elems, dtype, is_device, stream_handle(stream))
+
+
+def jpi_finalize_weights(ctx, stream=None) -> int:
+    return _lib.jpi_finalize_weights(ctx, stream_handle(stream))
+
+
+def jpi_prefix_buffers(ctx):
+    k, v = _vp(), _vp()
+    st = _lib.jpi_prefix_buffers(ctx, ctypes.byref(k), ctypes.byref(v))
+    return st, k.value, v.value
+
+
+def jpi_bind_prefix(ctx, k, v, prefix_len_host, batch: int, prefix: int, stream=None) -> int:
+    lens = _i32_host(prefix_len_host)
+    return _lib.jpi_bind_prefix(ctx, addr(k), addr(v), None if lens is None else lens.ctypes.data, batch, prefix,
+                                stream_handle(stream))
+
+
+def jpi_bind_state(ctx, committed_dev, n_fixed: int, corr_tokens=None, n_corr: int = 0, stream=None) -> int:
+    return _lib.jpi_bind_state(ctx, addr(committed_dev), n_fixed, addr(corr_tokens), n_corr, stream_handle(stream))
+
+
+def jpi_denoise(ctx, noise_dev, n_steps: int, actions_dev, stream=None) -> int:
+    return _lib.jpi_denoise(ctx, addr(noise_dev), n_steps, addr(actions_dev), stream_handle(stream))
+
+
+def jpi_sync(ctx, stream=None) -> int:
+    return _lib.jpi_sync(ctx, stream_handle(stream))
+
+
+def jpi_debug_gemm(A, W, C, M: int, N: int, K: int, dtype: int, splitk: int = 1, stream=None) -> int:
+    return _lib.jpi_debug_gemm(addr(A), addr(W), addr(C), M, N, K, dtype, splitk, stream_handle(stream))
+
+
+def jpi_debug_attention(q, ks, vs, kp, vp, prefix_len_host, batch, n_heads, H, P, Dh, dtype, out, stream=None) -> int:
+    lens = _i32_host(prefix_len_host)
+    return _lib.jpi_debug_attention(addr(q), addr(ks), addr(vs), addr(kp), addr(vp), lens.ctypes.data, batch, n_heads,
+                                    H, P, Dh, dtype, addr(out), stream_handle(stream))
+
+
+class JpiError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("%s: %s" % (jpi_status_str(status), msg))
+        self.status = status
+
+
+def check(status: int, ctx=None):
+    if status != JPI_OK:
+        raise JpiError(status, jpi_last_error(ctx))

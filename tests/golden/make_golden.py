@@ -1,0 +1,85 @@
+"""Write the oracle's outputs for the large workloads to tests/golden/.
+
+Calls only the CPU oracle and the seeded input generator.  Each output file
+``<name>.npy`` holds the fp64 actions [rollouts][H][A]; ``<name>.json`` records
+how it was made (workload, rollouts, seed, n_steps, dtype, sha256 of the
+oracle source and of the generator source at generation time).
+
+    python tests/golden/make_golden.py [name ...]
+"""
+from __future__ import annotations
+
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+sys.path.insert(0, ROOT)
+
+import oracle  # noqa: E402
+import synth  # noqa: E402
+
+# name -> (workload key, overrides, rollouts evaluated)
+CASES = {
+    "pi05-b1": ("pi05-b1", {}, None),
+    "pi05-b1-committed10": ("pi05-b1-committed10", {}, None),
+    "pi05-b8": ("pi05-b8", {}, None),
+    "pi05-b64-p1600.r0_31_63": ("pi05-b64-p1600", {}, [0, 31, 63]),
+    # not a benchmark workload: the pi0.5 shape in fp32, checked at 1e-4 so that
+    # attention or norm mistakes cannot hide inside the bf16 tolerance
+    "pi05-f32-b1": ("pi05-b1", {"dtype": "f32", "name": "pi05-f32-b1"}, None),
+    # ragged prefix lengths (masked slots) over two rollouts
+    "pi05-b2-ragged": ("pi05-b8", {"batch": 2, "prefix_len": (816, 301), "name": "pi05-b2-ragged"}, None),
+}
+
+
+def source_hash(*paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def workload(name):
+    key, over, rollouts = CASES[name]
+    return synth.WORKLOADS[key].with_(**over), rollouts
+
+
+def make(name):
+    wl, rollouts = workload(name)
+    rl = list(range(wl.batch)) if rollouts is None else rollouts
+    t0 = time.time()
+    w = synth.make_weights(wl)
+    K, V = synth.make_prefix(wl, rl)
+    noise = synth.make_noise(wl, rl)
+    com = synth.make_committed(wl, rl) if wl.n_fixed else None
+    lens = [wl.valid_lengths()[b] for b in rl]
+    ex = oracle.Expert(wl.dims, w)
+    t1 = time.time()
+    out = oracle.denoise(ex, noise, K, V, lens, wl.n_steps, committed=com, n_fixed=wl.n_fixed)
+    t2 = time.time()
+    np.save(os.path.join(HERE, name + ".npy"), out, allow_pickle=False)
+    meta = {"workload": wl.name, "base_workload": CASES[name][0], "overrides": {k: list(v) if isinstance(v, tuple) else v
+                                                                             for k, v in CASES[name][1].items()},
+            "rollouts": rl, "seed": wl.seed, "n_steps": wl.n_steps, "n_fixed": wl.n_fixed, "dtype": wl.dtype,
+            "prefix": wl.prefix, "prefix_len": lens,
+            "oracle_sha256": source_hash(os.path.join(ROOT, "oracle", "actionexpert.py")),
+            "synth_sha256": source_hash(os.path.join(ROOT, "synth", "synth.c"),
+                                        os.path.join(ROOT, "synth", "__init__.py")),
+            "oracle_seconds": round(t2 - t1, 2), "setup_seconds": round(t1 - t0, 2),
+            "made_by": "tests/golden/make_golden.py (oracle + synth only)"}
+    with open(os.path.join(HERE, name + ".json"), "w") as f:
+        json.dump(meta, f, indent=1)
+    print("%s: oracle %.1fs setup %.1fs" % (name, t2 - t1, t1 - t0), flush=True)
+
+
+if __name__ == "__main__":
+    names = sys.argv[1:] or list(CASES)
+    for n in names:
+        make(n)

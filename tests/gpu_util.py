@@ -1,0 +1,64 @@
+"""Helpers shared by the GPU tests: run a workload through the C ABI."""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        import pytest
+        pytest.skip("no GPU")
+    return torch
+
+
+class Inputs:
+    """Seeded inputs of a workload (host arrays)."""
+
+    def __init__(self, wl, rollouts=None):
+        self.wl = wl
+        self.rollouts = list(range(wl.batch)) if rollouts is None else list(rollouts)
+        self.weights = synth.make_weights(wl)
+        self.K, self.V = synth.make_prefix(wl, self.rollouts)
+        self.noise = synth.make_noise(wl, self.rollouts)
+        self.committed = synth.make_committed(wl, self.rollouts) if wl.n_fixed else None
+        self.prefix_len = [wl.valid_lengths()[b] for b in self.rollouts]
+
+
+def make_expert(wl, weights, max_batch=None, max_prefix=None):
+    from paper_2607_12659_amd.expert import ActionExpert
+    ae = ActionExpert(wl.dims, wl.dtype, max_batch or wl.batch, max_prefix if max_prefix is not None else wl.prefix)
+    ae.load_weights(weights)
+    return ae
+
+
+def run(ae, K, V, noise, n_steps, prefix_len=None, committed=None, n_fixed=0):
+    """Bind and denoise; returns fp64 host actions."""
+    torch = torch_cuda()
+    from paper_2607_12659_amd.expert import to_device
+    ae.bind_prefix(to_device(K), to_device(V), prefix_len)
+    ae.bind_state(None if committed is None else to_device(np.ascontiguousarray(committed, np.float32)), n_fixed)
+    out = ae.denoise(to_device(np.ascontiguousarray(noise, np.float32)), n_steps)
+    ae.sync()
+    torch.cuda.synchronize()
+    return out.cpu().numpy().astype(np.float64)
+
+
+def load_golden(name):
+    with open(os.path.join(GOLDEN, name + ".json")) as f:
+        meta = json.load(f)
+    return np.load(os.path.join(GOLDEN, name + ".npy"), allow_pickle=False), meta
+
+
+def rel_l2_per_rollout(got, ref):
+    """max over rollouts of ||got_b - ref_b||_2 / ||ref_b||_2."""
+    num = np.sqrt(((got - ref) ** 2).reshape(got.shape[0], -1).sum(1))
+    den = np.sqrt((ref ** 2).reshape(ref.shape[0], -1).sum(1))
+    return float((num / den).max())

@@ -1,0 +1,227 @@
+"""End-to-end parity of jpi_denoise with the fp64 oracle, plus invariants of
+the GPU path.
+
+Bars: fp32 path max-abs <= 1e-4 on every output element; bf16 path (bf16
+weights and prefix KV, fp32 accumulation) per-rollout relative L2 error
+<= 2e-2 on the final actions.  Large workloads compare with oracle outputs
+stored by tests/golden/make_golden.py (oracle + generator only).
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import Inputs, load_golden, make_expert, rel_l2_per_rollout, run, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-2
+F32_TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    wl = synth.WORKLOADS["tiny-fp32"]
+    inp = Inputs(wl)
+    ae = make_expert(wl, inp.weights, max_batch=4, max_prefix=wl.prefix)
+    yield wl, inp, ae
+    ae.close()
+
+
+def _oracle(wl, inp, n_steps=None, lens=None, noise=None, committed=None, n_fixed=0, K=None, V=None):
+    ex = oracle.Expert(wl.dims, inp.weights)
+    return oracle.denoise(ex, inp.noise if noise is None else noise, inp.K if K is None else K,
+                          inp.V if V is None else V, inp.prefix_len if lens is None else lens,
+                          n_steps or wl.n_steps, committed=committed, n_fixed=n_fixed)
+
+
+def test_tiny_fp32_matches_oracle(tiny):
+    wl, inp, ae = tiny
+    print("case tiny-fp32", flush=True)
+    got = run(ae, inp.K, inp.V, inp.noise, wl.n_steps)
+    ref = _oracle(wl, inp)
+    err = np.abs(got - ref).max()
+    print("tiny-fp32 max-abs %.3e" % err)
+    assert err <= F32_TOL
+
+
+@pytest.mark.parametrize("n_steps", [1, 2, 7])
+def test_tiny_fp32_step_counts(tiny, n_steps):
+    wl, inp, ae = tiny
+    got = run(ae, inp.K, inp.V, inp.noise, n_steps)
+    assert np.abs(got - _oracle(wl, inp, n_steps=n_steps)).max() <= F32_TOL
+
+
+def test_tiny_n_steps_1_is_noise_minus_velocity(tiny):
+    wl, inp, ae = tiny
+    got = run(ae, inp.K, inp.V, inp.noise, 1)
+    v = oracle.velocity(oracle.Expert(wl.dims, inp.weights), inp.noise.astype(np.float64), 1.0, inp.K, inp.V,
+                        inp.prefix_len)
+    assert np.abs(got - (inp.noise - v)).max() <= F32_TOL
+
+
+def test_tiny_batched_ragged_prefix_and_committed(tiny):
+    wl, inp, ae = tiny
+    wl4 = wl.with_(batch=3, n_fixed=3, prefix_len=(64, 0, 23))
+    i4 = Inputs(wl4)
+    got = run(ae, i4.K, i4.V, i4.noise, wl.n_steps, prefix_len=i4.prefix_len, committed=i4.committed, n_fixed=3)
+    ref = _oracle(wl4, i4, committed=i4.committed, n_fixed=3)
+    assert np.abs(got - ref).max() <= F32_TOL
+    assert np.array_equal(got[:, :3].astype(np.float32), i4.committed.astype(np.float32))
+
+
+def test_tiny_masked_garbage_invariance(tiny):
+    wl, inp, ae = tiny
+    lens = [40]
+    a = run(ae, inp.K, inp.V, inp.noise, wl.n_steps, prefix_len=lens)
+    K, V = inp.K.copy(), inp.V.copy()
+    K[:, 0, 40:] = np.nan
+    V[:, 0, 40:] = np.inf
+    b = run(ae, K, V, inp.noise, wl.n_steps, prefix_len=lens)
+    assert not np.isnan(b).any() and np.array_equal(a, b)
+    assert np.abs(a - _oracle(wl, inp, lens=lens)).max() <= F32_TOL
+
+
+def test_tiny_prefix_permutation_invariance(tiny):
+    wl, inp, ae = tiny
+    a = run(ae, inp.K, inp.V, inp.noise, wl.n_steps)
+    perm = np.random.default_rng(0).permutation(wl.prefix)
+    b = run(ae, inp.K[:, :, perm], inp.V[:, :, perm], inp.noise, wl.n_steps)
+    assert np.abs(a - b).max() <= 1e-5
+
+
+def test_tiny_graph_replay_matches_eager_bitwise(tiny):
+    wl, inp, ae = tiny
+    os.environ.pop("JPI_EAGER", None)
+    g1 = run(ae, inp.K, inp.V, inp.noise, wl.n_steps)
+    g2 = run(ae, inp.K, inp.V, inp.noise, wl.n_steps)
+    os.environ["JPI_EAGER"] = "1"
+    try:
+        e = run(ae, inp.K, inp.V, inp.noise, wl.n_steps)
+    finally:
+        os.environ.pop("JPI_EAGER", None)
+    assert np.array_equal(g1, g2) and np.array_equal(g1, e)
+
+
+def test_tiny_constant_velocity_field():
+    wl = synth.WORKLOADS["tiny-fp32"]
+    inp = Inputs(wl)
+    w = dict(inp.weights)
+    w["action_out.w"] = np.zeros_like(w["action_out.w"])
+    c = np.linspace(-1, 1, wl.dims.action_dim).astype(np.float32)
+    w["action_out.b"] = c
+    ae = make_expert(wl, w)
+    try:
+        got = run(ae, inp.K, inp.V, inp.noise, 5)
+    finally:
+        ae.close()
+    np.testing.assert_allclose(got, inp.noise - c.astype(np.float64), atol=2e-6, rtol=0)
+
+
+# ---------------------------------------------------------------------------
+# pi0.5-shape workloads against stored oracle outputs
+# ---------------------------------------------------------------------------
+@pytest.fixture(scope="module")
+def pi05():
+    torch_cuda()
+    wl = synth.WORKLOADS["pi05-b8"]
+    print("generating pi0.5 weights", flush=True)
+    w = synth.make_weights(wl)
+    ae = make_expert(wl, w, max_batch=8, max_prefix=816)
+    yield w, ae
+    ae.close()
+
+
+def _check_bf16(name, got):
+    ref, meta = load_golden(name)
+    rel = rel_l2_per_rollout(got, ref)
+    print("%s: rel-L2 %.3e max-abs %.3e" % (name, rel, np.abs(got - ref).max()), flush=True)
+    assert rel <= BF16_TOL
+    return ref
+
+
+def test_pi05_b1(pi05):
+    w, ae = pi05
+    wl = synth.WORKLOADS["pi05-b1"]
+    print("case pi05-b1", flush=True)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    got = run(ae, K, V, noise, wl.n_steps)
+    _check_bf16("pi05-b1", got)
+    # sensitivity: scaling the prefix V moves the actions far beyond the tolerance
+    got2 = run(ae, K, synth.f32_to_bf16_bits(synth.bf16_bits_to_f32(V) * 1.5), noise, wl.n_steps)
+    ref, _ = load_golden("pi05-b1")
+    assert rel_l2_per_rollout(got2, ref) > 5 * BF16_TOL
+    # replay determinism
+    assert np.array_equal(got, run(ae, K, V, noise, wl.n_steps))
+
+
+def test_pi05_b1_committed10(pi05):
+    w, ae = pi05
+    wl = synth.WORKLOADS["pi05-b1-committed10"]
+    print("case pi05-b1-committed10", flush=True)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    com = synth.make_committed(wl)
+    got = run(ae, K, V, noise, wl.n_steps, committed=com, n_fixed=wl.n_fixed)
+    _check_bf16("pi05-b1-committed10", got)
+    assert np.array_equal(got[:, :10].astype(np.float32), com)
+
+
+def test_pi05_b8_and_rollout_independence(pi05):
+    w, ae = pi05
+    wl = synth.WORKLOADS["pi05-b8"]
+    print("case pi05-b8", flush=True)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    got = run(ae, K, V, noise, wl.n_steps)
+    _check_bf16("pi05-b8", got)
+    ref1, _ = load_golden("pi05-b1")
+    # rollout 0 of the batch-8 workload is the batch-1 workload (shared seeds)
+    assert rel_l2_per_rollout(got[:1], ref1) <= BF16_TOL
+
+
+def test_pi05_ragged_prefix(pi05):
+    w, ae = pi05
+    ref, meta = load_golden("pi05-b2-ragged")
+    wl = synth.WORKLOADS["pi05-b8"].with_(batch=2, prefix_len=tuple(meta["prefix_len"]))
+    print("case pi05-b2-ragged", flush=True)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    got = run(ae, K, V, noise, wl.n_steps, prefix_len=meta["prefix_len"])
+    _check_bf16("pi05-b2-ragged", got)
+
+
+def test_pi05_b64_p1600_sampled_rollouts():
+    torch_cuda()
+    ref, meta = load_golden("pi05-b64-p1600.r0_31_63")
+    wl = synth.WORKLOADS["pi05-b64-p1600"]
+    print("case pi05-b64-p1600 (full batch on GPU, rollouts %s checked)" % meta["rollouts"], flush=True)
+    w = synth.make_weights(wl)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    ae = make_expert(wl, w)
+    try:
+        got = run(ae, K, V, noise, wl.n_steps)
+    finally:
+        ae.close()
+    assert np.isfinite(got).all()
+    _check_bf16("pi05-b64-p1600.r0_31_63", got[meta["rollouts"]])
+
+
+def test_pi05_fp32_shape_at_1e4():
+    torch_cuda()
+    ref, meta = load_golden("pi05-f32-b1")
+    wl = synth.WORKLOADS["pi05-b1"].with_(dtype="f32", name="pi05-f32-b1")
+    print("case pi05-f32-b1", flush=True)
+    inp = Inputs(wl)
+    ae = make_expert(wl, inp.weights)
+    try:
+        got = run(ae, inp.K, inp.V, inp.noise, wl.n_steps)
+    finally:
+        ae.close()
+    err = np.abs(got - ref).max()
+    print("pi05-f32-b1 max-abs %.3e" % err, flush=True)
+    assert err <= F32_TOL
