@@ -1,0 +1,226 @@
+"""Benchmark of the flow-matching action-expert denoise on one MI355X.
+
+One "step" of this benchmark is one jpi_denoise call: the whole hot path
+(n_steps Euler steps of the action expert over one action chunk per rollout,
+every layer attending to the resident prefix KV), on inputs already resident
+in HBM.  Prints one JSON line:
+
+  value      action chunks/s = batch * steps / timed seconds
+  roofline   the dominant weight-streaming kernel's algorithmic bytes per
+             launch / its average launch duration (start/stop HIP events tied
+             to every dispatch of that kernel on the stream it runs on, in a
+             timing pass right after the timed region), against MI355X's
+             8 TB/s HBM peak; "kernels" gives the same for every kernel kind
+  cpu_baseline  the fp64 CPU oracle timed on the host cores on one denoise call
+                of rollout 0 (a bounded sample)
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roofline"
+
+
+def algorithmic_counts(wl):
+    """Bytes and flops one denoise call must move / compute.
+
+    Weights are read once per Euler step (shared by the batch); each rollout's
+    valid prefix KV once per step; the modulation rows used per step are
+    counted; activations (cache-resident) and the once-per-(weights, N) time
+    MLP / modulation precompute are not.
+    """
+    d = wl.dims
+    es = 2 if wl.dtype == "bf16" else 4
+    W, F, Dh, nH, A, L, H = d.width, d.mlp_dim, d.head_dim, d.n_heads, d.action_dim, d.n_layers, d.horizon
+    per_layer = {"qkv": (nH + 2) * Dh * W, "oproj": W * nH * Dh, "gateup": 2 * F * W, "down": W * F}
+    w_layer = sum(per_layer.values()) * es
+    w_step = L * w_layer + (2 * W * A) * es
+    kv_step = sum(2 * L * pl * Dh * es for pl in wl.valid_lengths())
+    mod_step = (6 * L + 2) * W * 4
+    M = wl.batch * H
+    keys = [pl + H for pl in wl.valid_lengths()]
+    gemm_flops = 2 * M * (L * sum(per_layer.values()) + 2 * W * A)
+    attn_flops = sum(4 * L * nH * H * k * Dh for k in keys)
+    return {
+        "bytes_per_call": (w_step + kv_step + mod_step) * wl.n_steps,
+        "flops_per_call": (gemm_flops + attn_flops) * wl.n_steps,
+        "kernel_bytes": {k: v * es for k, v in per_layer.items()},
+        "kernel_flops": {k: 2 * M * v for k, v in per_layer.items()},
+    }
+
+
+def cpu_baseline(wl, weights, K, V, noise):
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    ex = oracle.Expert(wl.dims, weights)
+    lens = wl.valid_lengths()[:1]
+    t0 = time.perf_counter()
+    oracle.denoise(ex, noise[:1], K[:, :1], V[:, :1], lens, wl.n_steps)
+    dt = time.perf_counter() - t0
+    return {"value": round(1.0 / dt, 4), "unit": "chunks/s", "cores": int(threads), "kind": "oracle",
+            "sample": "one %d-step denoise of rollout 0 of %s (fp64 numpy, BLAS threads=%d), %.1f s"
+                      % (wl.n_steps, wl.name, threads, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="pi05-b1")
+    ap.add_argument("--timed-kernel", default="gateup", choices=["qkv", "attention", "oproj", "gateup", "down"])
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the denoise of one chunk runs on "
+              "one MI355X; rollouts would shard data-parallel with no exchange). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2607_12659_amd import jpi
+    from paper_2607_12659_amd.expert import ActionExpert, to_device
+
+    wl = synth.WORKLOADS[args.workload]
+    print("bench: workload %s, generating inputs" % wl.name, file=sys.stderr, flush=True)
+    weights = synth.make_weights(wl)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    committed = synth.make_committed(wl) if wl.n_fixed else None
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    ae = ActionExpert(wl.dims, wl.dtype, wl.batch, wl.prefix)
+    ae.load_weights(weights)
+    Kd, Vd = to_device(K), to_device(V)
+    ae.bind_prefix(Kd, Vd, wl.valid_lengths(), stream=stream)
+    ae.bind_state(None if committed is None else to_device(committed), wl.n_fixed, stream=stream)
+    noise_d = to_device(noise)
+    out = torch.empty_like(noise_d)
+    torch.cuda.synchronize()
+
+    # first call: modulation tables + graph capture + one replay
+    t0 = time.perf_counter()
+    ae.denoise(noise_d, wl.n_steps, out, stream=stream)
+    torch.cuda.synchronize()
+    first_ms = (time.perf_counter() - t0) * 1e3
+    print("bench: first call %.1f ms (tables + capture)" % first_ms, file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        ae.denoise(noise_d, wl.n_steps, out, stream=stream)
+    torch.cuda.synchronize()
+
+    # timed region
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    per_call = []
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(args.steps):
+        evs[i][0].record(stream)
+        ae.denoise(noise_d, wl.n_steps, out, stream=stream)
+        evs[i][1].record(stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = ev0.elapsed_time(ev1)
+    per_call = sorted(a.elapsed_time(b) for a, b in evs)
+    ms_per_call = total_ms / args.steps
+    value = wl.batch * args.steps / (total_ms / 1e3)
+    print("bench: %.3f ms per call (median %.3f, p10 %.3f, p90 %.3f)"
+          % (ms_per_call, per_call[len(per_call) // 2], per_call[len(per_call) // 10],
+             per_call[(9 * len(per_call)) // 10]), file=sys.stderr, flush=True)
+
+    counts = algorithmic_counts(wl)
+    # timing pass: start/stop events on the dispatch of every launch of one kernel kind
+    kinds = {"qkv": jpi.JPI_KERNEL_QKV, "attention": jpi.JPI_KERNEL_ATTENTION, "oproj": jpi.JPI_KERNEL_OPROJ,
+             "gateup": jpi.JPI_KERNEL_GATEUP, "down": jpi.JPI_KERNEL_DOWN}
+    per_kind = {}
+    reps = max(3, min(args.steps, 10))
+    for kname, kind in kinds.items():
+        jpi.check(jpi.jpi_debug_time_kernel(ae.ctx, kind), ae.ctx)
+        tot_ms, tot_n = 0.0, 0
+        for i in range(reps + 1):
+            ae.denoise(noise_d, wl.n_steps, out, stream=stream)
+            torch.cuda.synchronize()
+            st, ms, n = jpi.jpi_debug_kernel_time(ae.ctx)
+            jpi.check(st, ae.ctx)
+            if i > 0:  # the first call warms the eager path
+                tot_ms += ms
+                tot_n += n
+        avg_us = tot_ms / tot_n * 1e3
+        entry = {"avg_us": round(avg_us, 3), "launches": tot_n,
+                 "share_of_call": round(tot_ms / reps / ms_per_call, 4)}
+        if kname in counts["kernel_bytes"]:
+            entry["GBs"] = round(counts["kernel_bytes"][kname] / (avg_us * 1e-6) / 1e9, 1)
+        per_kind[kname] = entry
+    jpi.check(jpi.jpi_debug_time_kernel(ae.ctx, jpi.JPI_KERNEL_NONE), ae.ctx)
+    kname = args.timed_kernel
+    k_avg_us = per_kind[kname]["avg_us"]
+    tot_n = per_kind[kname]["launches"]
+    kbytes = counts["kernel_bytes"][kname]
+    achieved = kbytes / (k_avg_us * 1e-6) / 1e9
+    print("bench: per-kernel %s" % json.dumps(per_kind), file=sys.stderr, flush=True)
+
+    call_gbs = counts["bytes_per_call"] / (ms_per_call * 1e-3) / 1e9
+    call_tflops = counts["flops_per_call"] / (ms_per_call * 1e-3) / 1e12
+    mfma_peak = BF16_MFMA_PEAK_TFLOPS if wl.dtype == "bf16" else FP32_MFMA_PEAK_TFLOPS
+    result = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "chunks/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_call, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "prefix_tokens": wl.prefix, "horizon": wl.dims.horizon,
+                   "action_dim": wl.dims.action_dim, "euler_steps": wl.n_steps, "layers": wl.dims.n_layers,
+                   "width": wl.dims.width, "heads": wl.dims.n_heads, "kv_heads": wl.dims.n_kv_heads,
+                   "head_dim": wl.dims.head_dim, "mlp_dim": wl.dims.mlp_dim, "n_fixed": wl.n_fixed,
+                   "seed": wl.seed},
+        "per_euler_step_us": round(ms_per_call / wl.n_steps * 1e3, 2),
+        "first_call_ms": round(first_ms, 2),
+        "roofline": {"bound": "hbm", "kernel": "k_gemm (%s)" % kname, "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": kbytes, "avg_launch_us": round(k_avg_us, 3),
+                     "launches_timed": tot_n},
+        "kernels": per_kind,
+        "call_roofline": {"algorithmic_bytes": counts["bytes_per_call"], "achieved_GBs": round(call_gbs, 1),
+                          "hbm_frac": round(call_gbs / HBM_PEAK_GBS, 4),
+                          "algorithmic_flops": counts["flops_per_call"], "achieved_TFLOPs": round(call_tflops, 2),
+                          "mfma_frac": round(call_tflops / mfma_peak, 4)},
+    }
+    ae.close()
+    if not args.no_cpu:
+        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(wl, weights, K, V, noise)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

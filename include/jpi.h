@@ -186,6 +186,28 @@ jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, co
                                const int32_t* prefix_len_host, int batch, int n_heads, int H, int P,
                                int Dh, jpi_dtype dt, float* out, void* stream);
 
+/* ---- measurement support (used by the benchmark) ---------------------------- */
+
+/* Kernel kinds of one denoise step, in launch order per layer. */
+typedef enum {
+  JPI_KERNEL_NONE = -1,
+  JPI_KERNEL_QKV = 0,        /* adaRMSNorm'd activations x [q|k|v] weights, RoPE epilogue */
+  JPI_KERNEL_ATTENTION = 1,  /* prefix+self attention (chunk pass and combine) */
+  JPI_KERNEL_OPROJ = 2,      /* attention output x W_o, gated residual */
+  JPI_KERNEL_GATEUP = 3,     /* activations x [gate|up], GeGLU epilogue */
+  JPI_KERNEL_DOWN = 4        /* GeGLU output x W_down, gated residual */
+} jpi_kernel_kind;
+
+/* Ask jpi_denoise to record a pair of HIP events around every launch of
+ * `kind` (JPI_KERNEL_NONE switches it off).  While it is on, jpi_denoise
+ * enqueues the same kernels directly on the stream instead of replaying the
+ * captured graph (events recorded inside a graph cannot be timed). */
+jpi_status jpi_debug_time_kernel(jpi_ctx* ctx, int kind);
+
+/* After the stream of the last jpi_denoise has been synchronised: the sum of
+ * the recorded launch durations (ms) and the number of launches. */
+jpi_status jpi_debug_kernel_time(jpi_ctx* ctx, float* total_ms, int* launches);
+
 #ifdef __cplusplus
 }
 #endif

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <hip/hip_ext.h>
+
 #include "../../include/jpi.h"
 
 namespace jpi {
@@ -15,58 +17,69 @@ typedef __bf16 bf16;
 // acc[m][n] = sum_k A[m][k] W[n][k] (fp32) and hands each value to one of
 // these epilogues.  Packed column orders are described in jpi_runtime.hip.
 // ---------------------------------------------------------------------------
-enum EpiKind { EPI_STORE_F32 = 0, EPI_QKV = 1, EPI_GEGLU = 2, EPI_RESID = 3 };
+enum EpiKind { EPI_STORE_F32 = 0, EPI_QKV = 1, EPI_GEGLU = 2 };
 
 struct EpiParams {
-  // EPI_STORE_F32
-  float* out_f32;        // [M][N]
+  // EPI_STORE_F32: [splitk][M][N] (slice z at out_f32 + z*M*N)
+  float* out_f32;
   // EPI_QKV: packed columns [q heads | k | v]; RoPE on q and k
   void* q;               // [B][nH][H][Dh]
   void* ks;              // [B][H][Dh]
-  void* vs;              // [B][H][Dh]
+  void* vst;             // [B][Dh][H] (v stored transposed)
   const float2* rope;    // [B][H][Dh/2] (cos, sin) at position prefix_len[b] + i
   int n_heads, head_dim, horizon;
   // EPI_GEGLU: packed columns in 32-wide groups [gate 16 | up 16]
   void* z;               // [M][F]
   int mlp_dim;
-  // EPI_RESID: h[m][n] += gate[n] * acc
-  float* h;              // [M][N]
-  const float* gate;     // [N]
 };
 
 struct GemmLaunch {
   const void* A;         // [M][K]
   const void* W;         // [N][K]
   int M, N, K;
-  int splitk;
-  float* partial;        // [splitk][M][N] fp32 scratch when splitk > 1
-  unsigned* counters;    // one per output tile, zero on entry, left zero on exit
+  int splitk;            // > 1 only with EPI_STORE_F32
   EpiKind epi;
   EpiParams ep;
+  hipEvent_t ev_start, ev_stop;  // optional: timestamps of this launch (measurement)
 };
 
 // launchers (jpi_kernels.hip).  All return hipSuccess or the launch error.
 hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s);
-size_t gemm_tiles(jpi_dtype dt, int M, int N);          // counters needed
+size_t gemm_tiles(jpi_dtype dt, int M, int N);          // workgroup tiles of one K slice
 int gemm_pick_splitk(jpi_dtype dt, int M, int N, int K, int n_cu);
 
-hipError_t launch_rmsnorm_mod(jpi_dtype dt, const float* h, const float* scale, const float* shift,
-                              void* y, int M, int W, float eps, hipStream_t s);
+hipError_t launch_sum_slices(const float* P, float* C, int S, size_t MN, hipStream_t s);
+int gemm_k_quantum(jpi_dtype dt, int M);  // K of every split must be a multiple of this
 
-hipError_t launch_inproj(jpi_dtype dt, const float* x, const void* w_in, const float* b_in, float* h,
-                         int M, int W, int A, hipStream_t s);
-
-hipError_t launch_final_euler(jpi_dtype dt, const float* h, const float* scale, const float* shift,
-                              const void* w_out, const float* b_out, float* x, int M, int W, int A,
-                              int horizon, int n_fixed, float dt_step, float eps, hipStream_t s);
+// Per-row residual update + next adaRMSNorm (see k_resid_norm).
+struct RowLaunch {
+  const float* part;     // [S][M][W] split-K slices of the sublayer output
+  int S, M, W;
+  float* h;              // [M][W] residual stream (updated in place)
+  const float* gate;     // [W]
+  const float* scale;    // [W] next norm (final norm when final_step)
+  const float* shift;    // [W]
+  void* y;               // [M][W] normalised activations (not final_step)
+  float eps;
+  // final_step only: action-out projection and Euler update
+  const void* w_out;     // [A][W]
+  const float* b_out;    // [A]
+  float* x;              // [M][A]
+  int A, horizon, n_fixed;
+  float dt;
+};
+hipError_t launch_inproj_norm(jpi_dtype dt, const float* x, const void* w_in, const float* b_in, float* h,
+                              const float* scale, const float* shift, void* y, int M, int W, int A, float eps,
+                              hipStream_t s);
+hipError_t launch_resid_norm(jpi_dtype dt, const RowLaunch& r, bool final_step, hipStream_t s);
 
 struct AttnLaunch {
   const void* q;          // [B][nH][H][Dh]
   const void* ks;         // [B][H][Dh]
-  const void* vs;         // [B][H][Dh]
-  const void* kp;         // prefix K for this layer: rollout b at kp + b*kp_bstride elements
-  const void* vp;
-  int64_t kp_bstride;     // elements between rollouts in kp / vp
+  const void* vst;        // [B][Dh][H]   suffix V, transposed
+  const void* kp;         // prefix K: rollout b at kp + b*kp_bstride, key j at + j*Dh
+  const void* vpt;        // prefix V transposed: rollout b at vpt + b*vpt_bstride, dim d at + d*vpt_dstride
+  int64_t kp_bstride, vpt_bstride, vpt_dstride;  // elements; vpt_dstride a multiple of 8
   const int* prefix_len;  // device [B]
   int B, nH, H, P, Dh;
   float* opart;           // [B][nH][n_chunks][H][Dh]
@@ -74,9 +87,14 @@ struct AttnLaunch {
   float* lpart;           // [B][nH][n_chunks][H]
   void* out;              // [B*H][nH*Dh] of dtype, or fp32 if out_f32
   int out_f32;
+  hipEvent_t ev_start, ev_stop;  // optional: start of the chunk pass, end of the combine
 };
 int attn_chunk(jpi_dtype dt);
 int attn_n_chunks(jpi_dtype dt, int P, int H);
+int attn_max_prefix(jpi_dtype dt, int H);
+// dst[z][c][r] = src[z][r][c] (r < rows, c < cols) for nmat matrices
+hipError_t launch_transpose(jpi_dtype dt, const void* src, void* dst, int rows, int cols, int64_t sld, int64_t dld,
+                            int64_t sz, int64_t dz, int nmat, hipStream_t s);
 hipError_t launch_attention(jpi_dtype dt, const AttnLaunch& a, hipStream_t s);
 
 hipError_t launch_time_embed(const float* t, float* emb, int n, int W, hipStream_t s);

@@ -15,6 +15,15 @@
 
 namespace jpi {
 
+// Launch with optional start/stop events tied to the dispatch itself.
+#define JPI_LAUNCH(kern, grid, block, shm, strm, evs, eve, ...)                           \
+  do {                                                                                    \
+    if ((evs) || (eve))                                                                   \
+      hipExtLaunchKernelGGL(kern, grid, block, shm, strm, evs, eve, 0, __VA_ARGS__);      \
+    else                                                                                  \
+      hipLaunchKernelGGL(kern, grid, block, shm, strm, __VA_ARGS__);                      \
+  } while (0)
+
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
@@ -49,6 +58,12 @@ __device__ __forceinline__ T from_f32(float v) { return static_cast<T>(v); }
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;
 }
 
@@ -87,38 +102,19 @@ __device__ __forceinline__ float gelu_tanh(float z) {
 
 // ===========================================================================
 // GEMM: acc[m][n] = sum_k A[m][k] W[n][k], A and W row-major with leading
-// dimension K.  Workgroup tile BM x BN, 4 waves in a 2 x 2 arrangement, K
-// staged through LDS in BK slices with register double buffering.  With
-// splitk > 1, blockIdx.z owns one K slice; each slice writes its fp32 partial
-// tile and the last slice to finish (counted with an atomic) sums all slices
-// in order z = 0..splitk-1 and runs the epilogue.
+// dimension K.  With splitk > 1, blockIdx.z owns the K slice
+// [z K/splitk, (z+1) K/splitk) and the epilogue must be EPI_STORE_F32, which
+// then writes slice z's partial sums to out_f32 + z*M*N; a separate row kernel
+// sums the slices in order (no cross-workgroup signalling inside a GEMM).
 // ===========================================================================
-template <typename T, int BM, int BN>
-struct GemmShape {
-  static constexpr int BK = sizeof(T) == 2 ? 64 : 32;
-  static constexpr int VEC = 16 / sizeof(T);      // elements per 16-byte chunk
-  static constexpr int LDK = BK + VEC;            // padded LDS row (bank spread)
-  static constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
-  static constexpr int TM = WM / 16, TN = WN / 16;
-  static constexpr int CPR = BK / VEC;            // 16-byte chunks per tile row
-  static constexpr int A_CH = BM * CPR / 256;
-  static constexpr int W_CH = BN * CPR / 256;
-  static_assert(TN % 2 == 0, "epilogues pair n-subtiles 2t and 2t+1");
-  static_assert(A_CH >= 1 && W_CH >= 1, "tile too small for 256 threads");
-};
-
 template <typename T, EpiKind EPI>
-__device__ __forceinline__ void epilogue_pair(const EpiParams& ep, int M, int N, int row, int col_lo, float lo,
-                                              float hi) {
+__device__ __forceinline__ void epilogue_pair(const EpiParams& ep, float* out_f32, int M, int N, int row, int col_lo,
+                                              float lo, float hi) {
   if (row >= M) return;
   const int col_hi = col_lo + 16;
   if constexpr (EPI == EPI_STORE_F32) {
-    if (col_lo < N) ep.out_f32[(size_t)row * N + col_lo] = lo;
-    if (col_hi < N) ep.out_f32[(size_t)row * N + col_hi] = hi;
-  } else if constexpr (EPI == EPI_RESID) {
-    float* hr = ep.h + (size_t)row * N;
-    hr[col_lo] += ep.gate[col_lo] * lo;
-    hr[col_hi] += ep.gate[col_hi] * hi;
+    if (col_lo < N) out_f32[(size_t)row * N + col_lo] = lo;
+    if (col_hi < N) out_f32[(size_t)row * N + col_hi] = hi;
   } else if constexpr (EPI == EPI_GEGLU) {
     // packed group t of 32 columns: [gate f = 16t + c | up f = 16t + c]
     const int f = (col_lo >> 5) * 16 + (col_lo & 15);
@@ -141,13 +137,29 @@ __device__ __forceinline__ void epilogue_pair(const EpiParams& ep, int M, int N,
       dst[d] = from_f32<T>(r_lo);
       dst[d + half] = from_f32<T>(r_hi);
     } else {
-      const int within = col_lo - qcols - Dh;  // v: natural order
-      T* dst = reinterpret_cast<T*>(ep.vs) + ((size_t)b * H + i) * Dh;
-      dst[within] = from_f32<T>(lo);
-      dst[within + 16] = from_f32<T>(hi);
+      const int within = col_lo - qcols - Dh;  // v: natural order, stored transposed [b][d][i]
+      T* dst = reinterpret_cast<T*>(ep.vst) + (size_t)b * Dh * H + i;
+      dst[(size_t)within * H] = from_f32<T>(lo);
+      dst[(size_t)(within + 16) * H] = from_f32<T>(hi);
     }
   }
 }
+
+// ---- tiled GEMM for M > 64: workgroup tile BM x BN, 4 waves in 2 x 2, K
+// staged through LDS in BK slices with register double buffering ----------
+template <typename T, int BM, int BN>
+struct GemmShape {
+  static constexpr int BK = sizeof(T) == 2 ? 64 : 32;
+  static constexpr int VEC = 16 / sizeof(T);      // elements per 16-byte chunk
+  static constexpr int LDK = BK + VEC;            // padded LDS row (bank spread)
+  static constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
+  static constexpr int TM = WM / 16, TN = WN / 16;
+  static constexpr int CPR = BK / VEC;            // 16-byte chunks per tile row
+  static constexpr int A_CH = BM * CPR / 256;
+  static constexpr int W_CH = BN * CPR / 256;
+  static_assert(TN % 2 == 0, "epilogues pair n-subtiles 2t and 2t+1");
+  static_assert(A_CH >= 1 && W_CH >= 1, "tile too small for 256 threads");
+};
 
 template <typename T, int BM, int BN, EpiKind EPI>
 __global__ __launch_bounds__(256) void k_gemm(GemmLaunch g) {
@@ -155,7 +167,6 @@ __global__ __launch_bounds__(256) void k_gemm(GemmLaunch g) {
   using MF = Mfma<T>;
   __shared__ __attribute__((aligned(16))) T As[2][BM * S::LDK];
   __shared__ __attribute__((aligned(16))) T Ws[2][BN * S::LDK];
-  __shared__ unsigned s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -231,73 +242,118 @@ __global__ __launch_bounds__(256) void k_gemm(GemmLaunch g) {
 
   const int rbase = m0 + wm * S::WM + (lane >> 4) * 4;
   const int cbase = n0 + wn * S::WN + fr;
-  if (g.splitk > 1) {
-    float* P = g.partial + (size_t)blockIdx.z * M * N;
-#pragma unroll
-    for (int a = 0; a < S::TM; ++a)
-#pragma unroll
-      for (int b = 0; b < S::TN; ++b)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = rbase + a * 16 + i, col = cbase + b * 16;
-          if (row < M && col < N) P[(size_t)row * N + col] = acc[a][b][i];
-        }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-      const unsigned tile = blockIdx.y * gridDim.x + blockIdx.x;
-      const unsigned prev = atomicAdd(&g.counters[tile], 1u);
-      s_last = prev == (unsigned)g.splitk - 1u;
-      if (s_last) g.counters[tile] = 0u;  // every slice has arrived: ready for the next launch
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-#pragma unroll
-    for (int a = 0; a < S::TM; ++a)
-#pragma unroll
-      for (int b = 0; b < S::TN; ++b)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = rbase + a * 16 + i, col = cbase + b * 16;
-          float sum = 0.f;
-          if (row < M && col < N)
-            for (int z = 0; z < g.splitk; ++z) sum += g.partial[((size_t)z * M + row) * N + col];
-          acc[a][b][i] = sum;
-        }
-  }
+  float* out = g.ep.out_f32 ? g.ep.out_f32 + (size_t)blockIdx.z * M * N : nullptr;
 #pragma unroll
   for (int a = 0; a < S::TM; ++a)
 #pragma unroll
     for (int b = 0; b < S::TN; b += 2)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        epilogue_pair<T, EPI>(g.ep, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i], acc[a][b + 1][i]);
+        epilogue_pair<T, EPI>(g.ep, out, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i], acc[a][b + 1][i]);
 }
 
+// ---- skinny GEMM for M <= 64 (weight streaming): a workgroup owns 32 output
+// columns and one K slice; its 4 waves split the slice four ways.  Each wave
+// issues its weight fragments (16 bytes per lane per 16x32 tile) and
+// activation fragments straight from memory into registers, BATCH k-steps at
+// a time, before the MFMAs.  The four partial tiles are summed in LDS in wave
+// order. --------------------------------------------------------------------
 template <typename T>
-static void gemm_tile(int M, int& BM, int& BN) {
-  if (sizeof(T) == 2 && M > 64) {
-    BM = 128;
-    BN = 128;
-  } else {
-    BM = 64;
-    BN = 64;
+struct SkinnyShape {
+  static constexpr int KSUB = Mfma<T>::KSUB;
+  static constexpr int WAVES = 8;                        // K split inside the workgroup
+  static constexpr int BATCH = sizeof(T) == 2 ? 4 : 16;  // k steps in flight per wave
+};
+
+template <typename T, EpiKind EPI>
+__global__ __launch_bounds__(512) void k_gemm_skinny(GemmLaunch g) {
+  using MF = Mfma<T>;
+  using SS = SkinnyShape<T>;
+  __shared__ f32x4 red[SS::WAVES][4][2][64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int M = g.M, N = g.N, K = g.K;
+  const int n0 = blockIdx.x * 32;
+  const int kper = K / g.splitk;
+  const int kw = kper / SS::WAVES;
+  const int k0 = blockIdx.z * kper + wave * kw;
+  const int nsub = kw / SS::KSUB;
+  const T* A = reinterpret_cast<const T*>(g.A);
+  const T* W = reinterpret_cast<const T*>(g.W);
+  const int fr = lane & 15, fk = (lane >> 4) * MF::KPL;
+  const T* wp0 = W + (size_t)min(n0 + fr, N - 1) * K + k0 + fk;
+  const T* wp1 = W + (size_t)min(n0 + 16 + fr, N - 1) * K + k0 + fk;
+
+  f32x4 acc[4][2];
+#pragma unroll
+  for (int a = 0; a < 4; ++a) acc[a][0] = acc[a][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int s0 = 0; s0 < nsub; s0 += SS::BATCH) {
+    typename MF::frag wf[SS::BATCH][2], af[SS::BATCH][4];
+#pragma unroll
+    for (int c = 0; c < SS::BATCH; ++c) {
+      if (s0 + c < nsub) {
+        wf[c][0] = MF::load(wp0 + (s0 + c) * SS::KSUB);
+        wf[c][1] = MF::load(wp1 + (s0 + c) * SS::KSUB);
+      } else {
+        wf[c][0] = wf[c][1] = typename MF::frag{};
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < SS::BATCH; ++c)
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int row = a * 16 + fr;
+        af[c][a] = (s0 + c < nsub && row < M) ? MF::load(A + (size_t)row * K + k0 + (s0 + c) * SS::KSUB + fk)
+                                              : typename MF::frag{};
+      }
+#pragma unroll
+    for (int c = 0; c < SS::BATCH; ++c)
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        acc[a][0] = MF::run(af[c][a], wf[c][0], acc[a][0]);
+        acc[a][1] = MF::run(af[c][a], wf[c][1], acc[a][1]);
+      }
   }
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    red[wave][a][0][lane] = acc[a][0];
+    red[wave][a][1][lane] = acc[a][1];
+  }
+  __syncthreads();
+  if (wave >= 4) return;
+  // wave w finishes m-subtile w, summing the K-split waves in order
+  const int a = wave;
+  f32x4 lo = red[0][a][0][lane], hi = red[0][a][1][lane];
+#pragma unroll
+  for (int v = 1; v < SS::WAVES; ++v) {
+    lo += red[v][a][0][lane];
+    hi += red[v][a][1][lane];
+  }
+  float* out = g.ep.out_f32 ? g.ep.out_f32 + (size_t)blockIdx.z * M * N : nullptr;
+  const int rbase = a * 16 + (lane >> 4) * 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) epilogue_pair<T, EPI>(g.ep, out, M, N, rbase + i, n0 + fr, lo[i], hi[i]);
+}
+
+static bool use_skinny(int M) { return M <= 64; }
+
+int gemm_k_quantum(jpi_dtype dt, int M) {
+  if (use_skinny(M))
+    return SkinnyShape<bf16>::WAVES * (dt == JPI_BF16 ? SkinnyShape<bf16>::KSUB : SkinnyShape<float>::KSUB);
+  return dt == JPI_BF16 ? GemmShape<bf16, 128, 128>::BK : GemmShape<float, 64, 64>::BK;
 }
 
 size_t gemm_tiles(jpi_dtype dt, int M, int N) {
-  int BM, BN;
-  if (dt == JPI_BF16) gemm_tile<bf16>(M, BM, BN);
-  else gemm_tile<float>(M, BM, BN);
+  if (use_skinny(M)) return (size_t)((N + 31) / 32);
+  const int BM = dt == JPI_BF16 ? 128 : 64, BN = BM;
   return (size_t)((N + BN - 1) / BN) * ((M + BM - 1) / BM);
 }
 
 int gemm_pick_splitk(jpi_dtype dt, int M, int N, int K, int n_cu) {
-  const int BK = dt == JPI_BF16 ? 64 : 32;
+  const int q = gemm_k_quantum(dt, M);
   const size_t tiles = gemm_tiles(dt, M, N);
   int s = 1;
-  while (s < 16 && tiles * s < (size_t)(2 * n_cu) && K % (2 * s * BK) == 0) s *= 2;
+  while (s < 16 && tiles * s < (size_t)n_cu && K % (2 * s * q) == 0) s *= 2;
   return s;
 }
 
@@ -305,112 +361,198 @@ template <typename T, int BM, int BN>
 static hipError_t launch_gemm_t(const GemmLaunch& g, hipStream_t s) {
   dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, g.splitk);
   switch (g.epi) {
-    case EPI_STORE_F32: hipLaunchKernelGGL((k_gemm<T, BM, BN, EPI_STORE_F32>), grid, dim3(256), 0, s, g); break;
-    case EPI_QKV: hipLaunchKernelGGL((k_gemm<T, BM, BN, EPI_QKV>), grid, dim3(256), 0, s, g); break;
-    case EPI_GEGLU: hipLaunchKernelGGL((k_gemm<T, BM, BN, EPI_GEGLU>), grid, dim3(256), 0, s, g); break;
-    case EPI_RESID: hipLaunchKernelGGL((k_gemm<T, BM, BN, EPI_RESID>), grid, dim3(256), 0, s, g); break;
+    case EPI_STORE_F32:
+      JPI_LAUNCH((k_gemm<T, BM, BN, EPI_STORE_F32>), grid, dim3(256), 0, s, g.ev_start, g.ev_stop, g);
+      break;
+    case EPI_QKV: JPI_LAUNCH((k_gemm<T, BM, BN, EPI_QKV>), grid, dim3(256), 0, s, g.ev_start, g.ev_stop, g); break;
+    case EPI_GEGLU:
+      JPI_LAUNCH((k_gemm<T, BM, BN, EPI_GEGLU>), grid, dim3(256), 0, s, g.ev_start, g.ev_stop, g);
+      break;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_skinny_t(const GemmLaunch& g, hipStream_t s) {
+  dim3 grid((g.N + 31) / 32, 1, g.splitk), block(64 * SkinnyShape<T>::WAVES);
+  switch (g.epi) {
+    case EPI_STORE_F32:
+      JPI_LAUNCH((k_gemm_skinny<T, EPI_STORE_F32>), grid, block, 0, s, g.ev_start, g.ev_stop, g);
+      break;
+    case EPI_QKV: JPI_LAUNCH((k_gemm_skinny<T, EPI_QKV>), grid, block, 0, s, g.ev_start, g.ev_stop, g); break;
+    case EPI_GEGLU: JPI_LAUNCH((k_gemm_skinny<T, EPI_GEGLU>), grid, block, 0, s, g.ev_start, g.ev_stop, g); break;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s) {
-  if (dt == JPI_BF16) {
-    if (g.M > 64) return launch_gemm_t<bf16, 128, 128>(g, s);
-    return launch_gemm_t<bf16, 64, 64>(g, s);
+  if (g.splitk > 1 && g.epi != EPI_STORE_F32) return hipErrorInvalidValue;
+  if (g.K % (g.splitk * gemm_k_quantum(dt, g.M)) != 0) return hipErrorInvalidValue;
+  if (use_skinny(g.M)) {
+    if (dt == JPI_BF16) return launch_skinny_t<bf16>(g, s);
+    return launch_skinny_t<float>(g, s);
   }
+  if (dt == JPI_BF16) return launch_gemm_t<bf16, 128, 128>(g, s);
   return launch_gemm_t<float, 64, 64>(g, s);
 }
 
+// fixed-order sum of split-K slices: C[i] = sum_z P[z][i]
+__global__ void k_sum_slices(const float* __restrict__ P, float* __restrict__ C, int S, size_t MN) {
+  const size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+  if (i >= MN) return;
+  float v = 0.f;
+  for (int z = 0; z < S; ++z) v += P[z * MN + i];
+  C[i] = v;
+}
+
+hipError_t launch_sum_slices(const float* P, float* C, int S, size_t MN, hipStream_t s) {
+  hipLaunchKernelGGL(k_sum_slices, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, P, C, S, MN);
+  return hipGetLastError();
+}
+
 // ===========================================================================
-// adaRMSNorm: y[m][k] = h[m][k] / sqrt(mean_k h^2 + eps) * (1 + scale[k]) + shift[k]
+// Row kernels (one workgroup of 256 threads per activation row m).
+//
+// k_inproj_norm:  h = x W_in^T + b_in;  y = adaRMSNorm(h; scale, shift)
+// k_resid_norm:   h += gate * sum_z P[z][m];  y = adaRMSNorm(h; scale, shift)
+//   FINAL variant: v = adaRMSNorm(h; s_f, b_f) W_out^T + b_out and
+//                  x[m] += dt * v for rows i >= n_fixed
+// adaRMSNorm(h) = h / sqrt(mean(h^2) + eps) * (1 + scale) + shift.
 // ===========================================================================
+constexpr int ROW_MAX_W = 4096;
+
+__device__ __forceinline__ float row_rstd(const float* hs, int W, float eps, float* red) {
+  float ss = 0.f;
+  for (int k = threadIdx.x; k < W; k += 256) ss += hs[k] * hs[k];
+  ss = block_sum_256(ss, red);
+  return 1.0f / sqrtf(ss / (float)W + eps);
+}
+
 template <typename T>
-__global__ __launch_bounds__(256) void k_rmsnorm_mod(const float* __restrict__ h, const float* __restrict__ scale,
-                                                     const float* __restrict__ shift, T* __restrict__ y, int W,
-                                                     float eps) {
+__global__ __launch_bounds__(256) void k_inproj_norm(const float* __restrict__ x, const T* __restrict__ w_in,
+                                                     const float* __restrict__ b_in, float* __restrict__ h,
+                                                     const float* __restrict__ scale, const float* __restrict__ shift,
+                                                     T* __restrict__ y, int W, int A, float eps) {
+  __shared__ float hs[ROW_MAX_W];
+  __shared__ float xs[256];
   __shared__ float red[4];
   const int m = blockIdx.x;
-  const float* hr = h + (size_t)m * W;
-  float ss = 0.f;
-  for (int k = threadIdx.x; k < W; k += 256) ss += hr[k] * hr[k];
-  ss = block_sum_256(ss, red);
-  const float r = 1.0f / sqrtf(ss / (float)W + eps);
-  for (int k = threadIdx.x; k < W; k += 256)
-    y[(size_t)m * W + k] = from_f32<T>(hr[k] * r * (1.0f + scale[k]) + shift[k]);
-}
-
-hipError_t launch_rmsnorm_mod(jpi_dtype dt, const float* h, const float* scale, const float* shift, void* y,
-                              int M, int W, float eps, hipStream_t s) {
-  if (dt == JPI_BF16)
-    hipLaunchKernelGGL(k_rmsnorm_mod<bf16>, dim3(M), dim3(256), 0, s, h, scale, shift, (bf16*)y, W, eps);
-  else
-    hipLaunchKernelGGL(k_rmsnorm_mod<float>, dim3(M), dim3(256), 0, s, h, scale, shift, (float*)y, W, eps);
-  return hipGetLastError();
-}
-
-// ===========================================================================
-// action input projection: h[m][n] = sum_a x[m][a] W_in[n][a] + b_in[n]
-// ===========================================================================
-template <typename T>
-__global__ __launch_bounds__(256) void k_inproj(const float* __restrict__ x, const T* __restrict__ w,
-                                                const float* __restrict__ b, float* __restrict__ h, int M, int W,
-                                                int A) {
-  const int idx = blockIdx.x * 256 + threadIdx.x;
-  if (idx >= M * W) return;
-  const int m = idx / W, n = idx - m * W;
-  float acc = 0.f;
-  for (int a = 0; a < A; ++a) acc = fmaf(x[(size_t)m * A + a], static_cast<float>(w[(size_t)n * A + a]), acc);
-  h[idx] = acc + b[n];
-}
-
-hipError_t launch_inproj(jpi_dtype dt, const float* x, const void* w_in, const float* b_in, float* h, int M,
-                         int W, int A, hipStream_t s) {
-  const int blocks = (M * W + 255) / 256;
-  if (dt == JPI_BF16)
-    hipLaunchKernelGGL(k_inproj<bf16>, dim3(blocks), dim3(256), 0, s, x, (const bf16*)w_in, b_in, h, M, W, A);
-  else
-    hipLaunchKernelGGL(k_inproj<float>, dim3(blocks), dim3(256), 0, s, x, (const float*)w_in, b_in, h, M, W, A);
-  return hipGetLastError();
-}
-
-// ===========================================================================
-// final adaRMSNorm + action-out projection + Euler update of rows i >= n_fixed:
-// v = (rms(h) (1 + s_f) + b_f) W_out^T + b_out;  x += dt * v
-// ===========================================================================
-template <typename T>
-__global__ __launch_bounds__(256) void k_final_euler(const float* __restrict__ h, const float* __restrict__ scale,
-                                                     const float* __restrict__ shift, const T* __restrict__ w_out,
-                                                     const float* __restrict__ b_out, float* __restrict__ x, int W,
-                                                     int A, int H, int n_fixed, float dt, float eps) {
-  extern __shared__ float ys[];  // [W]
-  __shared__ float red[4];
-  const int m = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const float* hr = h + (size_t)m * W;
-  float ss = 0.f;
-  for (int k = threadIdx.x; k < W; k += 256) ss += hr[k] * hr[k];
-  ss = block_sum_256(ss, red);
-  const float r = 1.0f / sqrtf(ss / (float)W + eps);
-  for (int k = threadIdx.x; k < W; k += 256) ys[k] = hr[k] * r * (1.0f + scale[k]) + shift[k];
+  for (int a = threadIdx.x; a < A; a += 256) xs[a] = x[(size_t)m * A + a];
   __syncthreads();
-  const int i = m % H;
-  for (int a = wave; a < A; a += 4) {
+  for (int n = threadIdx.x; n < W; n += 256) {
     float acc = 0.f;
-    for (int k = lane; k < W; k += 64) acc = fmaf(ys[k], static_cast<float>(w_out[(size_t)a * W + k]), acc);
-    acc = wave_sum(acc);
-    if (lane == 0 && i >= n_fixed) x[(size_t)m * A + a] += dt * (acc + b_out[a]);
+    for (int a = 0; a < A; ++a) acc = fmaf(xs[a], static_cast<float>(w_in[(size_t)n * A + a]), acc);
+    const float v = acc + b_in[n];
+    hs[n] = v;
+    h[(size_t)m * W + n] = v;
+  }
+  __syncthreads();
+  const float r = row_rstd(hs, W, eps, red);
+  for (int k = threadIdx.x; k < W; k += 256)
+    y[(size_t)m * W + k] = from_f32<T>(hs[k] * r * (1.0f + scale[k]) + shift[k]);
+}
+
+constexpr int ROW_MAX_S = 16;
+constexpr int ROW_MAX_A = 64;
+
+template <typename T, bool FINAL>
+__global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
+  __shared__ float hs[ROW_MAX_W];
+  __shared__ float red[4];
+  __shared__ float dots[4][ROW_MAX_A];
+  const int m = blockIdx.x, W = r.W, S = r.S;
+  const size_t MW = (size_t)r.M * W;
+  float* hr = r.h + (size_t)m * W;
+  const float* pr = r.part + (size_t)m * W;
+  // four columns per thread per pass; all split-K slices loaded before summing
+  for (int k0 = threadIdx.x; k0 < W; k0 += 1024) {
+    float v[4][ROW_MAX_S], hv[4], gv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int k = k0 + 256 * j;
+#pragma unroll
+      for (int z = 0; z < ROW_MAX_S; ++z) v[j][z] = (z < S && k < W) ? pr[z * MW + k] : 0.f;
+      hv[j] = k < W ? hr[k] : 0.f;
+      gv[j] = k < W ? r.gate[k] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int k = k0 + 256 * j;
+      float sum = 0.f;
+#pragma unroll
+      for (int z = 0; z < ROW_MAX_S; ++z)
+        if (z < S) sum += v[j][z];
+      if (k < W) {
+        const float h2 = hv[j] + gv[j] * sum;
+        hr[k] = h2;
+        hs[k] = h2;
+      }
+    }
+  }
+  __syncthreads();
+  const float rs = row_rstd(hs, W, r.eps, red);
+  if constexpr (!FINAL) {
+    T* yr = reinterpret_cast<T*>(r.y) + (size_t)m * W;
+    for (int k = threadIdx.x; k < W; k += 256) yr[k] = from_f32<T>(hs[k] * rs * (1.0f + r.scale[k]) + r.shift[k]);
+  } else {
+    // v[a] = sum_k y[k] W_out[a][k] + b_out[a]; each thread owns columns k = t + 256 j
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const T* wo = reinterpret_cast<const T*>(r.w_out);
+    float yk[ROW_MAX_W / 256];
+#pragma unroll
+    for (int j = 0; j < ROW_MAX_W / 256; ++j) {
+      const int k = threadIdx.x + 256 * j;
+      yk[j] = k < W ? hs[k] * rs * (1.0f + r.scale[k]) + r.shift[k] : 0.f;
+    }
+    for (int a0 = 0; a0 < r.A; a0 += 8) {
+      float p[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        p[u] = 0.f;
+#pragma unroll
+        for (int j = 0; j < ROW_MAX_W / 256; ++j) {
+          const int k = threadIdx.x + 256 * j;
+          if (a0 + u < r.A && k < W) p[u] = fmaf(yk[j], static_cast<float>(wo[(size_t)(a0 + u) * W + k]), p[u]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float t = wave_sum(p[u]);
+        if (lane == 0 && a0 + u < r.A) dots[wave][a0 + u] = t;
+      }
+    }
+    __syncthreads();
+    const int i = m % r.horizon;
+    if (threadIdx.x < r.A && i >= r.n_fixed) {
+      const int a = threadIdx.x;
+      const float v = ((dots[0][a] + dots[1][a]) + dots[2][a]) + dots[3][a] + r.b_out[a];
+      r.x[(size_t)m * r.A + a] += r.dt * v;
+    }
   }
 }
 
-hipError_t launch_final_euler(jpi_dtype dt, const float* h, const float* scale, const float* shift,
-                              const void* w_out, const float* b_out, float* x, int M, int W, int A, int horizon,
-                              int n_fixed, float dt_step, float eps, hipStream_t s) {
-  const size_t lds = (size_t)W * sizeof(float);
+hipError_t launch_inproj_norm(jpi_dtype dt, const float* x, const void* w_in, const float* b_in, float* h,
+                              const float* scale, const float* shift, void* y, int M, int W, int A, float eps,
+                              hipStream_t s) {
+  if (W > ROW_MAX_W || A > 256) return hipErrorInvalidValue;
   if (dt == JPI_BF16)
-    hipLaunchKernelGGL(k_final_euler<bf16>, dim3(M), dim3(256), lds, s, h, scale, shift, (const bf16*)w_out, b_out,
-                       x, W, A, horizon, n_fixed, dt_step, eps);
+    hipLaunchKernelGGL(k_inproj_norm<bf16>, dim3(M), dim3(256), 0, s, x, (const bf16*)w_in, b_in, h, scale, shift,
+                       (bf16*)y, W, A, eps);
   else
-    hipLaunchKernelGGL(k_final_euler<float>, dim3(M), dim3(256), lds, s, h, scale, shift, (const float*)w_out,
-                       b_out, x, W, A, horizon, n_fixed, dt_step, eps);
+    hipLaunchKernelGGL(k_inproj_norm<float>, dim3(M), dim3(256), 0, s, x, (const float*)w_in, b_in, h, scale, shift,
+                       (float*)y, W, A, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_resid_norm(jpi_dtype dt, const RowLaunch& r, bool final_step, hipStream_t s) {
+  if (r.W > ROW_MAX_W || r.S > ROW_MAX_S || r.S < 1 || (final_step && r.A > ROW_MAX_A)) return hipErrorInvalidValue;
+  if (dt == JPI_BF16) {
+    if (final_step) hipLaunchKernelGGL((k_resid_norm<bf16, true>), dim3(r.M), dim3(256), 0, s, r);
+    else hipLaunchKernelGGL((k_resid_norm<bf16, false>), dim3(r.M), dim3(256), 0, s, r);
+  } else {
+    if (final_step) hipLaunchKernelGGL((k_resid_norm<float, true>), dim3(r.M), dim3(256), 0, s, r);
+    else hipLaunchKernelGGL((k_resid_norm<float, false>), dim3(r.M), dim3(256), 0, s, r);
+  }
   return hipGetLastError();
 }
 
@@ -420,12 +562,16 @@ hipError_t launch_final_euler(jpi_dtype dt, const float* h, const float* scale, 
 // The concatenated key sequence [prefix 0..pl-1 | action 0..H-1] is cut into
 // chunks of KC keys; a workgroup handles one (rollout, head, 64-query block,
 // chunk) and writes the chunk's running max, sum and unnormalised output.
-// Slots j >= pl of the prefix are never read.
+// K is read row-major ([key][Dh]); V is read transposed ([Dh][key]) so that
+// the P.V operand streams along keys.  Slots j >= pl of the prefix are never
+// used: a 16-byte V chunk that reaches past pl is assembled element by
+// element with the out-of-range keys set to zero.
 // ===========================================================================
 template <typename T>
 struct AttnShape {
   static constexpr int KC = sizeof(T) == 2 ? 64 : 32;
   static constexpr int PAD = 16 / sizeof(T);
+  static constexpr int MAX_CHUNKS = 512;
 };
 
 template <typename T, int DH>
@@ -436,6 +582,9 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnLaunch a) {
   constexpr int NST = DH / MF::KSUB;  // k steps over the head dim
   constexpr int NJ = KC / 16;         // key subtiles
   constexpr int VEC = 16 / sizeof(T);
+  constexpr int KCH = KC * (DH / VEC) / 256;  // 16-byte K chunks per thread
+  constexpr int VCH = DH * (KC / VEC) / 256;  // 16-byte V^T chunks per thread
+  static_assert(KCH >= 1 && VCH >= 1, "tile too small");
   __shared__ __attribute__((aligned(16))) T Ks[KC * LDK];
   __shared__ __attribute__((aligned(16))) T Vt[DH * LDV];
   __shared__ __attribute__((aligned(16))) T Ps[64 * LDP];
@@ -470,27 +619,36 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnLaunch a) {
   }
 
   const T* kp = reinterpret_cast<const T*>(a.kp) + (size_t)b * a.kp_bstride;
-  const T* vp = reinterpret_cast<const T*>(a.vp) + (size_t)b * a.kp_bstride;
+  const T* vpt = reinterpret_cast<const T*>(a.vpt) + (size_t)b * a.vpt_bstride;
   const T* ksb = reinterpret_cast<const T*>(a.ks) + (size_t)b * H * DH;
-  const T* vsb = reinterpret_cast<const T*>(a.vs) + (size_t)b * H * DH;
-  constexpr int CPR = DH / VEC;
-  for (int e = tid; e < KC * CPR; e += 256) {
-    const int r = e / CPR, cc = e - r * CPR;
-    const int kidx = kbase + r;
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (kidx < pl) {
-      kv = *reinterpret_cast<const uint4*>(kp + (size_t)kidx * DH + cc * VEC);
-      vv = *reinterpret_cast<const uint4*>(vp + (size_t)kidx * DH + cc * VEC);
-    } else if (kidx < nkeys) {
-      kv = *reinterpret_cast<const uint4*>(ksb + (size_t)(kidx - pl) * DH + cc * VEC);
-      vv = *reinterpret_cast<const uint4*>(vsb + (size_t)(kidx - pl) * DH + cc * VEC);
-    }
-    *reinterpret_cast<uint4*>(&Ks[r * LDK + cc * VEC]) = kv;
-    const T* vt = reinterpret_cast<const T*>(&vv);
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) Vt[(cc * VEC + j) * LDV + r] = vt[j];
-  }
+  const T* vstb = reinterpret_cast<const T*>(a.vst) + (size_t)b * DH * H;
 
+  // issue every global load of the chunk before the first LDS store
+  uint4 kr[KCH], vr[VCH];
+#pragma unroll
+  for (int it = 0; it < KCH; ++it) {
+    const int e = tid + it * 256, r = e / (DH / VEC), cc = e - r * (DH / VEC);
+    const int key = kbase + r;
+    const T* src = key < pl ? kp + (size_t)key * DH : ksb + (size_t)(key - pl) * DH;
+    kr[it] = key < nkeys ? *reinterpret_cast<const uint4*>(src + cc * VEC) : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int it = 0; it < VCH; ++it) {
+    const int e = tid + it * 256, d = e / (KC / VEC), kc = e - d * (KC / VEC);
+    const int key0 = kbase + kc * VEC;
+    if (key0 + VEC <= pl) {
+      vr[it] = *reinterpret_cast<const uint4*>(vpt + (size_t)d * a.vpt_dstride + key0);
+    } else {
+      T tmp[VEC];
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) {
+        const int key = key0 + j;
+        tmp[j] = key < pl ? vpt[(size_t)d * a.vpt_dstride + key]
+                          : (key < nkeys ? vstb[(size_t)d * H + (key - pl)] : from_f32<T>(0.f));
+      }
+      __builtin_memcpy(&vr[it], tmp, 16);
+    }
+  }
   // query fragments of this wave's 16 rows, kept in registers
   const int fr = lane & 15, fk = (lane >> 4) * MF::KPL;
   const int iq = qb * 64 + w * 16 + fr;
@@ -498,10 +656,17 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnLaunch a) {
   {
     const T* qrow = reinterpret_cast<const T*>(a.q) + (((size_t)b * a.nH + hn) * H + (iq < H ? iq : 0)) * DH;
 #pragma unroll
-    for (int st = 0; st < NST; ++st) {
-      if (iq < H) qf[st] = MF::load(qrow + st * MF::KSUB + fk);
-      else qf[st] = typename MF::frag{};
-    }
+    for (int st = 0; st < NST; ++st) qf[st] = iq < H ? MF::load(qrow + st * MF::KSUB + fk) : typename MF::frag{};
+  }
+#pragma unroll
+  for (int it = 0; it < KCH; ++it) {
+    const int e = tid + it * 256, r = e / (DH / VEC), cc = e - r * (DH / VEC);
+    *reinterpret_cast<uint4*>(&Ks[r * LDK + cc * VEC]) = kr[it];
+  }
+#pragma unroll
+  for (int it = 0; it < VCH; ++it) {
+    const int e = tid + it * 256, d = e / (KC / VEC), kc = e - d * (KC / VEC);
+    *reinterpret_cast<uint4*>(&Vt[d * LDV + kc * VEC]) = vr[it];
   }
   __syncthreads();
 
@@ -571,28 +736,42 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnLaunch a) {
 // out[(b*H + i)][hn*Dh + d] = sum_c e^(m_c - m) O_c[d] / sum_c e^(m_c - m) l_c
 template <typename TO, int DH>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnLaunch a, int nch) {
+  __shared__ float wts[AttnShape<float>::MAX_CHUNKS];
+  __shared__ float inv_l;
   const int H = a.H;
   const int i = blockIdx.x % H, bh = blockIdx.x / H;
   const int b = bh / a.nH, hn = bh - b * a.nH;
   const float* Mp = a.mpart + (size_t)bh * nch * H;
   const float* Lp = a.lpart + (size_t)bh * nch * H;
   const float* Op = a.opart + (size_t)bh * nch * H * DH;
-  float mx = -INFINITY;
-  for (int c = 0; c < nch; ++c) mx = fmaxf(mx, Mp[c * H + i]);
-  float L = 0.f;
-  for (int c = 0; c < nch; ++c) {
-    const float mc = Mp[c * H + i];
-    if (mc != -INFINITY) L += expf(mc - mx) * Lp[c * H + i];
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    float mx = -INFINITY;
+    for (int c = lane; c < nch; c += 64) mx = fmaxf(mx, Mp[c * H + i]);
+    mx = wave_max(mx);
+    float l = 0.f;
+    for (int c = lane; c < nch; c += 64) {
+      const float mc = Mp[c * H + i];
+      const float wc = mc == -INFINITY ? 0.f : expf(mc - mx);
+      wts[c] = wc;
+      l += wc * Lp[c * H + i];
+    }
+    l = wave_sum(l);
+    if (lane == 0) inv_l = 1.0f / l;
   }
-  const float inv = 1.0f / L;
+  __syncthreads();
   TO* out = reinterpret_cast<TO*>(a.out) + ((size_t)b * H + i) * a.nH * DH + hn * DH;
   for (int d = threadIdx.x; d < DH; d += blockDim.x) {
     float acc = 0.f;
-    for (int c = 0; c < nch; ++c) {
-      const float mc = Mp[c * H + i];
-      if (mc != -INFINITY) acc += expf(mc - mx) * Op[((size_t)c * H + i) * DH + d];
+    for (int c0 = 0; c0 < nch; c0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = c0 + u < nch ? Op[((size_t)(c0 + u) * H + i) * DH + d] : 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (c0 + u < nch) acc += wts[c0 + u] * v[u];
     }
-    out[d] = from_f32<TO>(acc * inv);
+    out[d] = from_f32<TO>(acc * inv_l);
   }
 }
 
@@ -601,19 +780,24 @@ int attn_n_chunks(jpi_dtype dt, int P, int H) {
   const int kc = attn_chunk(dt);
   return (P + H + kc - 1) / kc;
 }
+int attn_max_prefix(jpi_dtype dt, int H) { return AttnShape<float>::MAX_CHUNKS * attn_chunk(dt) - H; }
 
 template <typename T, int DH>
 static hipError_t launch_attention_t(const AttnLaunch& a, hipStream_t s) {
   const int nch = attn_n_chunks(sizeof(T) == 2 ? JPI_BF16 : JPI_F32, a.P, a.H);
+  if (nch > AttnShape<float>::MAX_CHUNKS) return hipErrorInvalidValue;
   const int nqb = (a.H + 63) / 64;
-  hipLaunchKernelGGL((k_attn_partial<T, DH>), dim3(nch, a.nH * nqb, a.B), dim3(256), 0, s, a);
+  JPI_LAUNCH((k_attn_partial<T, DH>), dim3(nch, a.nH * nqb, a.B), dim3(256), 0, s, a.ev_start, (hipEvent_t) nullptr,
+             a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int thr = DH < 256 ? DH : 256;
   if (a.out_f32)
-    hipLaunchKernelGGL((k_attn_combine<float, DH>), dim3(a.B * a.nH * a.H), dim3(thr), 0, s, a, nch);
+    JPI_LAUNCH((k_attn_combine<float, DH>), dim3(a.B * a.nH * a.H), dim3(thr), 0, s, (hipEvent_t) nullptr,
+               a.ev_stop, a, nch);
   else
-    hipLaunchKernelGGL((k_attn_combine<T, DH>), dim3(a.B * a.nH * a.H), dim3(thr), 0, s, a, nch);
+    JPI_LAUNCH((k_attn_combine<T, DH>), dim3(a.B * a.nH * a.H), dim3(thr), 0, s, (hipEvent_t) nullptr, a.ev_stop, a,
+               nch);
   return hipGetLastError();
 }
 
@@ -632,6 +816,39 @@ hipError_t launch_attention(jpi_dtype dt, const AttnLaunch& a, hipStream_t s) {
     }
   }
   return hipErrorInvalidValue;
+}
+
+// dst[z][c][r] = src[z][r][c] for r < rows, c < cols; 64 x 64 tiles through LDS.
+// src row stride `sld`, dst row stride `dld`, matrix strides sz / dz (elements).
+template <typename T>
+__global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ src, T* __restrict__ dst, int rows,
+                                                   int cols, int64_t sld, int64_t dld, int64_t sz, int64_t dz) {
+  __shared__ T tile[64][65];
+  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  const T* s = src + blockIdx.z * sz;
+  T* d = dst + blockIdx.z * dz;
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int r = e / 64, c = e % 64;
+    if (r0 + r < rows && c0 + c < cols) tile[r][c] = s[(size_t)(r0 + r) * sld + c0 + c];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int c = e / 64, r = e % 64;
+    if (r0 + r < rows && c0 + c < cols) d[(size_t)(c0 + c) * dld + r0 + r] = tile[r][c];
+  }
+}
+
+hipError_t launch_transpose(jpi_dtype dt, const void* src, void* dst, int rows, int cols, int64_t sld, int64_t dld,
+                            int64_t sz, int64_t dz, int nmat, hipStream_t s) {
+  if (rows == 0 || cols == 0 || nmat == 0) return hipSuccess;
+  dim3 grid((rows + 63) / 64, (cols + 63) / 64, nmat);
+  if (dt == JPI_BF16)
+    hipLaunchKernelGGL(k_transpose<bf16>, grid, dim3(256), 0, s, (const bf16*)src, (bf16*)dst, rows, cols, sld, dld,
+                       sz, dz);
+  else
+    hipLaunchKernelGGL(k_transpose<float>, grid, dim3(256), 0, s, (const float*)src, (float*)dst, rows, cols, sld,
+                       dld, sz, dz);
+  return hipGetLastError();
 }
 
 // ===========================================================================

@@ -82,7 +82,9 @@ struct jpi_ctx {
   std::vector<char> have;  // per (kind, layer)
   bool finalized = false;
   // prefix and state
-  void *kp = nullptr, *vp = nullptr;
+  void *kp = nullptr, *vp = nullptr;  // [L][Bmax][Pmax][Dh] as bound
+  void* vpt = nullptr;                 // [L][Bmax][Dh][Ppad] prefix V transposed at bind time
+  int Ppad = 0;                        // Pmax rounded up to a multiple of 8
   int* d_prefix_len = nullptr;
   int* h_prefix_len = nullptr;  // pinned staging
   int batch = 0, prefix = 0;
@@ -92,17 +94,19 @@ struct jpi_ctx {
   int n_fixed = 0;
   // activations
   float *x = nullptr, *h = nullptr;
-  void *y = nullptr, *q = nullptr, *ks = nullptr, *vs = nullptr, *o = nullptr, *z = nullptr;
-  float* partial = nullptr;
+  void *y = nullptr, *q = nullptr, *ks = nullptr, *vst = nullptr, *o = nullptr, *z = nullptr;
+  float* partial = nullptr;  // split-K slices of the O / Down projections
   size_t partial_cap = 0;
-  unsigned* counters = nullptr;
-  size_t counters_cap = 0;
-  float *opart = nullptr, *mlpart = nullptr;
+  float* opart = nullptr;    // attention chunk partials (O, running max, running sum)
   size_t attn_cap = 0;
   // caches
   std::map<int, float*> tables;
   std::map<GraphKey, hipGraphExec_t> graphs;
   hipStream_t cap_stream = nullptr;
+  // measurement: events around every launch of one kernel kind
+  int timed_kind = JPI_KERNEL_NONE;
+  std::vector<hipEvent_t> ev;  // pairs (start, end)
+  int ev_used = 0;
 };
 
 namespace {
@@ -144,6 +148,12 @@ jpi_status dmalloc(jpi_ctx* c, void** p, size_t bytes) {
 void drop_graphs(jpi_ctx* c) {
   for (auto& kv : c->graphs) (void)hipGraphExecDestroy(kv.second);
   c->graphs.clear();
+}
+
+void drop_events(jpi_ctx* c) {
+  for (hipEvent_t e : c->ev) (void)hipEventDestroy(e);
+  c->ev.clear();
+  c->ev_used = 0;
 }
 
 void drop_tables(jpi_ctx* c) {
@@ -240,9 +250,10 @@ jpi_status jpi_destroy(jpi_ctx* c) {
   (void)hipDeviceSynchronize();
   drop_graphs(c);
   drop_tables(c);
+  drop_events(c);
   void* bufs[] = {c->w_layers, c->w_in, c->w_t0, c->w_t1, c->w_mod, c->w_out, c->b_in, c->b_t0, c->b_t1, c->b_mod,
-                  c->b_out, c->kp, c->vp, c->d_prefix_len, c->rope_tab, c->committed, c->x, c->h, c->y, c->q, c->ks,
-                  c->vs, c->o, c->z, c->partial, c->counters, c->opart, c->mlpart};
+                  c->b_out, c->kp, c->vp, c->vpt, c->d_prefix_len, c->rope_tab, c->committed, c->x, c->h, c->y, c->q, c->ks,
+                  c->vst, c->o, c->z, c->partial, c->opart};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   if (c->h_prefix_len) (void)hipHostFree(c->h_prefix_len);
@@ -268,8 +279,13 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   if (g.dtype != JPI_F32 && g.dtype != JPI_BF16) return fail(nullptr, JPI_ERR_ARG, "jpi_create: bad dtype");
   if (!(g.rms_eps > 0.f) || !(g.rope_base > 1.f))
     return fail(nullptr, JPI_ERR_ARG, "jpi_create: rms_eps must be > 0 and rope_base > 1");
-  if ((long long)g.max_batch * g.horizon > (1 << 20) || g.max_prefix > (1 << 20))
-    return fail(nullptr, JPI_ERR_ARG, "jpi_create: max_batch*horizon or max_prefix too large");
+  if ((long long)g.max_batch * g.horizon > (1 << 20))
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: max_batch*horizon too large");
+  if (g.max_prefix > attn_max_prefix(g.dtype, g.horizon))
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: max_prefix above " +
+                                          std::to_string(attn_max_prefix(g.dtype, g.horizon)));
+  if (g.action_dim > 64) return fail(nullptr, JPI_ERR_ARG, "jpi_create: action_dim above 64");
+  if (g.width > 4096) return fail(nullptr, JPI_ERR_ARG, "jpi_create: width above 4096");
 
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev) {
@@ -333,6 +349,8 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   const size_t kv_elems = (size_t)c->L * c->Bmax * (size_t)c->Pmax * Dh;
   ALLOC(c->kp, kv_elems * es);
   ALLOC(c->vp, kv_elems * es);
+  c->Ppad = (c->Pmax + 7) / 8 * 8;
+  ALLOC(c->vpt, (size_t)c->L * c->Bmax * (size_t)c->Ppad * Dh * es);
   ALLOC(c->d_prefix_len, c->Bmax * 4);
   ALLOC(c->rope_tab, M * (Dh / 2) * sizeof(float2));
   ALLOC(c->committed, M * A * 4);
@@ -341,7 +359,7 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   ALLOC(c->y, M * W * es);
   ALLOC(c->q, M * nH * Dh * es);
   ALLOC(c->ks, M * Dh * es);
-  ALLOC(c->vs, M * Dh * es);
+  ALLOC(c->vst, M * Dh * es);
   ALLOC(c->o, M * nH * Dh * es);
   ALLOC(c->z, M * F * es);
 #undef ALLOC
@@ -517,6 +535,13 @@ jpi_status jpi_bind_prefix(jpi_ctx* c, const void* k, const void* v, const int32
                                  prefix * Dh * es, batch, hipMemcpyDeviceToDevice, s));
     }
   }
+  // prefix V transposed ([Dh][key]) for the attention kernels' P.V operand
+  for (int l = 0; l < c->L && prefix > 0; ++l) {
+    const size_t src_off = (size_t)l * c->Bmax * c->Pmax * Dh * es;
+    const size_t dst_off = (size_t)l * c->Bmax * c->Ppad * Dh * es;
+    HIPCHK(c, launch_transpose(c->dt, (const char*)c->vp + src_off, (char*)c->vpt + dst_off, prefix, (int)Dh,
+                               (int64_t)Dh, c->Ppad, (int64_t)c->Pmax * Dh, (int64_t)Dh * c->Ppad, batch, s));
+  }
   memcpy(c->h_prefix_len, lens.data(), batch * sizeof(int));
   HIPCHK(c, hipMemcpyAsync(c->d_prefix_len, c->h_prefix_len, batch * sizeof(int), hipMemcpyHostToDevice, s));
   HIPCHK(c, launch_rope_table(c->d_prefix_len, c->rope_tab, batch, c->H, c->Dh, c->cfg.rope_base, s));
@@ -580,33 +605,20 @@ jpi_status ensure_table(jpi_ctx* c, int n_steps, hipStream_t s, float** out) {
 
 struct StepGemms {
   int M;
-  int s_qkv, s_o, s_gu, s_d;
+  int s_o, s_d;  // split-K of the O and Down projections (QKV and GateUp are not split)
 };
 
 StepGemms plan_gemms(const jpi_ctx* c, int batch) {
   StepGemms p;
   p.M = batch * c->H;
-  const int qkvN = (c->nH + 2) * c->Dh;
-  p.s_qkv = gemm_pick_splitk(c->dt, p.M, qkvN, c->W, c->n_cu);
   p.s_o = gemm_pick_splitk(c->dt, p.M, c->W, c->nH * c->Dh, c->n_cu);
-  p.s_gu = gemm_pick_splitk(c->dt, p.M, 2 * c->F, c->W, c->n_cu);
   p.s_d = gemm_pick_splitk(c->dt, p.M, c->W, c->F, c->n_cu);
   return p;
 }
 
 jpi_status ensure_scratch(jpi_ctx* c, int batch, int prefix) {
   const StepGemms p = plan_gemms(c, batch);
-  const size_t M = p.M;
-  const size_t qkvN = (size_t)(c->nH + 2) * c->Dh;
-  size_t need = 0, tiles = 0;
-  auto acc = [&](int s, size_t N) {
-    if (s > 1) need = std::max(need, (size_t)s * M * N);
-    tiles = std::max(tiles, gemm_tiles(c->dt, (int)M, (int)N));
-  };
-  acc(p.s_qkv, qkvN);
-  acc(p.s_o, c->W);
-  acc(p.s_gu, 2 * (size_t)c->F);
-  acc(p.s_d, c->W);
+  const size_t need = (size_t)std::max(p.s_o, p.s_d) * p.M * c->W;
   bool changed = false;
   if (need > c->partial_cap) {
     if (c->partial) (void)hipFree(c->partial);
@@ -614,15 +626,6 @@ jpi_status ensure_scratch(jpi_ctx* c, int batch, int prefix) {
     c->partial_cap = 0;
     TRY(dmalloc(c, (void**)&c->partial, need * sizeof(float)));
     c->partial_cap = need;
-    changed = true;
-  }
-  if (tiles > c->counters_cap) {
-    if (c->counters) (void)hipFree(c->counters);
-    c->counters = nullptr;
-    c->counters_cap = 0;
-    TRY(dmalloc(c, (void**)&c->counters, tiles * sizeof(unsigned)));
-    HIPCHK(c, hipMemset(c->counters, 0, tiles * sizeof(unsigned)));
-    c->counters_cap = tiles;
     changed = true;
   }
   const size_t nch = attn_n_chunks(c->dt, prefix, c->H);
@@ -654,41 +657,58 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     e = (x);                        \
     if (e != hipSuccess) return e;  \
   } while (0)
+  // optional event pairs around one kernel kind (measurement support)
+  const int need_ev = c->timed_kind >= 0 ? 2 * n_steps * L : 0;
+  while ((int)c->ev.size() < need_ev) {
+    hipEvent_t ev;
+    ENQ(hipEventCreate(&ev));
+    c->ev.push_back(ev);
+  }
+  c->ev_used = 0;
+  // events bracketing the timed kernel kind, taken on the dispatch itself
+  auto timing = [&](int kind, hipEvent_t* start, hipEvent_t* stop) {
+    *start = *stop = nullptr;
+    if (kind != c->timed_kind) return;
+    *start = c->ev[c->ev_used];
+    *stop = c->ev[c->ev_used + 1];
+    c->ev_used += 2;
+  };
   for (int k = 0; k < n_steps; ++k) {
     const float* tk = table + (size_t)k * c->R;
-    ENQ(launch_inproj(c->dt, c->x, c->w_in, c->b_in, c->h, M, W, c->A, s));
+    const float* fm = tk + (size_t)(6 * L) * W;
+    ENQ(launch_inproj_norm(c->dt, c->x, c->w_in, c->b_in, c->h, tk, tk + W, c->y, M, W, c->A, eps, s));
     for (int l = 0; l < L; ++l) {
       const char* lay = (const char*)c->w_layers + (size_t)l * c->layer_elems * es;
       const float* am = tk + (size_t)(2 * l) * 3 * W;
       const float* mm = tk + (size_t)(2 * l + 1) * 3 * W;
-      ENQ(launch_rmsnorm_mod(c->dt, c->h, am, am + W, c->y, M, W, eps, s));
+      // QKV + RoPE (y holds adaRMSNorm(h) with this layer's attention modulation)
       GemmLaunch g{};
-      g.partial = c->partial;
-      g.counters = c->counters;
       g.M = M;
-      // QKV + RoPE
       g.A = c->y;
       g.W = lay;
       g.N = (nH + 2) * Dh;
       g.K = W;
-      g.splitk = p.s_qkv;
+      g.splitk = 1;
       g.epi = EPI_QKV;
       g.ep.q = c->q;
       g.ep.ks = c->ks;
-      g.ep.vs = c->vs;
+      g.ep.vst = c->vst;
       g.ep.rope = c->rope_tab;
       g.ep.n_heads = nH;
       g.ep.head_dim = Dh;
       g.ep.horizon = H;
+      timing(JPI_KERNEL_QKV, &g.ev_start, &g.ev_stop);
       ENQ(launch_gemm(c->dt, g, s));
       // attention
       AttnLaunch a{};
       a.q = c->q;
       a.ks = c->ks;
-      a.vs = c->vs;
+      a.vst = c->vst;
       a.kp = (const char*)c->kp + (size_t)l * c->Bmax * c->Pmax * Dh * es;
-      a.vp = (const char*)c->vp + (size_t)l * c->Bmax * c->Pmax * Dh * es;
+      a.vpt = (const char*)c->vpt + (size_t)l * c->Bmax * c->Ppad * Dh * es;
       a.kp_bstride = (int64_t)c->Pmax * Dh;
+      a.vpt_bstride = (int64_t)c->Ppad * Dh;
+      a.vpt_dstride = c->Ppad;
       a.prefix_len = c->d_prefix_len;
       a.B = batch;
       a.nH = nH;
@@ -700,41 +720,77 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       a.lpart = a.mpart + (size_t)batch * nH * nch * H;
       a.out = c->o;
       a.out_f32 = 0;
+      timing(JPI_KERNEL_ATTENTION, &a.ev_start, &a.ev_stop);
       ENQ(launch_attention(c->dt, a, s));
-      // O projection + gated residual
+      // O projection (split-K slices) -> gated residual + MLP adaRMSNorm
+      g = GemmLaunch{};
+      g.M = M;
       g.A = c->o;
       g.W = lay + c->off_o * es;
       g.N = W;
       g.K = nH * Dh;
       g.splitk = p.s_o;
-      g.epi = EPI_RESID;
-      g.ep.h = c->h;
-      g.ep.gate = am + 2 * W;
+      g.epi = EPI_STORE_F32;
+      g.ep.out_f32 = c->partial;
+      timing(JPI_KERNEL_OPROJ, &g.ev_start, &g.ev_stop);
       ENQ(launch_gemm(c->dt, g, s));
-      // MLP
-      ENQ(launch_rmsnorm_mod(c->dt, c->h, mm, mm + W, c->y, M, W, eps, s));
+      RowLaunch r{};
+      r.part = c->partial;
+      r.S = p.s_o;
+      r.M = M;
+      r.W = W;
+      r.h = c->h;
+      r.gate = am + 2 * W;
+      r.scale = mm;
+      r.shift = mm + W;
+      r.y = c->y;
+      r.eps = eps;
+      ENQ(launch_resid_norm(c->dt, r, false, s));
+      // GateUp + GeGLU
+      g = GemmLaunch{};
+      g.M = M;
       g.A = c->y;
       g.W = lay + c->off_gu * es;
       g.N = 2 * F;
       g.K = W;
-      g.splitk = p.s_gu;
+      g.splitk = 1;
       g.epi = EPI_GEGLU;
       g.ep.z = c->z;
       g.ep.mlp_dim = F;
+      timing(JPI_KERNEL_GATEUP, &g.ev_start, &g.ev_stop);
       ENQ(launch_gemm(c->dt, g, s));
+      // Down (split-K slices) -> gated residual + next norm (or final head + Euler)
+      g = GemmLaunch{};
+      g.M = M;
       g.A = c->z;
       g.W = lay + c->off_d * es;
       g.N = W;
       g.K = F;
       g.splitk = p.s_d;
-      g.epi = EPI_RESID;
-      g.ep.h = c->h;
-      g.ep.gate = mm + 2 * W;
+      g.epi = EPI_STORE_F32;
+      g.ep.out_f32 = c->partial;
+      timing(JPI_KERNEL_DOWN, &g.ev_start, &g.ev_stop);
       ENQ(launch_gemm(c->dt, g, s));
+      r.S = p.s_d;
+      r.gate = mm + 2 * W;
+      const bool last = l == L - 1;
+      if (!last) {
+        const float* an = tk + (size_t)(2 * (l + 1)) * 3 * W;
+        r.scale = an;
+        r.shift = an + W;
+      } else {
+        r.scale = fm;
+        r.shift = fm + W;
+        r.w_out = c->w_out;
+        r.b_out = c->b_out;
+        r.x = c->x;
+        r.A = c->A;
+        r.horizon = H;
+        r.n_fixed = c->n_fixed;
+        r.dt = dt_step;
+      }
+      ENQ(launch_resid_norm(c->dt, r, last, s));
     }
-    const float* fm = tk + (size_t)(6 * L) * W;
-    ENQ(launch_final_euler(c->dt, c->h, fm, fm + W, c->w_out, c->b_out, c->x, M, W, c->A, H, c->n_fixed, dt_step,
-                           eps, s));
   }
 #undef ENQ
   return hipSuccess;
@@ -761,7 +817,7 @@ jpi_status jpi_denoise(jpi_ctx* c, const float* noise_dev, int n_steps, float* a
   TRY(ensure_table(c, n_steps, s, &table));
   TRY(ensure_scratch(c, c->batch, c->prefix));
   HIPCHK(c, launch_init_x(noise_dev, c->committed, c->x, c->batch, c->H, c->A, c->n_fixed, s));
-  if (eager_mode()) {
+  if (eager_mode() || c->timed_kind >= 0) {
     HIPCHK(c, enqueue_steps(c, table, n_steps, s));
   } else {
     const GraphKey key{c->batch, c->prefix, n_steps, c->n_fixed};
@@ -797,14 +853,40 @@ jpi_status jpi_sync(jpi_ctx* c, void* stream) {
   return JPI_OK;
 }
 
+jpi_status jpi_debug_time_kernel(jpi_ctx* c, int kind) {
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_time_kernel: ctx is NULL");
+  if (kind < JPI_KERNEL_NONE || kind > JPI_KERNEL_DOWN) return fail(c, JPI_ERR_ARG, "jpi_debug_time_kernel: bad kind");
+  HIPCHK(c, hipSetDevice(c->device));
+  HIPCHK(c, hipDeviceSynchronize());
+  drop_graphs(c);
+  c->timed_kind = kind;
+  c->ev_used = 0;
+  return JPI_OK;
+}
+
+jpi_status jpi_debug_kernel_time(jpi_ctx* c, float* total_ms, int* launches) {
+  if (!c || !total_ms || !launches) return fail(c, JPI_ERR_ARG, "jpi_debug_kernel_time: NULL argument");
+  if (c->timed_kind < 0) return fail(c, JPI_ERR_STATE, "jpi_debug_kernel_time: timing is off");
+  HIPCHK(c, hipSetDevice(c->device));
+  float tot = 0.f;
+  for (int i = 0; i + 1 < c->ev_used; i += 2) {
+    float ms = 0.f;
+    HIPCHK(c, hipEventElapsedTime(&ms, c->ev[i], c->ev[i + 1]));
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = c->ev_used / 2;
+  return JPI_OK;
+}
+
 jpi_status jpi_debug_gemm(const void* A, const void* Wt, float* C, int M, int N, int K, jpi_dtype dt, int splitk,
                           void* stream) {
   if (!A || !Wt || !C) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_gemm: NULL pointer");
   if (M < 1 || N < 1 || K < 1 || splitk < 1) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_gemm: sizes must be >= 1");
   if (dt != JPI_F32 && dt != JPI_BF16) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_gemm: bad dtype");
-  const int BK = dt == JPI_BF16 ? 64 : 32;
-  if (K % (BK * splitk) != 0)
-    return fail(nullptr, JPI_ERR_ARG, "jpi_debug_gemm: K must be a multiple of " + std::to_string(BK) + "*splitk");
+  const int q = gemm_k_quantum(dt, M);
+  if (K % (q * splitk) != 0)
+    return fail(nullptr, JPI_ERR_ARG, "jpi_debug_gemm: K must be a multiple of " + std::to_string(q) + "*splitk");
   hipStream_t s = (hipStream_t)stream;
   GemmLaunch g{};
   g.A = A;
@@ -815,20 +897,21 @@ jpi_status jpi_debug_gemm(const void* A, const void* Wt, float* C, int M, int N,
   g.splitk = splitk;
   g.epi = EPI_STORE_F32;
   g.ep.out_f32 = C;
-  const size_t tiles = gemm_tiles(dt, M, N);
-  hipError_t ea = hipMalloc((void**)&g.counters, tiles * sizeof(unsigned));
-  if (ea != hipSuccess) {
-    (void)hipGetLastError();
-    return fail(nullptr, ea == hipErrorOutOfMemory ? JPI_ERR_OOM : JPI_ERR_HIP,
-                std::string("jpi_debug_gemm: counters: ") + hipGetErrorString(ea));
+  float* part = nullptr;
+  hipError_t e = hipSuccess;
+  if (splitk > 1) {
+    e = hipMalloc((void**)&part, (size_t)splitk * M * N * sizeof(float));
+    g.ep.out_f32 = part;
   }
-  hipError_t e = hipMemsetAsync(g.counters, 0, tiles * sizeof(unsigned), s);
-  if (e == hipSuccess && splitk > 1) e = hipMalloc((void**)&g.partial, (size_t)splitk * M * N * sizeof(float));
   if (e == hipSuccess) e = launch_gemm(dt, g, s);
+  if (e == hipSuccess && splitk > 1) e = launch_sum_slices(part, C, splitk, (size_t)M * N, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
-  if (g.partial) (void)hipFree(g.partial);
-  (void)hipFree(g.counters);
-  if (e != hipSuccess) return fail(nullptr, JPI_ERR_HIP, std::string("jpi_debug_gemm: ") + hipGetErrorString(e));
+  if (part) (void)hipFree(part);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(nullptr, e == hipErrorOutOfMemory ? JPI_ERR_OOM : JPI_ERR_HIP,
+                std::string("jpi_debug_gemm: ") + hipGetErrorString(e));
+  }
   return JPI_OK;
 }
 
@@ -840,29 +923,43 @@ jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, co
   if (batch < 1 || n_heads < 1 || H < 1 || P < 0 || (Dh != 64 && Dh != 128 && Dh != 256))
     return fail(nullptr, JPI_ERR_ARG, "jpi_debug_attention: bad sizes");
   if (dt != JPI_F32 && dt != JPI_BF16) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_attention: bad dtype");
+  if (P > attn_max_prefix(dt, H)) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_attention: prefix too long");
   for (int b = 0; b < batch; ++b)
     if (prefix_len_host[b] < 0 || prefix_len_host[b] > P)
       return fail(nullptr, JPI_ERR_ARG, "jpi_debug_attention: prefix_len out of range");
   hipStream_t s = (hipStream_t)stream;
+  const size_t es = dt == JPI_BF16 ? 2 : 4;
   const int nch = attn_n_chunks(dt, P, H);
+  const int Ppad = (P + 7) / 8 * 8 > 0 ? (P + 7) / 8 * 8 : 8;
   int* dlen = nullptr;
   float* part = nullptr;
+  void *vpt = nullptr, *vst = nullptr;
   const size_t np = (size_t)batch * n_heads * nch * H * (Dh + 2);
   hipError_t ea = hipMalloc((void**)&dlen, batch * sizeof(int));
   if (ea == hipSuccess) ea = hipMalloc((void**)&part, np * sizeof(float));
+  if (ea == hipSuccess) ea = hipMalloc(&vpt, (size_t)batch * Dh * Ppad * es);
+  if (ea == hipSuccess) ea = hipMalloc(&vst, (size_t)batch * Dh * H * es);
+  auto cleanup = [&]() {
+    if (dlen) (void)hipFree(dlen);
+    if (part) (void)hipFree(part);
+    if (vpt) (void)hipFree(vpt);
+    if (vst) (void)hipFree(vst);
+  };
   if (ea != hipSuccess) {
     (void)hipGetLastError();
-    if (dlen) (void)hipFree(dlen);
+    cleanup();
     return fail(nullptr, ea == hipErrorOutOfMemory ? JPI_ERR_OOM : JPI_ERR_HIP,
                 std::string("jpi_debug_attention: scratch: ") + hipGetErrorString(ea));
   }
   AttnLaunch a{};
   a.q = q;
   a.ks = ks;
-  a.vs = vs;
+  a.vst = vst;
   a.kp = kp ? kp : ks;
-  a.vp = vp ? vp : vs;
+  a.vpt = vpt;
   a.kp_bstride = (int64_t)P * Dh;
+  a.vpt_bstride = (int64_t)Ppad * Dh;
+  a.vpt_dstride = Ppad;
   a.prefix_len = dlen;
   a.B = batch;
   a.nH = n_heads;
@@ -875,10 +972,12 @@ jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, co
   a.out = out;
   a.out_f32 = 1;
   hipError_t e = hipMemcpyAsync(dlen, prefix_len_host, batch * sizeof(int), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && P > 0)
+    e = launch_transpose(dt, vp, vpt, P, Dh, Dh, Ppad, (int64_t)P * Dh, (int64_t)Dh * Ppad, batch, s);
+  if (e == hipSuccess) e = launch_transpose(dt, vs, vst, H, Dh, Dh, H, (int64_t)H * Dh, (int64_t)Dh * H, batch, s);
   if (e == hipSuccess) e = launch_attention(dt, a, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
-  (void)hipFree(dlen);
-  (void)hipFree(part);
+  cleanup();
   if (e != hipSuccess) return fail(nullptr, JPI_ERR_HIP, std::string("jpi_debug_attention: ") + hipGetErrorString(e));
   return JPI_OK;
 }

@@ -20,7 +20,8 @@ JPI_F32, JPI_BF16 = 0, 1
 
 EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create", "jpi_destroy", "jpi_set_weight",
             "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
-            "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention"]
+            "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time"]
+JPI_KERNEL_NONE, JPI_KERNEL_QKV, JPI_KERNEL_ATTENTION, JPI_KERNEL_OPROJ, JPI_KERNEL_GATEUP, JPI_KERNEL_DOWN = range(-1, 5)
 
 
 class jpi_config(ctypes.Structure):
@@ -58,6 +59,8 @@ _sig = {
     "jpi_sync": (_i, [_vp, _vp]),
     "jpi_debug_gemm": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "jpi_debug_attention": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
+    "jpi_debug_time_kernel": (_i, [_vp, _i]),
+    "jpi_debug_kernel_time": (_i, [_vp, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_i)]),
 }
 for _name, (_res, _args) in _sig.items():
     _fn = getattr(_lib, _name)
@@ -159,6 +162,16 @@ def jpi_debug_attention(q, ks, vs, kp, vp, prefix_len_host, batch, n_heads, H, P
     lens = _i32_host(prefix_len_host)
     return _lib.jpi_debug_attention(addr(q), addr(ks), addr(vs), addr(kp), addr(vp), lens.ctypes.data, batch, n_heads,
                                     H, P, Dh, dtype, addr(out), stream_handle(stream))
+
+
+def jpi_debug_time_kernel(ctx, kind: int) -> int:
+    return _lib.jpi_debug_time_kernel(ctx, kind)
+
+
+def jpi_debug_kernel_time(ctx):
+    ms, n = ctypes.c_float(), _i()
+    st = _lib.jpi_debug_kernel_time(ctx, ctypes.byref(ms), ctypes.byref(n))
+    return st, ms.value, n.value
 
 
 class JpiError(RuntimeError):

