@@ -163,7 +163,9 @@ jpi_status jpi_bind_state(jpi_ctx* ctx, const float* committed_dev, int n_fixed,
  * finalized or no prefix bound), JPI_ERR_ARG (NULL, n_steps < 1). */
 jpi_status jpi_denoise(jpi_ctx* ctx, const float* noise_dev, int n_steps, float* actions_dev, void* stream);
 
-/* Synchronise `stream` and report asynchronous HIP errors as JPI_ERR_HIP. */
+/* Synchronise `stream` and report asynchronous HIP errors as JPI_ERR_HIP,
+ * including a barrier wait of the single-launch denoise kernel that timed
+ * out (its output is then invalid). */
 jpi_status jpi_sync(jpi_ctx* ctx, void* stream);
 
 /* ---- kernel-level entry points used by the parity tests ------------------ */
@@ -195,7 +197,8 @@ typedef enum {
   JPI_KERNEL_ATTENTION = 1,  /* prefix+self attention (chunk pass and combine) */
   JPI_KERNEL_OPROJ = 2,      /* attention output x W_o, gated residual */
   JPI_KERNEL_GATEUP = 3,     /* activations x [gate|up], GeGLU epilogue */
-  JPI_KERNEL_DOWN = 4        /* GeGLU output x W_down, gated residual */
+  JPI_KERNEL_DOWN = 4,       /* GeGLU output x W_down, gated residual */
+  JPI_KERNEL_PERSISTENT = 5  /* the single-launch denoise kernel (batch*horizon <= 64, bf16) */
 } jpi_kernel_kind;
 
 /* Ask jpi_denoise to record a pair of HIP events around every launch of

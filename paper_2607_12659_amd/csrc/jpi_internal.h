@@ -97,6 +97,48 @@ hipError_t launch_transpose(jpi_dtype dt, const void* src, void* dst, int rows, 
                             int64_t sz, int64_t dz, int nmat, hipStream_t s);
 hipError_t launch_attention(jpi_dtype dt, const AttnLaunch& a, hipStream_t s);
 
+// Persistent single-launch denoise (jpi_persist.hip), M <= 64, bf16.
+struct PersistArgs {
+  int L, W, nH, Dh, F, A, H, B, M;
+  int C;                    // attention chunks (32 keys) per rollout
+  int n_steps, n_fixed, s_o, s_d, R;
+  float eps, dt;
+  const void* w_layers;     // packed layer weights (bf16)
+  int64_t layer_elems, off_o, off_gu, off_d;
+  const void* w_in;
+  const float* b_in;
+  const void* w_out;
+  const float* b_out;
+  const float* table;       // [n_steps][R] modulation
+  const void* kp;           // prefix K [L][Bmax][Pmax][Dh]
+  const void* vpt;          // prefix V transposed [L][Bmax][Dh][Ppad]
+  int64_t kp_lstride, kp_bstride, vpt_lstride, vpt_bstride, vpt_dstride;
+  const int* prefix_len;    // [B]
+  const float2* rope;       // [B][H][Dh/2]
+  float* x;                 // [M][A]
+  float* h;                 // [M][W]
+  void* y;                  // [M][W] bf16
+  void* q;                  // [B][nH][H][Dh]
+  void* ks;                 // [B][H][Dh]
+  void* vst;                // [B][Dh][H]
+  float* opart;             // [B][nH][C][H][Dh]
+  float* ml;                // [B][nH][C][H][2]
+  void* o;                  // [M][nH*Dh]
+  float* part;              // [max(s_o, s_d)][M][W]
+  void* z;                  // [M][F]
+  unsigned* flags;          // [grid][32] barrier arrival epochs
+  unsigned* err;            // set to 1 if a barrier wait timed out
+  hipEvent_t ev_start, ev_stop;
+};
+bool persist_supported(jpi_dtype dt, int M, int W, int nH, int Dh, int F, int H, int A, int Pmax);
+int persist_chunks(int P, int H);
+int persist_pick_split(int tiles, int K, int grid);
+int persist_block_threads();
+int persist_max_grid();    // largest grid the barrier supports
+int persist_flag_words();  // size of the barrier flag buffer in 32-bit words
+hipError_t persist_occupancy(int Dh, int* blocks_per_cu);
+hipError_t launch_persist(const PersistArgs& a, int grid, hipStream_t s);
+
 hipError_t launch_time_embed(const float* t, float* emb, int n, int W, hipStream_t s);
 // out[m][n] = act(sum_k in[m][k] w[n][k] + b[n]), fp64 accumulation; act 0 = none, 1 = swish
 hipError_t launch_rowdot(jpi_dtype dt, const float* in, const void* w, const float* b, float* out, int M,

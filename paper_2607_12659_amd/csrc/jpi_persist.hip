@@ -1,0 +1,781 @@
+// Persistent single-launch denoise for small batches (M = batch * horizon <= 64,
+// bf16 weights).  One workgroup per compute unit runs every Euler step of the
+// flow-matching loop and every layer of the action expert (paper: Appendix
+// "Model Architecture of pi series Models" for the expert, Section "System
+// Design" for running all denoising steps as one unrolled unit); phases are
+// separated by a grid-wide barrier.
+//
+// Phases of one layer (items are distributed over the workgroups):
+//   0 QKV     adaRMSNorm'd activations y x packed [q|k|v] weights, RoPE
+//             epilogue; the action rows' V goes into the transposed prefix V
+//             buffer right after each rollout's valid prefix
+//   1 ATTN    (rollout, head, 32-key chunk) items over prefix + action keys:
+//             per-chunk max / sum / unnormalised output
+//   2 COMB    chunk combine per (rollout, head, query row) -> o
+//   3 OPROJ   o x W_o, split-K slices -> part
+//   4 ROWS    row owner: residual += gate * sum of slices; MLP adaRMSNorm -> y
+//   5 GATEUP  y x [gate|up], GeGLU epilogue -> z
+//   6 DOWN    z x W_down, split-K slices -> part
+//   7 ROWS    row owner: residual update + next layer's attention norm, or
+//             (last layer) final norm, action-out projection, Euler update
+//             of x and the next step's in-projection + first norm
+//
+// Code size: every phase has exactly one call site (the kernel loops over a
+// phase index) and the four GEMM phases share one GEMM body, so the kernel
+// stays within the instruction cache; a phase whose code was evicted since
+// the previous layer pays instruction-fetch latency on every new cache line.
+//
+// Row ownership: workgroup m < M owns action row m.  Its residual row, the
+// in-projection weights (transposed) and b_in live in LDS for the whole
+// launch and x[m][a] lives in a register of thread a.
+//
+// Memory model: data that one workgroup writes and another reads within the
+// launch (activations, slices, attention partials, the action rows' K and V,
+// barrier flags) is stored and loaded with device-scope coherent buffer
+// accesses (cache policy sc1); a barrier arrival is stored only after
+// s_waitcnt vmcnt(0) confirms the workgroup's stores.  No agent-scope fences
+// are used (on gfx950 they serialise across the chip).  Weights, the prefix K,
+// the prefix part of the transposed V, the modulation table and the RoPE
+// table are read-only during the launch and use plain loads.
+//
+// Every barrier wait is bounded: after SPIN_LIMIT polls the workgroup records
+// an error word and stops waiting, so a launch always terminates; the host
+// reports the error from jpi_sync.
+#include "jpi_device.h"
+#include "jpi_internal.h"
+
+namespace jpi {
+
+namespace {
+
+constexpr int PT = 256;  // threads per workgroup (one wave per SIMD)
+constexpr int NWV = PT / 64;
+constexpr int CPOL_DEV = 16;  // sc1: device-scope coherent access
+constexpr int KC = 32;        // keys per attention chunk
+constexpr int MAX_CH = 128;   // attention chunks per rollout
+constexpr unsigned SPIN_LIMIT = 1u << 21;
+constexpr int SMEM_BYTES = 48 * 1024;  // per-phase scratch
+constexpr int MAX_W = 2048;            // model width held in LDS by a row owner
+constexpr int WIN_ELEMS = 32768;       // in-projection weights held in LDS (A * W)
+constexpr int RMAX_S = 16;             // split-K slices summed by the row phases
+constexpr int MAX_GRID = 256;          // barrier flags are polled as 64 lanes x 4 lines
+constexpr int FLAG_STRIDE = 32;        // words between barrier flags: one 128-byte line per workgroup
+constexpr int FLAG_WORDS = MAX_GRID * FLAG_STRIDE;
+constexpr int CPT = 8;     // combine: chunks per thread per round trip
+constexpr int OUT_G = 16;  // action-out projection: 16-byte weight granules per thread
+
+enum : int { EPI_QKV = 0, EPI_GEGLU = 1, EPI_SLICE = 2 };
+
+typedef unsigned u32;
+typedef u32 u32x2 __attribute__((ext_vector_type(2)));
+typedef u32 u32x4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+// Buffer resource over [base, base + bytes): loads beyond the range return
+// zero and stores beyond it are dropped.
+__device__ __forceinline__ rsrc_t rsrc(const void* base, u32 bytes = 0x7fffffffu) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 ld16(rsrc_t r, u32 off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, CPOL_DEV);
+}
+// Bit casts take scalars by value: with this compiler, __builtin_bit_cast
+// applied directly to an element of an ext_vector_type value (v[i]) reads
+// element 0 whatever the index.
+__device__ __forceinline__ u32 f2u(float v) { return __builtin_bit_cast(u32, v); }
+__device__ __forceinline__ float u2f(u32 v) { return __builtin_bit_cast(float, v); }
+__device__ __forceinline__ float2 ld8f(rsrc_t r, u32 off) {
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, CPOL_DEV));
+}
+// A polling load: the empty asm with a memory clobber keeps the compiler from
+// treating the load as loop-invariant and hoisting it out of the wait loop.
+__device__ __forceinline__ u32 poll4(rsrc_t r, u32 off) {
+  asm volatile("" ::: "memory");
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, CPOL_DEV);
+}
+__device__ __forceinline__ void st4(rsrc_t r, u32 off, u32 v) { __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, CPOL_DEV); }
+__device__ __forceinline__ void st8(rsrc_t r, u32 off, u32x2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, CPOL_DEV);
+}
+__device__ __forceinline__ u32 bf16_bits(float v) { return __builtin_bit_cast(unsigned short, static_cast<bf16>(v)); }
+__device__ __forceinline__ void st_bf16(rsrc_t r, u32 off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b16((unsigned short)bf16_bits(v), r, off, 0, CPOL_DEV);
+}
+__device__ __forceinline__ u32x2 pack4_bf16(f32x4 v) {
+  return u32x2{bf16_bits(v[0]) | (bf16_bits(v[1]) << 16), bf16_bits(v[2]) | (bf16_bits(v[3]) << 16)};
+}
+__device__ __forceinline__ float bf16_lo(u32 w) { return u2f(w << 16); }
+__device__ __forceinline__ float bf16_hi(u32 w) { return u2f(w & 0xffff0000u); }
+__device__ __forceinline__ f32x4 as_f4(u32x4 v) { return __builtin_bit_cast(f32x4, v); }
+
+// Fixed-order sum over the waves of a workgroup.
+__device__ __forceinline__ float block_sum_wg(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float t = red[0];
+#pragma unroll
+  for (int i = 1; i < NWV; ++i) t += red[i];
+  return t;
+}
+
+// Grid barrier.  Each workgroup stores its arrival epoch into its own 128-byte
+// flag line; wave 0 of every workgroup then polls all lines (lane l reads the
+// lines of workgroups l, l+64, l+128, l+192 with independent loads).
+__device__ __forceinline__ void grid_sync(const PersistArgs& a, u32 epoch, u32* s_abort) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const rsrc_t rf = rsrc(a.flags);
+    if (threadIdx.x == 0) st4(rf, blockIdx.x * (FLAG_STRIDE * 4u), epoch);
+    if (*s_abort == 0u) {
+      const u32 g = gridDim.x;
+      for (u32 spins = 0;; ++spins) {
+        u32 f[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const u32 b = threadIdx.x + 64u * u;
+          f[u] = b < g ? poll4(rf, b * (FLAG_STRIDE * 4u)) : epoch;
+        }
+        if (__all(f[0] >= epoch && f[1] >= epoch && f[2] >= epoch && f[3] >= epoch)) break;
+        if (spins > SPIN_LIMIT) {
+          if (threadIdx.x == 0) {
+            *s_abort = 1u;
+            st4(rsrc(a.err), 0, 1u);
+          }
+          break;
+        }
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// GEMM item: rows 0..63 x 32 output columns [n0, n0+32) over the K range
+// [kbeg, kbeg + klen), split evenly over the waves.  `ra` covers exactly the
+// M valid rows of the bf16 activation matrix A (leading dimension lda), so the
+// rows >= M of the 64-row tile read as zero without a branch.  W is packed
+// bf16 weights [N][ldw].  Returns the sums for m-subtile `wave` in lo
+// (columns n0 + lane%16) and hi (n0 + 16 + lane%16).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void gemm_item(rsrc_t ra, int lda, const bf16* W, int ldw, int n0, int kbeg, int klen,
+                                          f32x4* red, f32x4& lo, f32x4& hi) {
+  using MF = Mfma<bf16>;
+  constexpr int BATCH = 8;
+  static_assert(NWV == 4, "one m-subtile of the 64-row tile per wave");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int fr = lane & 15, fk = (lane >> 4) * MF::KPL;
+  const int kw = klen / NWV;
+  const int k0 = kbeg + wave * kw;
+  const int nsub = kw / MF::KSUB;
+  const bf16* wp0 = W + (size_t)(n0 + fr) * ldw + k0 + fk;
+  const bf16* wp1 = wp0 + (size_t)16 * ldw;
+  const u32 aoff = (u32)(((size_t)fr * lda + k0 + fk) * 2);
+  const u32 astep = (u32)(16 * lda * 2);
+  f32x4 acc[4][2];
+#pragma unroll
+  for (int a = 0; a < 4; ++a) acc[a][0] = acc[a][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < nsub; s0 += BATCH) {
+    MF::frag wf[BATCH][2], af[BATCH][4];
+#pragma unroll
+    for (int c = 0; c < BATCH; ++c) {
+      const bool ok = s0 + c < nsub;
+      wf[c][0] = ok ? MF::load(wp0 + (s0 + c) * MF::KSUB) : MF::frag{};
+      wf[c][1] = ok ? MF::load(wp1 + (s0 + c) * MF::KSUB) : MF::frag{};
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+        af[c][a] = ok ? __builtin_bit_cast(MF::frag, ld16(ra, aoff + a * astep + (u32)((s0 + c) * MF::KSUB * 2)))
+                      : MF::frag{};
+    }
+#pragma unroll
+    for (int c = 0; c < BATCH; ++c)
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        acc[a][0] = MF::run(af[c][a], wf[c][0], acc[a][0]);
+        acc[a][1] = MF::run(af[c][a], wf[c][1], acc[a][1]);
+      }
+  }
+  // red layout [wave][a][2][64]
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    red[((wave * 4 + a) * 2 + 0) * 64 + lane] = acc[a][0];
+    red[((wave * 4 + a) * 2 + 1) * 64 + lane] = acc[a][1];
+  }
+  __syncthreads();
+  lo = red[((0 * 4 + wave) * 2 + 0) * 64 + lane];
+  hi = red[((0 * 4 + wave) * 2 + 1) * 64 + lane];
+#pragma unroll
+  for (int v = 1; v < NWV; ++v) {
+    lo += red[((v * 4 + wave) * 2 + 0) * 64 + lane];
+    hi += red[((v * 4 + wave) * 2 + 1) * 64 + lane];
+  }
+  __syncthreads();  // red is reused by the next item
+}
+
+struct GemmJob {
+  const void* A;  // activations [M][K] bf16
+  const bf16* w;  // weights [N][K] bf16
+  int K;          // reduction length (also the leading dimension of A and w)
+  int tiles;      // N / 32
+  int S;          // split-K slices
+  int kind;       // EPI_*
+};
+
+// ---- phases 0, 3, 5, 6: GEMM with a per-kind epilogue ----------------------
+__device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& j, int l, char* smem) {
+  f32x4* red = reinterpret_cast<f32x4*>(smem);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, fr = lane & 15;
+  const int Dh = a.Dh, half = Dh / 2, H = a.H, nH = a.nH, qcols = nH * Dh, M = a.M, Wd = a.W;
+  const int klen = j.K / j.S;
+  const rsrc_t ra = rsrc(j.A, (u32)(M * j.K * 2));
+  const rsrc_t rq = rsrc(a.q), rk = rsrc(a.ks), rz = rsrc(a.z), rp = rsrc(a.part);
+  const rsrc_t rv = rsrc(reinterpret_cast<const bf16*>(a.vpt) + (size_t)l * a.vpt_lstride);
+  for (int it = blockIdx.x; it < j.tiles * j.S; it += gridDim.x) {
+    const int t = it % j.tiles, s = it / j.tiles;
+    const int col = t * 32 + fr;  // column of lo; hi is col + 16
+    // QKV: q/k columns are packed so that a RoPE pair (d, d + Dh/2) sits in
+    // lo/hi of one lane.  The rotation factors and the prefix lengths do not
+    // depend on the GEMM, so their loads are issued first.
+    const bool qkv = j.kind == EPI_QKV;
+    const bool roped = qkv && col < qcols + Dh;
+    const int hn = col < qcols ? col / Dh : -1;
+    const int within = col < qcols ? col - hn * Dh : col - qcols;
+    const int d = (within >> 5) * 16 + (within & 15);
+    float2 cs[4];
+    int plv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int row = wave * 16 + (lane >> 4) * 4 + e;
+      cs[e] = (roped && row < M) ? a.rope[(size_t)row * half + d] : float2{1.f, 0.f};
+      plv[e] = (qkv && !roped && row < M) ? a.prefix_len[row / H] : 0;
+    }
+    f32x4 lo, hi;
+    gemm_item(ra, j.K, j.w, j.K, t * 32, s * klen, klen, red, lo, hi);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int row = wave * 16 + (lane >> 4) * 4 + e;
+      if (row >= M) continue;
+      if (j.kind == EPI_SLICE) {
+        const u32 base = (u32)(((size_t)s * M + row) * Wd + col) * 4u;
+        st4(rp, base, f2u(lo[e]));
+        st4(rp, base + 64u, f2u(hi[e]));
+      } else if (j.kind == EPI_GEGLU) {  // gate/up rows interleaved in 16-row groups
+        st_bf16(rz, (u32)((size_t)row * a.F + t * 16 + fr) * 2u, gelu_tanh(lo[e]) * hi[e]);
+      } else {
+        const int b = row / H, i = row - b * H;
+        if (roped) {
+          const float r_lo = lo[e] * cs[e].x - hi[e] * cs[e].y;
+          const float r_hi = lo[e] * cs[e].y + hi[e] * cs[e].x;
+          const u32 base = hn >= 0 ? (u32)((((size_t)b * nH + hn) * H + i) * Dh) : (u32)(((size_t)b * H + i) * Dh);
+          const rsrc_t rd = hn >= 0 ? rq : rk;
+          st_bf16(rd, (base + d) * 2u, r_lo);
+          st_bf16(rd, (base + d + half) * 2u, r_hi);
+        } else {
+          // V of action row i: transposed prefix V buffer at key prefix_len + i
+          const int dv = col - qcols - Dh;
+          const u32 off = (u32)((size_t)b * a.vpt_bstride + (size_t)dv * a.vpt_dstride + plv[e] + i) * 2u;
+          st_bf16(rv, off, lo[e]);
+          st_bf16(rv, off + (u32)(16 * a.vpt_dstride * 2), hi[e]);
+        }
+      }
+    }
+  }
+}
+
+// ---- phase 1: attention chunk partials ----------------------------------------
+template <int DH>
+__device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* smem) {
+  using MF = Mfma<bf16>;
+  constexpr int PAD = 8, LDK = DH + PAD, LDV = KC + PAD, LDP = KC + PAD;
+  constexpr int NST = DH / MF::KSUB, NJ = KC / 16;
+  constexpr int KCH = KC * (DH / 8) / PT, VCH = DH * (KC / 8) / PT;
+  static_assert(KCH >= 1 && VCH >= 1, "chunk too small for the workgroup");
+  static_assert((KC * LDK + DH * LDV + 64 * LDP) * 2 <= SMEM_BYTES, "attention LDS");
+  bf16* Ks = reinterpret_cast<bf16*>(smem);
+  bf16* Vt = Ks + KC * LDK;
+  bf16* Ps = Vt + DH * LDV;  // [64][LDP]
+  const int H = a.H, nH = a.nH, C = a.C;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int fr = lane & 15, fk = (lane >> 4) * MF::KPL;
+  const int n_items = a.B * nH * C;
+  const bf16* kpl = reinterpret_cast<const bf16*>(a.kp) + (size_t)l * a.kp_lstride;
+  const bf16* vpl = reinterpret_cast<const bf16*>(a.vpt) + (size_t)l * a.vpt_lstride;
+  const rsrc_t rv = rsrc(vpl), rks = rsrc(a.ks), rq = rsrc(a.q), ro = rsrc(a.opart), rml = rsrc(a.ml);
+  for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+    const int c = it % C, hn = (it / C) % nH, b = it / (C * nH);
+    const int pl = a.prefix_len[b];
+    const int nkeys = pl + H;
+    const int kbase = c * KC;
+    if (kbase >= nkeys) continue;  // uniform across the workgroup; combine skips it
+    const bf16* kp = kpl + (size_t)b * a.kp_bstride;
+    const bf16* vb = vpl + (size_t)b * a.vpt_bstride;
+    const u32 vboff = (u32)((size_t)b * a.vpt_bstride * 2);
+    u32x4 kr[KCH], vr[VCH];
+#pragma unroll
+    for (int u = 0; u < KCH; ++u) {
+      const int e = tid + u * PT, r = e / (DH / 8), cc = e - r * (DH / 8);
+      const int key = kbase + r;
+      if (key < pl) kr[u] = *reinterpret_cast<const u32x4*>(kp + (size_t)key * DH + cc * 8);
+      else if (key < nkeys) kr[u] = ld16(rks, (u32)((((size_t)b * H + (key - pl)) * DH + cc * 8) * 2));
+      else kr[u] = u32x4{0u, 0u, 0u, 0u};
+    }
+    // V^T rows: keys < prefix_len were bound before the launch (plain loads);
+    // the action keys were written by this launch (coherent loads); keys past
+    // the end are zeroed so that stale memory never meets a zero probability.
+#pragma unroll
+    for (int u = 0; u < VCH; ++u) {
+      const int e = tid + u * PT, d = e / (KC / 8), kc = e - d * (KC / 8);
+      const int key0 = kbase + kc * 8;
+      if (key0 + 8 <= pl) {
+        vr[u] = *reinterpret_cast<const u32x4*>(vb + (size_t)d * a.vpt_dstride + key0);
+      } else if (key0 < nkeys) {
+        u32x4 v = ld16(rv, vboff + (u32)(((size_t)d * a.vpt_dstride + key0) * 2));
+        const int n_ok = nkeys - key0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          v[q] &= (2 * q < n_ok ? 0x0000ffffu : 0u) | (2 * q + 1 < n_ok ? 0xffff0000u : 0u);
+        vr[u] = v;
+      } else {
+        vr[u] = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+    // wave w: query rows w*16 .. +16 of head hn
+    const int iq = w * 16 + fr;
+    MF::frag qf[NST];
+#pragma unroll
+    for (int st = 0; st < NST; ++st)
+      qf[st] = iq < H ? __builtin_bit_cast(
+                            MF::frag, ld16(rq, (u32)(((((size_t)b * nH + hn) * H + iq) * DH + st * MF::KSUB + fk) * 2)))
+                      : MF::frag{};
+#pragma unroll
+    for (int u = 0; u < KCH; ++u) {
+      const int e = tid + u * PT, r = e / (DH / 8), cc = e - r * (DH / 8);
+      *reinterpret_cast<u32x4*>(&Ks[r * LDK + cc * 8]) = kr[u];
+    }
+#pragma unroll
+    for (int u = 0; u < VCH; ++u) {
+      const int e = tid + u * PT, d = e / (KC / 8), kc = e - d * (KC / 8);
+      *reinterpret_cast<u32x4*>(&Vt[d * LDV + kc * 8]) = vr[u];
+    }
+    __syncthreads();
+    f32x4 sc[NJ];
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj) sc[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < NST; ++st)
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj)
+        sc[jj] = MF::run(qf[st], MF::load(&Ks[(jj * 16 + fr) * LDK + st * MF::KSUB + fk]), sc[jj]);
+    const float scale = 1.0f / sqrtf((float)DH);
+    float mrow[4], lrow[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj) {
+        const int key = kbase + jj * 16 + fr;
+        const float v = key < nkeys ? sc[jj][e] * scale : -INFINITY;
+        sc[jj][e] = v;
+        mx = fmaxf(mx, v);
+      }
+      mx = group16_max(mx);
+      float sum = 0.f;
+#pragma unroll
+      for (int jj = 0; jj < NJ; ++jj) {
+        const float p = mx == -INFINITY ? 0.f : expf(sc[jj][e] - mx);
+        sc[jj][e] = p;
+        sum += p;
+      }
+      mrow[e] = mx;
+      lrow[e] = group16_sum(sum);
+    }
+    const int prow = w * 16 + (lane >> 4) * 4;
+#pragma unroll
+    for (int jj = 0; jj < NJ; ++jj)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Ps[(prow + e) * LDP + jj * 16 + fr] = static_cast<bf16>(sc[jj][e]);
+    __syncthreads();
+    f32x4 o[DH / 16];
+#pragma unroll
+    for (int nt = 0; nt < DH / 16; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < KC / MF::KSUB; ++st) {
+      const MF::frag pa = MF::load(&Ps[(w * 16 + fr) * LDP + st * MF::KSUB + fk]);
+#pragma unroll
+      for (int nt = 0; nt < DH / 16; ++nt)
+        o[nt] = MF::run(pa, MF::load(&Vt[(nt * 16 + fr) * LDV + st * MF::KSUB + fk]), o[nt]);
+    }
+    const size_t slot = ((size_t)b * nH + hn) * C + c;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = prow + e;
+      if (i < H) {
+        const u32 base = (u32)(((slot * H + i) * DH + fr) * 4);
+#pragma unroll
+        for (int nt = 0; nt < DH / 16; ++nt) st4(ro, base + nt * 64u, f2u(o[nt][e]));
+        if (fr == 0)
+          st8(rml, (u32)((slot * H + i) * 8), u32x2{f2u(mrow[e]), f2u(lrow[e])});
+      }
+    }
+    __syncthreads();  // LDS reused by the next item
+  }
+}
+
+// ---- phase 2: combine chunk partials -> o -------------------------------------
+// One (rollout, head, query row) per iteration.  Thread t owns output columns
+// 4*(t % (Dh/4)) .. +4 and the chunks c = t / (Dh/4) + G*u (G chunk groups);
+// each pass loads CPT chunks' partial outputs and (max, sum) pairs in one
+// round trip and folds them into a running (max, sum, acc); the G groups are
+// then merged through LDS.
+__device__ __forceinline__ void phase_combine(const PersistArgs& a, char* smem) {
+  const int H = a.H, nH = a.nH, C = a.C, Dh = a.Dh;
+  const int nq = Dh / 4, G = PT / nq;
+  const int t = threadIdx.x, q4 = t % nq, g = t / nq;
+  float* sm = reinterpret_cast<float*>(smem);  // [PT] max, [PT] sum, [PT][4] acc
+  float* sl = sm + PT;
+  f32x4* sacc = reinterpret_cast<f32x4*>(sl + PT);
+  const rsrc_t ro = rsrc(a.opart), rml = rsrc(a.ml), rout = rsrc(a.o);
+  const int rows = a.B * nH * H;
+  for (int r = blockIdx.x; r < rows; r += gridDim.x) {
+    const int i = r % H, bh = r / H;
+    const int b = bh / nH, hn = bh - b * nH;
+    const int nch = (a.prefix_len[b] + H + KC - 1) / KC;
+    const size_t slot0 = (size_t)bh * C;
+    float m = -INFINITY, lsum = 0.f;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c0 = g; c0 < nch; c0 += G * CPT) {
+      u32x4 ov[CPT];
+      float2 mv[CPT];  // (chunk max, chunk sum)
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int c = c0 + G * u;
+        const bool ok = c < nch;
+        ov[u] = ok ? ld16(ro, (u32)((((slot0 + c) * H + i) * Dh + q4 * 4) * 4)) : u32x4{0u, 0u, 0u, 0u};
+        mv[u] = ok ? ld8f(rml, (u32)(((slot0 + c) * H + i) * 8)) : float2{-INFINITY, 0.f};
+      }
+      float mp = m;
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) mp = fmaxf(mp, mv[u].x);
+      const float f = m == -INFINITY ? 0.f : expf(m - mp);
+      acc *= f;
+      lsum *= f;
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const float wc = mv[u].x == -INFINITY ? 0.f : expf(mv[u].x - mp);
+        acc += wc * as_f4(ov[u]);
+        lsum += wc * mv[u].y;
+      }
+      m = mp;
+    }
+    sm[t] = m;
+    sl[t] = lsum;
+    sacc[t] = acc;
+    __syncthreads();
+    if (g == 0) {
+      float mx = -INFINITY;
+      for (int gg = 0; gg < G; ++gg) mx = fmaxf(mx, sm[gg * nq + q4]);
+      float L = 0.f;
+      f32x4 o4 = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int gg = 0; gg < G; ++gg) {
+        const float mg = sm[gg * nq + q4];
+        const float wg = mg == -INFINITY ? 0.f : expf(mg - mx);
+        o4 += wg * sacc[gg * nq + q4];
+        L += wg * sl[gg * nq + q4];
+      }
+      o4 *= 1.0f / L;
+      st8(rout, (u32)(((((size_t)b * H + i) * nH + hn) * Dh + q4 * 4) * 2), pack4_bf16(o4));
+    }
+    __syncthreads();
+  }
+}
+
+constexpr int NGRP = MAX_W / (4 * PT);  // 4-column groups per thread of a row
+
+// Modulation (scale, shift) of this thread's column groups k4 = 4t + 4*PT*jg.
+__device__ __forceinline__ void load_mod(const PersistArgs& a, const float* scale, const float* shift, f32x4* sc,
+                                         f32x4* sh) {
+#pragma unroll
+  for (int jg = 0; jg < NGRP; ++jg) {
+    const int k4 = 4 * threadIdx.x + 4 * PT * jg;
+    const bool ok = k4 < a.W;
+    sc[jg] = ok ? *reinterpret_cast<const f32x4*>(scale + k4) : f32x4{0.f, 0.f, 0.f, 0.f};
+    sh[jg] = ok ? *reinterpret_cast<const f32x4*>(shift + k4) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+
+// adaRMSNorm of the owner's residual row (LDS) -> y row (bf16, coherent).
+__device__ __forceinline__ void store_y(const PersistArgs& a, const float* hrow, float rs, const f32x4* sc,
+                                        const f32x4* sh) {
+  const rsrc_t ry = rsrc(a.y);
+  const int m = blockIdx.x, W = a.W;
+#pragma unroll
+  for (int jg = 0; jg < NGRP; ++jg) {
+    const int k4 = 4 * threadIdx.x + 4 * PT * jg;
+    if (k4 < W) {
+      const f32x4 h = *reinterpret_cast<const f32x4*>(hrow + k4);
+      st8(ry, (u32)((size_t)m * W + k4) * 2u, pack4_bf16(h * rs * (1.0f + sc[jg]) + sh[jg]));
+    }
+  }
+}
+
+// In-projection of the owner's row: h = x W_in^T + b_in (x and the transposed
+// W_in in LDS), then the step's first adaRMSNorm -> y.
+__device__ __forceinline__ void inproj_row(const PersistArgs& a, const float* scale, const float* shift, float* hrow,
+                                           const float* bin, const bf16* win, const float* xs, float* red) {
+  const int W = a.W, A = a.A;
+  f32x4 sc[NGRP], sh[NGRP];
+  load_mod(a, scale, shift, sc, sh);
+  __syncthreads();  // xs
+  for (int n = threadIdx.x; n < W; n += PT) {
+    float acc = 0.f;
+    for (int c = 0; c < A; ++c) acc = fmaf(xs[c], static_cast<float>(win[c * W + n]), acc);
+    hrow[n] = acc + bin[n];
+  }
+  __syncthreads();
+  float ss = 0.f;
+  for (int k = threadIdx.x; k < W; k += PT) ss += hrow[k] * hrow[k];
+  const float rs = 1.0f / sqrtf(block_sum_wg(ss, red) / (float)W + a.eps);
+  store_y(a, hrow, rs, sc, sh);
+}
+
+struct RowJob {
+  int S;                // split-K slices to sum
+  const float* gate;    // residual gate of the finished sublayer
+  const float* scale;   // next adaRMSNorm (or the final norm)
+  const float* shift;
+  bool final_step;      // last layer: final norm, action-out projection, Euler update
+  const float* nscale;  // final: the next step's first norm (nullptr after the last step)
+  const float* nshift;
+};
+
+// ---- phases 4, 7: row owner updates -----------------------------------------------
+__device__ __forceinline__ void phase_rows(const PersistArgs& a, const RowJob& r, float& xreg, float* hrow,
+                                           const float* bin, const bf16* win, float* xs, char* smem) {
+  const int m = blockIdx.x, W = a.W, A = a.A, t = threadIdx.x;
+  if (m >= a.M) return;
+  float* red = reinterpret_cast<float*>(smem);  // [NWV]
+  float* ys = red + 16;                         // [MAX_W] final normalised row
+  float* pp = ys + MAX_W;                       // [PT] projection partials
+  // final step: the action-out weights do not depend on this step's data, so
+  // their loads go out together with the slice loads
+  const int apad = A <= 8 ? 8 : A <= 16 ? 16 : A <= 32 ? 32 : 64;
+  const int tpa = PT / apad, kper = W / tpa, ao = t % apad, kso = t / apad;
+  u32x4 wv[OUT_G];
+  float bo = 0.f;
+  if (r.final_step) {
+    const bf16* wo = reinterpret_cast<const bf16*>(a.w_out) + (size_t)ao * W + kso * kper;
+#pragma unroll
+    for (int gi = 0; gi < OUT_G; ++gi)
+      wv[gi] = (gi * 8 < kper && ao < A) ? *reinterpret_cast<const u32x4*>(wo + gi * 8) : u32x4{0u, 0u, 0u, 0u};
+    if (t < A) bo = a.b_out[t];
+  }
+  f32x4 sc[NGRP], sh[NGRP];
+  load_mod(a, r.scale, r.shift, sc, sh);
+  const rsrc_t rp = rsrc(a.part, (u32)((size_t)r.S * a.M * W * 4));  // slices z >= S read as zero
+#pragma unroll
+  for (int jg = 0; jg < NGRP; ++jg) {
+    const int k4 = 4 * t + 4 * PT * jg;
+    if (k4 >= W) break;
+    f32x4 v[RMAX_S];
+#pragma unroll
+    for (int z = 0; z < RMAX_S; ++z) v[z] = as_f4(ld16(rp, (u32)(((size_t)z * a.M + m) * W + k4) * 4u));
+    const f32x4 g4 = *reinterpret_cast<const f32x4*>(r.gate + k4);
+    f32x4 sum = v[0];
+#pragma unroll
+    for (int z = 1; z < RMAX_S; ++z) sum += v[z];
+    f32x4* hp = reinterpret_cast<f32x4*>(hrow + k4);
+    *hp = *hp + g4 * sum;
+  }
+  __syncthreads();
+  float ss = 0.f;
+  for (int k = t; k < W; k += PT) ss += hrow[k] * hrow[k];
+  const float rs = 1.0f / sqrtf(block_sum_wg(ss, red) / (float)W + a.eps);
+  if (!r.final_step) {
+    store_y(a, hrow, rs, sc, sh);
+    return;
+  }
+#pragma unroll
+  for (int jg = 0; jg < NGRP; ++jg) {
+    const int k4 = 4 * t + 4 * PT * jg;
+    if (k4 < W)
+      *reinterpret_cast<f32x4*>(ys + k4) = *reinterpret_cast<const f32x4*>(hrow + k4) * rs * (1.0f + sc[jg]) + sh[jg];
+  }
+  __syncthreads();
+  float p = 0.f;
+  const float* yk = ys + kso * kper;
+#pragma unroll
+  for (int gi = 0; gi < OUT_G; ++gi) {
+    if (gi * 8 >= kper) break;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      p = fmaf(yk[gi * 8 + 2 * q], bf16_lo(wv[gi][q]), p);
+      p = fmaf(yk[gi * 8 + 2 * q + 1], bf16_hi(wv[gi][q]), p);
+    }
+  }
+  pp[t] = p;
+  __syncthreads();
+  if (t < A) {
+    float v = pp[t];
+    for (int s = 1; s < tpa; ++s) v += pp[s * apad + t];
+    if (m % a.H >= a.n_fixed) xreg += a.dt * (v + bo);
+    xs[t] = xreg;
+  }
+  if (r.nscale) inproj_row(a, r.nscale, r.nshift, hrow, bin, win, xs, red);
+}
+
+template <int DH>
+__global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[SMEM_BYTES];
+  __shared__ __attribute__((aligned(16))) float s_hrow[MAX_W];  // residual row of the owned action row
+  __shared__ __attribute__((aligned(16))) float s_bin[MAX_W];
+  __shared__ __attribute__((aligned(16))) bf16 s_win[WIN_ELEMS];  // in-projection weights, [A][W]
+  __shared__ float s_x[64];
+  __shared__ u32 s_abort;
+  const int t = threadIdx.x, m = blockIdx.x;
+  const int L = a.L, W = a.W, A = a.A;
+  const bool owner = m < a.M;
+  float xreg = 0.f;
+  if (t == 0) s_abort = 0u;
+  if (owner) {
+    // W_in [W][A] -> LDS transposed [A][W]; 16-byte granules, four per thread in flight
+    const bf16* wi = reinterpret_cast<const bf16*>(a.w_in);
+    const int ng = W * A / 8;
+    for (int g0 = t; g0 < ng; g0 += 4 * PT) {
+      u32x4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        v[u] = g0 + PT * u < ng ? *reinterpret_cast<const u32x4*>(wi + (size_t)(g0 + PT * u) * 8) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (g0 + PT * u >= ng) break;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int el = (g0 + PT * u) * 8 + e, n = el / A, c = el - n * A;
+          s_win[c * W + n] = __builtin_bit_cast(bf16, (unsigned short)(v[u][e >> 1] >> (16 * (e & 1))));
+        }
+      }
+    }
+    for (int k4 = 4 * t; k4 < W; k4 += 4 * PT)
+      *reinterpret_cast<f32x4*>(s_bin + k4) = *reinterpret_cast<const f32x4*>(a.b_in + k4);
+    if (t < A) {
+      xreg = a.x[(size_t)m * A + t];
+      s_x[t] = xreg;
+    }
+  }
+  __syncthreads();
+  u32 epoch = 0;
+  if (owner) inproj_row(a, a.table, a.table + W, s_hrow, s_bin, s_win, s_x, reinterpret_cast<float*>(smem));
+  grid_sync(a, ++epoch, &s_abort);
+  const int last_phase = a.n_steps * L * 8 - 1;
+  for (int ph = 0; ph <= last_phase; ++ph) {
+    const int k = ph / (8 * L), l = (ph / 8) % L, p = ph % 8;
+    const float* tk = a.table + (size_t)k * a.R;
+    const float* am = tk + (size_t)(2 * l) * 3 * W;      // attention modulation: scale | shift | gate
+    const float* mm = tk + (size_t)(2 * l + 1) * 3 * W;  // MLP modulation
+    const bf16* lay = reinterpret_cast<const bf16*>(a.w_layers) + (size_t)l * a.layer_elems;
+    if (p == 1) {
+      phase_attn<DH>(a, l, smem);
+    } else if (p == 2) {
+      phase_combine(a, smem);
+    } else if (p == 4 || p == 7) {
+      RowJob r;
+      r.nscale = r.nshift = nullptr;
+      r.final_step = false;
+      if (p == 4) {
+        r.S = a.s_o;
+        r.gate = am + 2 * W;
+        r.scale = mm;
+        r.shift = mm + W;
+      } else {
+        r.S = a.s_d;
+        r.gate = mm + 2 * W;
+        if (l + 1 < L) {
+          r.scale = am + 6 * W;  // next layer's attention modulation
+          r.shift = am + 7 * W;
+        } else {
+          const float* fm = tk + (size_t)(6 * L) * W;
+          r.scale = fm;
+          r.shift = fm + W;
+          r.final_step = true;
+          if (k + 1 < a.n_steps) {
+            r.nscale = tk + a.R;
+            r.nshift = tk + a.R + W;
+          }
+        }
+      }
+      phase_rows(a, r, xreg, s_hrow, s_bin, s_win, s_x, smem);
+    } else {
+      GemmJob j;
+      if (p == 0) {
+        j = GemmJob{a.y, lay, W, (a.nH + 2) * a.Dh / 32, 1, EPI_QKV};
+      } else if (p == 3) {
+        j = GemmJob{a.o, lay + a.off_o, a.nH * a.Dh, W / 32, a.s_o, EPI_SLICE};
+      } else if (p == 5) {
+        j = GemmJob{a.y, lay + a.off_gu, W, 2 * a.F / 32, 1, EPI_GEGLU};
+      } else {
+        j = GemmJob{a.z, lay + a.off_d, a.F, W / 32, a.s_d, EPI_SLICE};
+      }
+      phase_gemm(a, j, l, smem);
+    }
+    if (ph < last_phase) grid_sync(a, ++epoch, &s_abort);
+  }
+  if (owner && t < A) a.x[(size_t)m * A + t] = xreg;
+}
+
+__global__ void k_persist_reset(u32* flags, int n) {  // n = FLAG_WORDS
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) flags[i] = 0u;
+}
+
+}  // namespace
+
+bool persist_supported(jpi_dtype dt, int M, int W, int nH, int Dh, int F, int H, int A, int Pmax) {
+  if (dt != JPI_BF16 || M > 64 || H > 64 || nH % 2 != 0 || !(Dh == 64 || Dh == 128 || Dh == 256)) return false;
+  if (W % (NWV * 32) != 0 || F % (NWV * 32) != 0 || (nH * Dh) % (NWV * 32) != 0) return false;
+  if (W > MAX_W || A < 1 || A > 64 || A * W > WIN_ELEMS || Pmax + H > MAX_CH * KC) return false;
+  const int apad = A <= 8 ? 8 : A <= 16 ? 16 : A <= 32 ? 32 : 64;
+  const int kper = W / (PT / apad);  // action-out projection: columns per thread
+  return kper % 8 == 0 && kper <= OUT_G * 8;
+}
+
+int persist_chunks(int P, int H) { return (P + H + KC - 1) / KC; }
+
+int persist_pick_split(int tiles, int K, int grid) {
+  int s = 1;
+  while (s < RMAX_S && tiles * s < grid && K % (2 * s * NWV * 32) == 0) s *= 2;
+  return s;
+}
+
+int persist_block_threads() { return PT; }
+
+int persist_max_grid() { return MAX_GRID; }
+
+int persist_flag_words() { return FLAG_WORDS; }
+
+hipError_t persist_occupancy(int Dh, int* blocks_per_cu) {
+  switch (Dh) {
+    case 64: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k_persist<64>, PT, 0);
+    case 128: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k_persist<128>, PT, 0);
+    case 256: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k_persist<256>, PT, 0);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_persist(const PersistArgs& a, int grid, hipStream_t s) {
+  if (grid > MAX_GRID) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_persist_reset, dim3((FLAG_WORDS + 255) / 256), dim3(256), 0, s, a.flags, FLAG_WORDS);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  switch (a.Dh) {
+    case 64: JPI_LAUNCH((k_persist<64>), dim3(grid), dim3(PT), 0, s, a.ev_start, a.ev_stop, a); break;
+    case 128: JPI_LAUNCH((k_persist<128>), dim3(grid), dim3(PT), 0, s, a.ev_start, a.ev_stop, a); break;
+    case 256: JPI_LAUNCH((k_persist<256>), dim3(grid), dim3(PT), 0, s, a.ev_start, a.ev_stop, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace jpi

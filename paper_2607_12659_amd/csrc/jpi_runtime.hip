@@ -50,8 +50,10 @@ bool kind_is_matrix(int k) {
 
 struct GraphKey {
   int batch, prefix, n_steps, n_fixed;
+  bool persist;  // the single-launch path and the multi-kernel path capture different graphs
   bool operator<(const GraphKey& o) const {
-    return std::tie(batch, prefix, n_steps, n_fixed) < std::tie(o.batch, o.prefix, o.n_steps, o.n_fixed);
+    return std::tie(batch, prefix, n_steps, n_fixed, persist) <
+           std::tie(o.batch, o.prefix, o.n_steps, o.n_fixed, o.persist);
   }
 };
 
@@ -84,7 +86,7 @@ struct jpi_ctx {
   // prefix and state
   void *kp = nullptr, *vp = nullptr;  // [L][Bmax][Pmax][Dh] as bound
   void* vpt = nullptr;                 // [L][Bmax][Dh][Ppad] prefix V transposed at bind time
-  int Ppad = 0;                        // Pmax rounded up to a multiple of 8
+  int Ppad = 0;                        // Pmax + horizon rounded up to a multiple of 8
   int* d_prefix_len = nullptr;
   int* h_prefix_len = nullptr;  // pinned staging
   int batch = 0, prefix = 0;
@@ -103,6 +105,10 @@ struct jpi_ctx {
   std::map<int, float*> tables;
   std::map<GraphKey, hipGraphExec_t> graphs;
   hipStream_t cap_stream = nullptr;
+  // single-launch (persistent) path
+  unsigned* pflags = nullptr;  // barrier arrival lines (one per workgroup) + release line
+  unsigned* perr = nullptr;    // barrier timeout word
+  int persist_occ = -1;        // workgroups per CU the persistent kernel fits (-1: not queried)
   // measurement: events around every launch of one kernel kind
   int timed_kind = JPI_KERNEL_NONE;
   std::vector<hipEvent_t> ev;  // pairs (start, end)
@@ -253,7 +259,7 @@ jpi_status jpi_destroy(jpi_ctx* c) {
   drop_events(c);
   void* bufs[] = {c->w_layers, c->w_in, c->w_t0, c->w_t1, c->w_mod, c->w_out, c->b_in, c->b_t0, c->b_t1, c->b_mod,
                   c->b_out, c->kp, c->vp, c->vpt, c->d_prefix_len, c->rope_tab, c->committed, c->x, c->h, c->y, c->q, c->ks,
-                  c->vst, c->o, c->z, c->partial, c->opart};
+                  c->vst, c->o, c->z, c->partial, c->opart, c->pflags, c->perr};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   if (c->h_prefix_len) (void)hipHostFree(c->h_prefix_len);
@@ -349,7 +355,9 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   const size_t kv_elems = (size_t)c->L * c->Bmax * (size_t)c->Pmax * Dh;
   ALLOC(c->kp, kv_elems * es);
   ALLOC(c->vp, kv_elems * es);
-  c->Ppad = (c->Pmax + 7) / 8 * 8;
+  // room for the action keys after the longest prefix (the single-launch
+  // path stores the action rows' V there), rounded to 16-byte rows
+  c->Ppad = (c->Pmax + c->H + 7) / 8 * 8;
   ALLOC(c->vpt, (size_t)c->L * c->Bmax * (size_t)c->Ppad * Dh * es);
   ALLOC(c->d_prefix_len, c->Bmax * 4);
   ALLOC(c->rope_tab, M * (Dh / 2) * sizeof(float2));
@@ -362,7 +370,10 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   ALLOC(c->vst, M * Dh * es);
   ALLOC(c->o, M * nH * Dh * es);
   ALLOC(c->z, M * F * es);
+  ALLOC(c->pflags, (size_t)persist_flag_words() * sizeof(unsigned));
+  ALLOC(c->perr, 256);
 #undef ALLOC
+  if (hipMemset(c->perr, 0, 256) != hipSuccess) return cleanup_fail(fail(c, JPI_ERR_HIP, "hipMemset"));
   if (hipHostMalloc((void**)&c->h_prefix_len, c->Bmax * sizeof(int)) != hipSuccess) {
     (void)hipGetLastError();
     c->h_prefix_len = nullptr;
@@ -606,13 +617,36 @@ jpi_status ensure_table(jpi_ctx* c, int n_steps, hipStream_t s, float** out) {
 struct StepGemms {
   int M;
   int s_o, s_d;  // split-K of the O and Down projections (QKV and GateUp are not split)
+  bool persist;  // single-launch path
 };
 
-StepGemms plan_gemms(const jpi_ctx* c, int batch) {
+bool use_persist(jpi_ctx* c, int batch) {
+  const char* e = getenv("JPI_PERSIST");
+  if (e && e[0] == '0') return false;
+  if (!persist_supported(c->dt, batch * c->H, c->W, c->nH, c->Dh, c->F, c->H, c->A, c->Pmax)) return false;
+  if (c->n_cu > persist_max_grid()) return false;
+  if (c->persist_occ < 0) {
+    int occ = 0;
+    if (persist_occupancy(c->Dh, &occ) != hipSuccess) {
+      (void)hipGetLastError();
+      occ = 0;
+    }
+    c->persist_occ = occ;
+  }
+  return c->persist_occ >= 1;  // one workgroup per CU, grid = CU count: all co-resident
+}
+
+StepGemms plan_gemms(jpi_ctx* c, int batch) {
   StepGemms p;
   p.M = batch * c->H;
-  p.s_o = gemm_pick_splitk(c->dt, p.M, c->W, c->nH * c->Dh, c->n_cu);
-  p.s_d = gemm_pick_splitk(c->dt, p.M, c->W, c->F, c->n_cu);
+  p.persist = use_persist(c, batch);
+  if (p.persist) {
+    p.s_o = persist_pick_split(c->W / 32, c->nH * c->Dh, c->n_cu);
+    p.s_d = persist_pick_split(c->W / 32, c->F, c->n_cu);
+  } else {
+    p.s_o = gemm_pick_splitk(c->dt, p.M, c->W, c->nH * c->Dh, c->n_cu);
+    p.s_d = gemm_pick_splitk(c->dt, p.M, c->W, c->F, c->n_cu);
+  }
   return p;
 }
 
@@ -628,7 +662,7 @@ jpi_status ensure_scratch(jpi_ctx* c, int batch, int prefix) {
     c->partial_cap = need;
     changed = true;
   }
-  const size_t nch = attn_n_chunks(c->dt, prefix, c->H);
+  const size_t nch = p.persist ? (size_t)persist_chunks(prefix, c->H) : (size_t)attn_n_chunks(c->dt, prefix, c->H);
   const size_t attn = (size_t)batch * c->nH * nch * c->H * (c->Dh + 2);
   if (attn > c->attn_cap) {
     if (c->opart) (void)hipFree(c->opart);
@@ -673,6 +707,61 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     *stop = c->ev[c->ev_used + 1];
     c->ev_used += 2;
   };
+  if (p.persist) {
+    PersistArgs pa{};
+    pa.L = L;
+    pa.W = W;
+    pa.nH = nH;
+    pa.Dh = Dh;
+    pa.F = F;
+    pa.A = c->A;
+    pa.H = H;
+    pa.B = batch;
+    pa.M = M;
+    pa.C = persist_chunks(prefix, H);
+    pa.n_steps = n_steps;
+    pa.n_fixed = c->n_fixed;
+    pa.s_o = p.s_o;
+    pa.s_d = p.s_d;
+    pa.R = c->R;
+    pa.eps = eps;
+    pa.dt = dt_step;
+    pa.w_layers = c->w_layers;
+    pa.layer_elems = (int64_t)c->layer_elems;
+    pa.off_o = (int64_t)c->off_o;
+    pa.off_gu = (int64_t)c->off_gu;
+    pa.off_d = (int64_t)c->off_d;
+    pa.w_in = c->w_in;
+    pa.b_in = c->b_in;
+    pa.w_out = c->w_out;
+    pa.b_out = c->b_out;
+    pa.table = table;
+    pa.kp = c->kp;
+    pa.vpt = c->vpt;
+    pa.kp_lstride = (int64_t)c->Bmax * c->Pmax * Dh;
+    pa.kp_bstride = (int64_t)c->Pmax * Dh;
+    pa.vpt_lstride = (int64_t)c->Bmax * c->Ppad * Dh;
+    pa.vpt_bstride = (int64_t)c->Ppad * Dh;
+    pa.vpt_dstride = c->Ppad;
+    pa.prefix_len = c->d_prefix_len;
+    pa.rope = c->rope_tab;
+    pa.x = c->x;
+    pa.h = c->h;
+    pa.y = c->y;
+    pa.q = c->q;
+    pa.ks = c->ks;
+    pa.vst = c->vst;
+    pa.opart = c->opart;
+    pa.ml = c->opart + (size_t)batch * nH * pa.C * H * Dh;
+    pa.o = c->o;
+    pa.part = c->partial;
+    pa.z = c->z;
+    pa.flags = c->pflags;
+    pa.err = c->perr;
+    timing(JPI_KERNEL_PERSISTENT, &pa.ev_start, &pa.ev_stop);
+    ENQ(launch_persist(pa, c->n_cu, s));
+    return hipSuccess;
+  }
   for (int k = 0; k < n_steps; ++k) {
     const float* tk = table + (size_t)k * c->R;
     const float* fm = tk + (size_t)(6 * L) * W;
@@ -820,7 +909,7 @@ jpi_status jpi_denoise(jpi_ctx* c, const float* noise_dev, int n_steps, float* a
   if (eager_mode() || c->timed_kind >= 0) {
     HIPCHK(c, enqueue_steps(c, table, n_steps, s));
   } else {
-    const GraphKey key{c->batch, c->prefix, n_steps, c->n_fixed};
+    const GraphKey key{c->batch, c->prefix, n_steps, c->n_fixed, use_persist(c, c->batch)};
     auto it = c->graphs.find(key);
     if (it == c->graphs.end()) {
       hipGraph_t graph = nullptr;
@@ -850,12 +939,19 @@ jpi_status jpi_sync(jpi_ctx* c, void* stream) {
   HIPCHK(c, hipSetDevice(c->device));
   HIPCHK(c, hipStreamSynchronize((hipStream_t)stream));
   HIPCHK(c, hipGetLastError());
+  unsigned perr = 0;
+  HIPCHK(c, hipMemcpy(&perr, c->perr, sizeof(perr), hipMemcpyDeviceToHost));
+  if (perr != 0) {
+    HIPCHK(c, hipMemset(c->perr, 0, sizeof(perr)));
+    return fail(c, JPI_ERR_HIP, "single-launch denoise: a grid barrier wait timed out; the output is invalid");
+  }
   return JPI_OK;
 }
 
 jpi_status jpi_debug_time_kernel(jpi_ctx* c, int kind) {
   if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_time_kernel: ctx is NULL");
-  if (kind < JPI_KERNEL_NONE || kind > JPI_KERNEL_DOWN) return fail(c, JPI_ERR_ARG, "jpi_debug_time_kernel: bad kind");
+  if (kind < JPI_KERNEL_NONE || kind > JPI_KERNEL_PERSISTENT)
+    return fail(c, JPI_ERR_ARG, "jpi_debug_time_kernel: bad kind");
   HIPCHK(c, hipSetDevice(c->device));
   HIPCHK(c, hipDeviceSynchronize());
   drop_graphs(c);

@@ -230,3 +230,55 @@ def test_pi05_fp32_shape_at_1e4():
     err = np.abs(got - ref).max()
     print("pi05-f32-b1 max-abs %.3e" % err, flush=True)
     assert err <= F32_TOL
+
+
+# ---------------------------------------------------------------------------
+# single-launch (persistent) path: batch * horizon <= 64 with bf16 weights
+# ---------------------------------------------------------------------------
+def _run_env(ae, env, *args, **kw):
+    old = os.environ.get("JPI_PERSIST")
+    if env is None:
+        os.environ.pop("JPI_PERSIST", None)
+    else:
+        os.environ["JPI_PERSIST"] = env
+    try:
+        return run(ae, *args, **kw)
+    finally:
+        if old is None:
+            os.environ.pop("JPI_PERSIST", None)
+        else:
+            os.environ["JPI_PERSIST"] = old
+
+
+def test_persistent_tiny_bf16_batched_ragged_committed():
+    torch_cuda()
+    wl = synth.WORKLOADS["tiny-fp32"].with_(dtype="bf16", batch=3, n_fixed=2, prefix_len=(64, 5, 41),
+                                            name="tiny-bf16-b3")
+    inp = Inputs(wl)
+    ae = make_expert(wl, inp.weights)
+    try:
+        got = _run_env(ae, None, inp.K, inp.V, inp.noise, wl.n_steps, prefix_len=inp.prefix_len,
+                       committed=inp.committed, n_fixed=2)
+        multi = _run_env(ae, "0", inp.K, inp.V, inp.noise, wl.n_steps, prefix_len=inp.prefix_len,
+                         committed=inp.committed, n_fixed=2)
+    finally:
+        ae.close()
+    ref = _oracle(wl, inp, committed=inp.committed, n_fixed=2)
+    rel = rel_l2_per_rollout(got, ref)
+    print("tiny-bf16-b3 persistent: rel-L2 %.3e, vs multi-kernel path %.3e" % (rel, rel_l2_per_rollout(got, multi)))
+    assert rel <= BF16_TOL
+    assert rel_l2_per_rollout(got, multi) <= 5e-3
+    assert np.array_equal(got[:, :2].astype(np.float32), inp.committed.astype(np.float32))
+
+
+def test_persistent_matches_multikernel_pi05(pi05):
+    w, ae = pi05
+    wl = synth.WORKLOADS["pi05-b1"]
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    a = _run_env(ae, None, K, V, noise, 2)
+    b = _run_env(ae, "0", K, V, noise, 2)
+    print("pi05 2-step: persistent vs multi-kernel rel-L2 %.3e" % rel_l2_per_rollout(a, b))
+    assert rel_l2_per_rollout(a, b) <= 5e-3
+    # graph replay determinism of the single-launch kernel
+    assert np.array_equal(a, _run_env(ae, None, K, V, noise, 2))
