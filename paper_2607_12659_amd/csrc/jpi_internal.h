@@ -104,6 +104,7 @@ struct PersistArgs {
   int n_steps, n_fixed, s_o, s_d, R;
   float eps, dt;
   const void* w_layers;     // packed layer weights (bf16)
+  const void* w_frag;       // the same, each matrix fragment-ordered
   int64_t layer_elems, off_o, off_gu, off_d;
   const void* w_in;
   const float* b_in;
@@ -117,15 +118,15 @@ struct PersistArgs {
   const float2* rope;       // [B][H][Dh/2]
   float* x;                 // [M][A]
   float* h;                 // [M][W]
-  void* y;                  // [M][W] bf16
-  void* q;                  // [B][nH][H][Dh]
+  void* y;                  // fragment-ordered [64][W] bf16 (single-launch path)
+  void* q;                  // fragment-ordered [B][nH][64][Dh]
   void* ks;                 // [B][H][Dh]
   void* vst;                // [B][Dh][H]
   float* opart;             // [B][nH][C][H][Dh]
   float* ml;                // [B][nH][C][H][2]
-  void* o;                  // [M][nH*Dh]
+  void* o;                  // fragment-ordered [64][nH*Dh]
   float* part;              // [max(s_o, s_d)][M][W]
-  void* z;                  // [M][F]
+  void* z;                  // fragment-ordered [64][F]
   unsigned* flags;          // [grid][32] barrier arrival epochs
   unsigned* err;            // set to 1 if a barrier wait timed out
   hipEvent_t ev_start, ev_stop;
@@ -136,6 +137,8 @@ int persist_pick_split(int tiles, int K, int grid);
 int persist_block_threads();
 int persist_max_grid();    // largest grid the barrier supports
 int persist_flag_words();  // size of the barrier flag buffer in 32-bit words
+// dst = fragment-ordered copy of the row-major bf16 matrix src [R][K]
+hipError_t launch_frag_order(const void* src, void* dst, int R, int K, hipStream_t s);
 hipError_t persist_occupancy(int Dh, int* blocks_per_cu);
 hipError_t launch_persist(const PersistArgs& a, int grid, hipStream_t s);
 

@@ -25,6 +25,15 @@
 // stays within the instruction cache; a phase whose code was evicted since
 // the previous layer pays instruction-fetch latency on every new cache line.
 //
+// Operand layout: every matrix that feeds an MFMA (the layer weights, a
+// fragment-ordered copy made by the host, and the activations y, o, z, q
+// written by the phases) is stored as 16x32 blocks in (row group, k step)
+// order, each block holding the 64 lanes' 8-element fragments in lane order.
+// A wave then loads a whole fragment as one contiguous kilobyte; row-major
+// fragments would touch half of sixteen cache lines per instruction, which
+// halves the load throughput of a compute unit.  Activation matrices are
+// padded to 64 rows; rows >= M are never written and stay zero.
+//
 // Row ownership: workgroup m < M owns action row m.  Its residual row, the
 // in-projection weights (transposed) and b_in live in LDS for the whole
 // launch and x[m][a] lives in a register of thread a.
@@ -41,6 +50,8 @@
 // Every barrier wait is bounded: after SPIN_LIMIT polls the workgroup records
 // an error word and stops waiting, so a launch always terminates; the host
 // reports the error from jpi_sync.
+#include <algorithm>
+
 #include "jpi_device.h"
 #include "jpi_internal.h"
 
@@ -54,9 +65,8 @@ constexpr int CPOL_DEV = 16;  // sc1: device-scope coherent access
 constexpr int KC = 32;        // keys per attention chunk
 constexpr int MAX_CH = 128;   // attention chunks per rollout
 constexpr unsigned SPIN_LIMIT = 1u << 21;
-constexpr int SMEM_BYTES = 48 * 1024;  // per-phase scratch
+constexpr int SMEM_BYTES = 42496;      // per-phase scratch (attention staging at Dh = 256)
 constexpr int MAX_W = 2048;            // model width held in LDS by a row owner
-constexpr int WIN_ELEMS = 32768;       // in-projection weights held in LDS (A * W)
 constexpr int RMAX_S = 16;             // split-K slices summed by the row phases
 constexpr int MAX_GRID = 256;          // barrier flags are polled as 64 lanes x 4 lines
 constexpr int FLAG_STRIDE = 32;        // words between barrier flags: one 128-byte line per workgroup
@@ -108,6 +118,12 @@ __device__ __forceinline__ float bf16_lo(u32 w) { return u2f(w << 16); }
 __device__ __forceinline__ float bf16_hi(u32 w) { return u2f(w & 0xffff0000u); }
 __device__ __forceinline__ f32x4 as_f4(u32x4 v) { return __builtin_bit_cast(f32x4, v); }
 
+// Element offset of (row, k) in the fragment-ordered layout of a bf16 matrix
+// with KS = K / 32 k steps.
+__device__ __forceinline__ u32 frag_off(int row, int k, int KS) {
+  return (u32)((((row >> 4) * KS + (k >> 5)) * 64 + (row & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7));
+}
+
 // Fixed-order sum over the waves of a workgroup.
 __device__ __forceinline__ float block_sum_wg(float v, float* red) {
   v = wave_sum(v);
@@ -155,26 +171,26 @@ __device__ __forceinline__ void grid_sync(const PersistArgs& a, u32 epoch, u32* 
 
 // ---------------------------------------------------------------------------
 // GEMM item: rows 0..63 x 32 output columns [n0, n0+32) over the K range
-// [kbeg, kbeg + klen), split evenly over the waves.  `ra` covers exactly the
-// M valid rows of the bf16 activation matrix A (leading dimension lda), so the
-// rows >= M of the 64-row tile read as zero without a branch.  W is packed
-// bf16 weights [N][ldw].  Returns the sums for m-subtile `wave` in lo
-// (columns n0 + lane%16) and hi (n0 + 16 + lane%16).
+// [kbeg, kbeg + klen), split evenly over the waves.  A (`ra`, fragment-ordered,
+// 64 padded rows, read coherently) contributes its first `mgroups` 16-row
+// groups; W is the fragment-ordered weight matrix with KS k steps.  All
+// fragments of a wave's K range are loaded before the first MFMA.  Returns
+// the sums for m-subtile `wave` in lo (columns n0 + lane%16) and hi
+// (n0 + 16 + lane%16).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void gemm_item(rsrc_t ra, int lda, const bf16* W, int ldw, int n0, int kbeg, int klen,
+__device__ __forceinline__ void gemm_item(rsrc_t ra, int mgroups, const bf16* W, int KS, int n0, int kbeg, int klen,
                                           f32x4* red, f32x4& lo, f32x4& hi) {
   using MF = Mfma<bf16>;
   constexpr int BATCH = 8;
   static_assert(NWV == 4, "one m-subtile of the 64-row tile per wave");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int fr = lane & 15, fk = (lane >> 4) * MF::KPL;
   const int kw = klen / NWV;
-  const int k0 = kbeg + wave * kw;
+  const int s_beg = (kbeg + wave * kw) / MF::KSUB;
   const int nsub = kw / MF::KSUB;
-  const bf16* wp0 = W + (size_t)(n0 + fr) * ldw + k0 + fk;
-  const bf16* wp1 = wp0 + (size_t)16 * ldw;
-  const u32 aoff = (u32)(((size_t)fr * lda + k0 + fk) * 2);
-  const u32 astep = (u32)(16 * lda * 2);
+  const bf16* wp0 = W + ((size_t)((n0 >> 4) * KS + s_beg) * 64 + lane) * 8;
+  const bf16* wp1 = wp0 + (size_t)KS * 512;  // next 16-row group
+  const u32 aoff = (u32)(s_beg * 64 + lane) * 16u;
+  const u32 astep = (u32)KS * 1024u;  // bytes per 16-row group
   f32x4 acc[4][2];
 #pragma unroll
   for (int a = 0; a < 4; ++a) acc[a][0] = acc[a][1] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -183,12 +199,13 @@ __device__ __forceinline__ void gemm_item(rsrc_t ra, int lda, const bf16* W, int
 #pragma unroll
     for (int c = 0; c < BATCH; ++c) {
       const bool ok = s0 + c < nsub;
-      wf[c][0] = ok ? MF::load(wp0 + (s0 + c) * MF::KSUB) : MF::frag{};
-      wf[c][1] = ok ? MF::load(wp1 + (s0 + c) * MF::KSUB) : MF::frag{};
+      wf[c][0] = ok ? MF::load(wp0 + (s0 + c) * 512) : MF::frag{};
+      wf[c][1] = ok ? MF::load(wp1 + (s0 + c) * 512) : MF::frag{};
 #pragma unroll
       for (int a = 0; a < 4; ++a)
-        af[c][a] = ok ? __builtin_bit_cast(MF::frag, ld16(ra, aoff + a * astep + (u32)((s0 + c) * MF::KSUB * 2)))
-                      : MF::frag{};
+        af[c][a] = (ok && a < mgroups)
+                       ? __builtin_bit_cast(MF::frag, ld16(ra, aoff + a * astep + (u32)(s0 + c) * 1024u))
+                       : MF::frag{};
     }
 #pragma unroll
     for (int c = 0; c < BATCH; ++c)
@@ -216,9 +233,9 @@ __device__ __forceinline__ void gemm_item(rsrc_t ra, int lda, const bf16* W, int
 }
 
 struct GemmJob {
-  const void* A;  // activations [M][K] bf16
-  const bf16* w;  // weights [N][K] bf16
-  int K;          // reduction length (also the leading dimension of A and w)
+  const void* A;  // activations, fragment-ordered [64][K] bf16
+  const bf16* w;  // weights, fragment-ordered [N][K] bf16
+  int K;          // reduction length
   int tiles;      // N / 32
   int S;          // split-K slices
   int kind;       // EPI_*
@@ -229,8 +246,8 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
   f32x4* red = reinterpret_cast<f32x4*>(smem);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, fr = lane & 15;
   const int Dh = a.Dh, half = Dh / 2, H = a.H, nH = a.nH, qcols = nH * Dh, M = a.M, Wd = a.W;
-  const int klen = j.K / j.S;
-  const rsrc_t ra = rsrc(j.A, (u32)(M * j.K * 2));
+  const int klen = j.K / j.S, KS = j.K / 32, mgroups = (M + 15) / 16;
+  const rsrc_t ra = rsrc(j.A, (u32)(64 * j.K * 2));
   const rsrc_t rq = rsrc(a.q), rk = rsrc(a.ks), rz = rsrc(a.z), rp = rsrc(a.part);
   const rsrc_t rv = rsrc(reinterpret_cast<const bf16*>(a.vpt) + (size_t)l * a.vpt_lstride);
   for (int it = blockIdx.x; it < j.tiles * j.S; it += gridDim.x) {
@@ -253,7 +270,7 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
       plv[e] = (qkv && !roped && row < M) ? a.prefix_len[row / H] : 0;
     }
     f32x4 lo, hi;
-    gemm_item(ra, j.K, j.w, j.K, t * 32, s * klen, klen, red, lo, hi);
+    gemm_item(ra, mgroups, j.w, KS, t * 32, s * klen, klen, red, lo, hi);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int row = wave * 16 + (lane >> 4) * 4 + e;
@@ -263,16 +280,21 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
         st4(rp, base, f2u(lo[e]));
         st4(rp, base + 64u, f2u(hi[e]));
       } else if (j.kind == EPI_GEGLU) {  // gate/up rows interleaved in 16-row groups
-        st_bf16(rz, (u32)((size_t)row * a.F + t * 16 + fr) * 2u, gelu_tanh(lo[e]) * hi[e]);
+        st_bf16(rz, frag_off(row, t * 16 + fr, a.F / 32) * 2u, gelu_tanh(lo[e]) * hi[e]);
       } else {
         const int b = row / H, i = row - b * H;
         if (roped) {
           const float r_lo = lo[e] * cs[e].x - hi[e] * cs[e].y;
           const float r_hi = lo[e] * cs[e].y + hi[e] * cs[e].x;
-          const u32 base = hn >= 0 ? (u32)((((size_t)b * nH + hn) * H + i) * Dh) : (u32)(((size_t)b * H + i) * Dh);
-          const rsrc_t rd = hn >= 0 ? rq : rk;
-          st_bf16(rd, (base + d) * 2u, r_lo);
-          st_bf16(rd, (base + d + half) * 2u, r_hi);
+          if (hn >= 0) {  // q: fragment-ordered [b][head][64 rows][Dh]
+            const u32 base = (u32)(((size_t)b * nH + hn) * 64 * Dh);
+            st_bf16(rq, (base + frag_off(i, d, Dh / 32)) * 2u, r_lo);
+            st_bf16(rq, (base + frag_off(i, d + half, Dh / 32)) * 2u, r_hi);
+          } else {  // action K rows: row-major [b][H][Dh]
+            const u32 base = (u32)(((size_t)b * H + i) * Dh);
+            st_bf16(rk, (base + d) * 2u, r_lo);
+            st_bf16(rk, (base + d + half) * 2u, r_hi);
+          }
         } else {
           // V of action row i: transposed prefix V buffer at key prefix_len + i
           const int dv = col - qcols - Dh;
@@ -342,14 +364,13 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
         vr[u] = u32x4{0u, 0u, 0u, 0u};
       }
     }
-    // wave w: query rows w*16 .. +16 of head hn
-    const int iq = w * 16 + fr;
+    // wave w: query rows w*16 .. +16 of head hn (fragment-ordered; rows >= H are zero)
     MF::frag qf[NST];
+    const u32 qoff = (u32)(((((size_t)b * nH + hn) * 4 + w) * NST) * 64 + lane) * 16u;
 #pragma unroll
     for (int st = 0; st < NST; ++st)
-      qf[st] = iq < H ? __builtin_bit_cast(
-                            MF::frag, ld16(rq, (u32)(((((size_t)b * nH + hn) * H + iq) * DH + st * MF::KSUB + fk) * 2)))
-                      : MF::frag{};
+      qf[st] = w * 16 < H ? __builtin_bit_cast(MF::frag, ld16(rq, qoff + (u32)st * 1024u)) : MF::frag{};
+
 #pragma unroll
     for (int u = 0; u < KCH; ++u) {
       const int e = tid + u * PT, r = e / (DH / 8), cc = e - r * (DH / 8);
@@ -486,7 +507,7 @@ __device__ __forceinline__ void phase_combine(const PersistArgs& a, char* smem) 
         L += wg * sl[gg * nq + q4];
       }
       o4 *= 1.0f / L;
-      st8(rout, (u32)(((((size_t)b * H + i) * nH + hn) * Dh + q4 * 4) * 2), pack4_bf16(o4));
+      st8(rout, frag_off(b * H + i, hn * Dh + q4 * 4, nH * Dh / 32) * 2u, pack4_bf16(o4));
     }
     __syncthreads();
   }
@@ -516,23 +537,57 @@ __device__ __forceinline__ void store_y(const PersistArgs& a, const float* hrow,
     const int k4 = 4 * threadIdx.x + 4 * PT * jg;
     if (k4 < W) {
       const f32x4 h = *reinterpret_cast<const f32x4*>(hrow + k4);
-      st8(ry, (u32)((size_t)m * W + k4) * 2u, pack4_bf16(h * rs * (1.0f + sc[jg]) + sh[jg]));
+      st8(ry, frag_off(m, k4, W / 32) * 2u, pack4_bf16(h * rs * (1.0f + sc[jg]) + sh[jg]));
     }
   }
 }
 
-// In-projection of the owner's row: h = x W_in^T + b_in (x and the transposed
-// W_in in LDS), then the step's first adaRMSNorm -> y.
+// In-projection of the owner's row: h = x W_in^T + b_in (x in LDS, W_in
+// [W][A] in global memory; with A % 8 == 0 a thread loads its rows as
+// 16-byte pieces, all in flight), then the step's first adaRMSNorm -> y.
 __device__ __forceinline__ void inproj_row(const PersistArgs& a, const float* scale, const float* shift, float* hrow,
-                                           const float* bin, const bf16* win, const float* xs, float* red) {
+                                           const float* bin, const float* xs, float* red) {
   const int W = a.W, A = a.A;
+  const bf16* win = reinterpret_cast<const bf16*>(a.w_in);
   f32x4 sc[NGRP], sh[NGRP];
   load_mod(a, scale, shift, sc, sh);
   __syncthreads();  // xs
-  for (int n = threadIdx.x; n < W; n += PT) {
-    float acc = 0.f;
-    for (int c = 0; c < A; ++c) acc = fmaf(xs[c], static_cast<float>(win[c * W + n]), acc);
-    hrow[n] = acc + bin[n];
+  if ((A & 7) == 0) {
+    constexpr int NJ = MAX_W / PT;  // rows per thread
+    for (int j0 = 0; j0 < NJ; j0 += 4) {
+      if (PT * j0 >= W) break;
+      u32x4 v[4][8];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int n = threadIdx.x + PT * (j0 + jj);
+#pragma unroll
+        for (int c8 = 0; c8 < 8; ++c8)
+          v[jj][c8] = (n < W && c8 * 8 < A) ? *reinterpret_cast<const u32x4*>(win + (size_t)n * A + c8 * 8)
+                                             : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int n = threadIdx.x + PT * (j0 + jj);
+        if (n >= W) continue;
+        float acc = 0.f;
+#pragma unroll
+        for (int c8 = 0; c8 < 8; ++c8) {
+          if (c8 * 8 >= A) break;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            acc = fmaf(xs[c8 * 8 + 2 * q], bf16_lo(v[jj][c8][q]), acc);
+            acc = fmaf(xs[c8 * 8 + 2 * q + 1], bf16_hi(v[jj][c8][q]), acc);
+          }
+        }
+        hrow[n] = acc + bin[n];
+      }
+    }
+  } else {
+    for (int n = threadIdx.x; n < W; n += PT) {
+      float acc = 0.f;
+      for (int c = 0; c < A; ++c) acc = fmaf(xs[c], static_cast<float>(win[(size_t)n * A + c]), acc);
+      hrow[n] = acc + bin[n];
+    }
   }
   __syncthreads();
   float ss = 0.f;
@@ -542,18 +597,16 @@ __device__ __forceinline__ void inproj_row(const PersistArgs& a, const float* sc
 }
 
 struct RowJob {
-  int S;                // split-K slices to sum
-  const float* gate;    // residual gate of the finished sublayer
-  const float* scale;   // next adaRMSNorm (or the final norm)
+  int S;               // split-K slices to sum
+  const float* gate;   // residual gate of the finished sublayer
+  const float* scale;  // next adaRMSNorm (or the final norm)
   const float* shift;
-  bool final_step;      // last layer: final norm, action-out projection, Euler update
-  const float* nscale;  // final: the next step's first norm (nullptr after the last step)
-  const float* nshift;
+  bool final_step;     // last layer: final norm, action-out projection, Euler update
 };
 
 // ---- phases 4, 7: row owner updates -----------------------------------------------
 __device__ __forceinline__ void phase_rows(const PersistArgs& a, const RowJob& r, float& xreg, float* hrow,
-                                           const float* bin, const bf16* win, float* xs, char* smem) {
+                                           const float* bin, float* xs, char* smem) {
   const int m = blockIdx.x, W = a.W, A = a.A, t = threadIdx.x;
   if (m >= a.M) return;
   float* red = reinterpret_cast<float*>(smem);  // [NWV]
@@ -623,7 +676,14 @@ __device__ __forceinline__ void phase_rows(const PersistArgs& a, const RowJob& r
     if (m % a.H >= a.n_fixed) xreg += a.dt * (v + bo);
     xs[t] = xreg;
   }
-  if (r.nscale) inproj_row(a, r.nscale, r.nshift, hrow, bin, win, xs, red);
+}
+
+__device__ __forceinline__ GemmJob make_job(const PersistArgs& a, int p, int l) {
+  const bf16* lay = reinterpret_cast<const bf16*>(a.w_frag) + (size_t)l * a.layer_elems;
+  if (p == 0) return GemmJob{a.y, lay, a.W, (a.nH + 2) * a.Dh / 32, 1, EPI_QKV};
+  if (p == 3) return GemmJob{a.o, lay + a.off_o, a.nH * a.Dh, a.W / 32, a.s_o, EPI_SLICE};
+  if (p == 5) return GemmJob{a.y, lay + a.off_gu, a.W, 2 * a.F / 32, 1, EPI_GEGLU};
+  return GemmJob{a.z, lay + a.off_d, a.F, a.W / 32, a.s_d, EPI_SLICE};
 }
 
 template <int DH>
@@ -631,7 +691,6 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[SMEM_BYTES];
   __shared__ __attribute__((aligned(16))) float s_hrow[MAX_W];  // residual row of the owned action row
   __shared__ __attribute__((aligned(16))) float s_bin[MAX_W];
-  __shared__ __attribute__((aligned(16))) bf16 s_win[WIN_ELEMS];  // in-projection weights, [A][W]
   __shared__ float s_x[64];
   __shared__ u32 s_abort;
   const int t = threadIdx.x, m = blockIdx.x;
@@ -640,24 +699,6 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   float xreg = 0.f;
   if (t == 0) s_abort = 0u;
   if (owner) {
-    // W_in [W][A] -> LDS transposed [A][W]; 16-byte granules, four per thread in flight
-    const bf16* wi = reinterpret_cast<const bf16*>(a.w_in);
-    const int ng = W * A / 8;
-    for (int g0 = t; g0 < ng; g0 += 4 * PT) {
-      u32x4 v[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        v[u] = g0 + PT * u < ng ? *reinterpret_cast<const u32x4*>(wi + (size_t)(g0 + PT * u) * 8) : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (g0 + PT * u >= ng) break;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int el = (g0 + PT * u) * 8 + e, n = el / A, c = el - n * A;
-          s_win[c * W + n] = __builtin_bit_cast(bf16, (unsigned short)(v[u][e >> 1] >> (16 * (e & 1))));
-        }
-      }
-    }
     for (int k4 = 4 * t; k4 < W; k4 += 4 * PT)
       *reinterpret_cast<f32x4*>(s_bin + k4) = *reinterpret_cast<const f32x4*>(a.b_in + k4);
     if (t < A) {
@@ -667,22 +708,23 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   }
   __syncthreads();
   u32 epoch = 0;
-  if (owner) inproj_row(a, a.table, a.table + W, s_hrow, s_bin, s_win, s_x, reinterpret_cast<float*>(smem));
-  grid_sync(a, ++epoch, &s_abort);
   const int last_phase = a.n_steps * L * 8 - 1;
-  for (int ph = 0; ph <= last_phase; ++ph) {
-    const int k = ph / (8 * L), l = (ph / 8) % L, p = ph % 8;
+  // ph = -1 is the first step's in-projection; the later ones follow the final
+  // row phase of the previous step in the same workgroup (no barrier between)
+  for (int ph = -1; ph <= last_phase; ++ph) {
+    // in-projection + first norm of step ki (one call site for every step)
+    int ki = ph < 0 ? 0 : -1;
+    const int k = ph < 0 ? 0 : ph / (8 * L), l = ph < 0 ? 0 : (ph / 8) % L, p = ph < 0 ? -1 : ph % 8;
     const float* tk = a.table + (size_t)k * a.R;
     const float* am = tk + (size_t)(2 * l) * 3 * W;      // attention modulation: scale | shift | gate
     const float* mm = tk + (size_t)(2 * l + 1) * 3 * W;  // MLP modulation
-    const bf16* lay = reinterpret_cast<const bf16*>(a.w_layers) + (size_t)l * a.layer_elems;
-    if (p == 1) {
+    if (p < 0) {
+    } else if (p == 1) {
       phase_attn<DH>(a, l, smem);
     } else if (p == 2) {
       phase_combine(a, smem);
     } else if (p == 4 || p == 7) {
       RowJob r;
-      r.nscale = r.nshift = nullptr;
       r.final_step = false;
       if (p == 4) {
         r.S = a.s_o;
@@ -700,29 +742,34 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
           r.scale = fm;
           r.shift = fm + W;
           r.final_step = true;
-          if (k + 1 < a.n_steps) {
-            r.nscale = tk + a.R;
-            r.nshift = tk + a.R + W;
-          }
         }
       }
-      phase_rows(a, r, xreg, s_hrow, s_bin, s_win, s_x, smem);
+      phase_rows(a, r, xreg, s_hrow, s_bin, s_x, smem);
+      if (r.final_step && k + 1 < a.n_steps) ki = k + 1;  // same workgroup, no barrier needed
     } else {
-      GemmJob j;
-      if (p == 0) {
-        j = GemmJob{a.y, lay, W, (a.nH + 2) * a.Dh / 32, 1, EPI_QKV};
-      } else if (p == 3) {
-        j = GemmJob{a.o, lay + a.off_o, a.nH * a.Dh, W / 32, a.s_o, EPI_SLICE};
-      } else if (p == 5) {
-        j = GemmJob{a.y, lay + a.off_gu, W, 2 * a.F / 32, 1, EPI_GEGLU};
-      } else {
-        j = GemmJob{a.z, lay + a.off_d, a.F, W / 32, a.s_d, EPI_SLICE};
-      }
-      phase_gemm(a, j, l, smem);
+      phase_gemm(a, make_job(a, p, l), l, smem);
+    }
+    if (ki >= 0 && owner) {
+      const float* ti = a.table + (size_t)ki * a.R;
+      inproj_row(a, ti, ti + W, s_hrow, s_bin, s_x, reinterpret_cast<float*>(smem));
     }
     if (ph < last_phase) grid_sync(a, ++epoch, &s_abort);
   }
   if (owner && t < A) a.x[(size_t)m * A + t] = xreg;
+}
+
+// dst = fragment-ordered copy of the row-major bf16 matrix src [R][K]
+// (R % 16 == 0, K % 32 == 0); one 16-byte chunk per thread.
+__global__ void k_frag_order(const u32x4* __restrict__ src, u32x4* __restrict__ dst, int R, int K) {
+  const int KS = K / 32;
+  const size_t n = (size_t)(R / 16) * KS * 64;
+  for (size_t c = (size_t)blockIdx.x * blockDim.x + threadIdx.x; c < n; c += (size_t)gridDim.x * blockDim.x) {
+    const size_t blk = c / 64;
+    const int l = (int)(c % 64);
+    const size_t row = (blk / KS) * 16 + (l & 15);
+    const int k = (int)(blk % KS) * 32 + (l >> 4) * 8;
+    dst[c] = src[(row * K + k) / 8];
+  }
 }
 
 __global__ void k_persist_reset(u32* flags, int n) {  // n = FLAG_WORDS
@@ -735,7 +782,7 @@ __global__ void k_persist_reset(u32* flags, int n) {  // n = FLAG_WORDS
 bool persist_supported(jpi_dtype dt, int M, int W, int nH, int Dh, int F, int H, int A, int Pmax) {
   if (dt != JPI_BF16 || M > 64 || H > 64 || nH % 2 != 0 || !(Dh == 64 || Dh == 128 || Dh == 256)) return false;
   if (W % (NWV * 32) != 0 || F % (NWV * 32) != 0 || (nH * Dh) % (NWV * 32) != 0) return false;
-  if (W > MAX_W || A < 1 || A > 64 || A * W > WIN_ELEMS || Pmax + H > MAX_CH * KC) return false;
+  if (W > MAX_W || A < 1 || A > 64 || Pmax + H > MAX_CH * KC) return false;
   const int apad = A <= 8 ? 8 : A <= 16 ? 16 : A <= 32 ? 32 : 64;
   const int kper = W / (PT / apad);  // action-out projection: columns per thread
   return kper % 8 == 0 && kper <= OUT_G * 8;
@@ -754,6 +801,15 @@ int persist_block_threads() { return PT; }
 int persist_max_grid() { return MAX_GRID; }
 
 int persist_flag_words() { return FLAG_WORDS; }
+
+hipError_t launch_frag_order(const void* src, void* dst, int R, int K, hipStream_t s) {
+  if (R % 16 != 0 || K % 32 != 0) return hipErrorInvalidValue;
+  const size_t n = (size_t)(R / 16) * (K / 32) * 64;
+  const int grid = (int)std::min<size_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_frag_order, dim3(grid), dim3(256), 0, s, reinterpret_cast<const u32x4*>(src),
+                     reinterpret_cast<u32x4*>(dst), R, K);
+  return hipGetLastError();
+}
 
 hipError_t persist_occupancy(int Dh, int* blocks_per_cu) {
   switch (Dh) {

@@ -109,6 +109,9 @@ struct jpi_ctx {
   unsigned* pflags = nullptr;  // barrier arrival lines (one per workgroup) + release line
   unsigned* perr = nullptr;    // barrier timeout word
   int persist_occ = -1;        // workgroups per CU the persistent kernel fits (-1: not queried)
+  void* w_frag = nullptr;      // layer weights with every matrix fragment-ordered
+  bool frag_ready = false;     // w_frag matches w_layers
+  void *ysw = nullptr, *osw = nullptr, *zsw = nullptr, *qsw = nullptr;  // fragment-ordered activations
   // measurement: events around every launch of one kernel kind
   int timed_kind = JPI_KERNEL_NONE;
   std::vector<hipEvent_t> ev;  // pairs (start, end)
@@ -259,7 +262,8 @@ jpi_status jpi_destroy(jpi_ctx* c) {
   drop_events(c);
   void* bufs[] = {c->w_layers, c->w_in, c->w_t0, c->w_t1, c->w_mod, c->w_out, c->b_in, c->b_t0, c->b_t1, c->b_mod,
                   c->b_out, c->kp, c->vp, c->vpt, c->d_prefix_len, c->rope_tab, c->committed, c->x, c->h, c->y, c->q, c->ks,
-                  c->vst, c->o, c->z, c->partial, c->opart, c->pflags, c->perr};
+                  c->vst, c->o, c->z, c->partial, c->opart, c->pflags, c->perr, c->w_frag, c->ysw, c->osw,
+                  c->zsw, c->qsw};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   if (c->h_prefix_len) (void)hipHostFree(c->h_prefix_len);
@@ -481,6 +485,7 @@ jpi_status jpi_set_weight(jpi_ctx* c, const char* name, const void* data, int64_
   HIPCHK(c, hipStreamSynchronize(s));
   c->have[have_index(c, kind, layer)] = 1;
   c->finalized = false;
+  c->frag_ready = false;
   drop_graphs(c);
   drop_tables(c);
   return JPI_OK;
@@ -501,6 +506,7 @@ jpi_status jpi_finalize_weights(jpi_ctx* c, void* stream) {
   drop_graphs(c);
   drop_tables(c);
   c->finalized = true;
+  c->frag_ready = false;
   return JPI_OK;
 }
 
@@ -672,7 +678,44 @@ jpi_status ensure_scratch(jpi_ctx* c, int batch, int prefix) {
     c->attn_cap = attn;
     changed = true;
   }
+  if (p.persist && !c->ysw) {
+    // fragment-ordered activations, 64 padded rows (the padding stays zero)
+    const size_t es = c->esz, bq = std::max(1, 64 / c->H);
+    TRY(dmalloc(c, &c->ysw, (size_t)64 * c->W * es));
+    TRY(dmalloc(c, &c->osw, (size_t)64 * c->nH * c->Dh * es));
+    TRY(dmalloc(c, &c->zsw, (size_t)64 * c->F * es));
+    TRY(dmalloc(c, &c->qsw, bq * c->nH * 64 * c->Dh * es));
+    HIPCHK(c, hipMemset(c->ysw, 0, (size_t)64 * c->W * es));
+    HIPCHK(c, hipMemset(c->osw, 0, (size_t)64 * c->nH * c->Dh * es));
+    HIPCHK(c, hipMemset(c->zsw, 0, (size_t)64 * c->F * es));
+    HIPCHK(c, hipMemset(c->qsw, 0, bq * c->nH * 64 * c->Dh * es));
+    HIPCHK(c, hipDeviceSynchronize());
+    changed = true;
+  }
+  if (p.persist && !c->w_frag) {
+    TRY(dmalloc(c, &c->w_frag, c->layer_elems * c->L * c->esz));
+    c->frag_ready = false;
+    changed = true;
+  }
   if (changed) drop_graphs(c);  // captured graphs point at the old scratch
+  return JPI_OK;
+}
+
+// Fragment-ordered copy of the layer weights for the single-launch path
+// (enqueued on s before the kernel that reads it; redone after weight changes).
+jpi_status ensure_frag(jpi_ctx* c, hipStream_t s) {
+  if (c->frag_ready) return JPI_OK;
+  const int W = c->W, HD = c->nH * c->Dh, F = c->F;
+  const size_t es = c->esz;
+  for (int l = 0; l < c->L; ++l) {
+    const char* src = (const char*)c->w_layers + (size_t)l * c->layer_elems * es;
+    char* dst = (char*)c->w_frag + (size_t)l * c->layer_elems * es;
+    HIPCHK(c, launch_frag_order(src, dst, (c->nH + 2) * c->Dh, W, s));
+    HIPCHK(c, launch_frag_order(src + c->off_o * es, dst + c->off_o * es, W, HD, s));
+    HIPCHK(c, launch_frag_order(src + c->off_gu * es, dst + c->off_gu * es, 2 * F, W, s));
+    HIPCHK(c, launch_frag_order(src + c->off_d * es, dst + c->off_d * es, W, F, s));
+  }
+  c->frag_ready = true;
   return JPI_OK;
 }
 
@@ -727,6 +770,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     pa.eps = eps;
     pa.dt = dt_step;
     pa.w_layers = c->w_layers;
+    pa.w_frag = c->w_frag;
     pa.layer_elems = (int64_t)c->layer_elems;
     pa.off_o = (int64_t)c->off_o;
     pa.off_gu = (int64_t)c->off_gu;
@@ -747,15 +791,15 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     pa.rope = c->rope_tab;
     pa.x = c->x;
     pa.h = c->h;
-    pa.y = c->y;
-    pa.q = c->q;
+    pa.y = c->ysw;
+    pa.q = c->qsw;
     pa.ks = c->ks;
     pa.vst = c->vst;
     pa.opart = c->opart;
     pa.ml = c->opart + (size_t)batch * nH * pa.C * H * Dh;
-    pa.o = c->o;
+    pa.o = c->osw;
     pa.part = c->partial;
-    pa.z = c->z;
+    pa.z = c->zsw;
     pa.flags = c->pflags;
     pa.err = c->perr;
     timing(JPI_KERNEL_PERSISTENT, &pa.ev_start, &pa.ev_stop);
@@ -905,6 +949,7 @@ jpi_status jpi_denoise(jpi_ctx* c, const float* noise_dev, int n_steps, float* a
   float* table = nullptr;
   TRY(ensure_table(c, n_steps, s, &table));
   TRY(ensure_scratch(c, c->batch, c->prefix));
+  if (use_persist(c, c->batch)) TRY(ensure_frag(c, s));
   HIPCHK(c, launch_init_x(noise_dev, c->committed, c->x, c->batch, c->H, c->A, c->n_fixed, s));
   if (eager_mode() || c->timed_kind >= 0) {
     HIPCHK(c, enqueue_steps(c, table, n_steps, s));
