@@ -67,6 +67,7 @@ constexpr int MAX_CH = 128;   // attention chunks per rollout
 constexpr unsigned SPIN_LIMIT = 1u << 21;
 constexpr int SMEM_BYTES = 42496;      // per-phase scratch (attention staging at Dh = 256)
 constexpr int MAX_W = 2048;            // model width held in LDS by a row owner
+constexpr int WT_STEPS = 32;           // weight tile in LDS: 32-wide k steps of a 32-row tile (64 KB)
 constexpr int RMAX_S = 16;             // split-K slices summed by the row phases
 constexpr int MAX_GRID = 256;          // barrier flags are polled as 64 lanes x 4 lines
 constexpr int FLAG_STRIDE = 32;        // words between barrier flags: one 128-byte line per workgroup
@@ -80,6 +81,8 @@ typedef unsigned u32;
 typedef u32 u32x2 __attribute__((ext_vector_type(2)));
 typedef u32 u32x4 __attribute__((ext_vector_type(4)));
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef __attribute__((address_space(3))) char lds_t;  // LDS byte pointer (direct-to-LDS loads)
+typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
 
 // Buffer resource over [base, base + bytes): loads beyond the range return
 // zero and stores beyond it are dropped.
@@ -137,12 +140,42 @@ __device__ __forceinline__ float block_sum_wg(float v, float* red) {
   return t;
 }
 
+struct GemmJob {
+  const void* A;  // activations, fragment-ordered [64][K] bf16
+  const bf16* w;  // weights, fragment-ordered [N][K] bf16
+  int K;          // reduction length
+  int tiles;      // N / 32
+  int S;          // split-K slices
+  int kind;       // EPI_*
+};
+
+// Direct-to-LDS loads of k steps [ks0, ks0 + nk) of row groups rg0, rg0 + 1 of
+// the fragment-ordered matrix W (KS k steps per row group) into the tile
+// [2][nk][64 lanes][16 B]; waves w0 .. NWV-1 take the 1 KB blocks round-robin.
+__device__ __forceinline__ void load_wtile(lds_t* lds, const bf16* W, int KS, int rg0, int ks0, int nk, int w0) {
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (wave < w0) return;
+  for (int i = wave - w0; i < 2 * nk; i += NWV - w0) {
+    const int rgl = i >= nk, kk = i - rgl * nk;
+    __builtin_amdgcn_global_load_lds(W + ((size_t)((rg0 + rgl) * KS + ks0 + kk) * 64 + lane) * 8, lds + i * 1024, 16,
+                                     0, 0);
+  }
+}
+
 // Grid barrier.  Each workgroup stores its arrival epoch into its own 128-byte
 // flag line; wave 0 of every workgroup then polls all lines (lane l reads the
-// lines of workgroups l, l+64, l+128, l+192 with independent loads).
-__device__ __forceinline__ void grid_sync(const PersistArgs& a, u32 epoch, u32* s_abort) {
+// lines of workgroups l, l+64, l+128, l+192 with independent loads).  If the
+// next phase is a GEMM, waves 1..3 meanwhile start the direct-to-LDS loads of
+// the workgroup's first weight tile so that their latency overlaps the wait;
+// the closing workgroup barrier does not wait for them (the GEMM does).
+__device__ __forceinline__ void grid_sync(const PersistArgs& a, u32 epoch, u32* s_abort, bool gemm_next,
+                                          const GemmJob& next, lds_t* wt) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  if (gemm_next && (int)blockIdx.x < next.tiles * next.S) {
+    const int it = blockIdx.x, t = it % next.tiles, sl = it / next.tiles, nk_item = next.K / next.S / 32;
+    load_wtile(wt, next.w, next.K / 32, 2 * t, sl * nk_item, min(WT_STEPS, nk_item), 1);
+  }
   if (threadIdx.x < 64) {
     const rsrc_t rf = rsrc(a.flags);
     if (threadIdx.x == 0) st4(rf, blockIdx.x * (FLAG_STRIDE * 4u), epoch);
@@ -166,87 +199,62 @@ __device__ __forceinline__ void grid_sync(const PersistArgs& a, u32 epoch, u32* 
       }
     }
   }
-  __syncthreads();
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // s_abort
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // ---------------------------------------------------------------------------
-// GEMM item: rows 0..63 x 32 output columns [n0, n0+32) over the K range
-// [kbeg, kbeg + klen), split evenly over the waves.  A (`ra`, fragment-ordered,
-// 64 padded rows, read coherently) contributes its first `mgroups` 16-row
-// groups; W is the fragment-ordered weight matrix with KS k steps.  All
-// fragments of a wave's K range are loaded before the first MFMA.  Returns
-// the sums for m-subtile `wave` in lo (columns n0 + lane%16) and hi
-// (n0 + 16 + lane%16).
+// GEMM items: 32 output columns (two 16-row groups of W) x all 64 padded rows
+// x a K range of 32-wide k steps, split evenly over the waves.  The weight
+// part lives in the LDS tile (filled by direct-to-LDS loads: for a
+// workgroup's first item during the preceding grid barrier, otherwise here);
+// A (fragment-ordered, read coherently) contributes its first `mgroups`
+// 16-row groups.  K ranges longer than the tile are processed in chunks.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void gemm_item(rsrc_t ra, int mgroups, const bf16* W, int KS, int n0, int kbeg, int klen,
-                                          f32x4* red, f32x4& lo, f32x4& hi) {
+__device__ __forceinline__ void gemm_chunk(rsrc_t ra, int mgroups, int KS, int ksA, const lds_t* wt, int nk,
+                                           f32x4 (&acc)[4][2]) {
   using MF = Mfma<bf16>;
   constexpr int BATCH = 8;
-  static_assert(NWV == 4, "one m-subtile of the 64-row tile per wave");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int kw = klen / NWV;
-  const int s_beg = (kbeg + wave * kw) / MF::KSUB;
-  const int nsub = kw / MF::KSUB;
-  const bf16* wp0 = W + ((size_t)((n0 >> 4) * KS + s_beg) * 64 + lane) * 8;
-  const bf16* wp1 = wp0 + (size_t)KS * 512;  // next 16-row group
-  const u32 aoff = (u32)(s_beg * 64 + lane) * 16u;
-  const u32 astep = (u32)KS * 1024u;  // bytes per 16-row group
-  f32x4 acc[4][2];
-#pragma unroll
-  for (int a = 0; a < 4; ++a) acc[a][0] = acc[a][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nsub = nk / NWV, kk0 = wave * nsub;
+  const u32 aoff = (u32)((ksA + kk0) * 64 + lane) * 16u;
+  const u32 astep = (u32)KS * 1024u;  // bytes per 16-row group of A
   for (int s0 = 0; s0 < nsub; s0 += BATCH) {
-    MF::frag wf[BATCH][2], af[BATCH][4];
-#pragma unroll
-    for (int c = 0; c < BATCH; ++c) {
-      const bool ok = s0 + c < nsub;
-      wf[c][0] = ok ? MF::load(wp0 + (s0 + c) * 512) : MF::frag{};
-      wf[c][1] = ok ? MF::load(wp1 + (s0 + c) * 512) : MF::frag{};
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-        af[c][a] = (ok && a < mgroups)
-                       ? __builtin_bit_cast(MF::frag, ld16(ra, aoff + a * astep + (u32)(s0 + c) * 1024u))
-                       : MF::frag{};
-    }
+    MF::frag af[BATCH][4];
 #pragma unroll
     for (int c = 0; c < BATCH; ++c)
 #pragma unroll
+      for (int a = 0; a < 4; ++a)
+        af[c][a] = (s0 + c < nsub && a < mgroups)
+                       ? __builtin_bit_cast(MF::frag, ld16(ra, aoff + a * astep + (u32)(s0 + c) * 1024u))
+                       : MF::frag{};
+    if (s0 == 0) {  // every wave's part of the tile has landed
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+    }
+#pragma unroll
+    for (int c = 0; c < BATCH; ++c) {
+      if (s0 + c >= nsub) break;
+      const int kk = kk0 + s0 + c;
+      const MF::frag w0 = *(lds_frag*)(wt + (kk * 64 + lane) * 16);
+      const MF::frag w1 = *(lds_frag*)(wt + ((nk + kk) * 64 + lane) * 16);
+#pragma unroll
       for (int a = 0; a < 4; ++a) {
-        acc[a][0] = MF::run(af[c][a], wf[c][0], acc[a][0]);
-        acc[a][1] = MF::run(af[c][a], wf[c][1], acc[a][1]);
+        acc[a][0] = MF::run(af[c][a], w0, acc[a][0]);
+        acc[a][1] = MF::run(af[c][a], w1, acc[a][1]);
       }
+    }
   }
-  // red layout [wave][a][2][64]
-#pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    red[((wave * 4 + a) * 2 + 0) * 64 + lane] = acc[a][0];
-    red[((wave * 4 + a) * 2 + 1) * 64 + lane] = acc[a][1];
-  }
-  __syncthreads();
-  lo = red[((0 * 4 + wave) * 2 + 0) * 64 + lane];
-  hi = red[((0 * 4 + wave) * 2 + 1) * 64 + lane];
-#pragma unroll
-  for (int v = 1; v < NWV; ++v) {
-    lo += red[((v * 4 + wave) * 2 + 0) * 64 + lane];
-    hi += red[((v * 4 + wave) * 2 + 1) * 64 + lane];
-  }
-  __syncthreads();  // red is reused by the next item
 }
 
-struct GemmJob {
-  const void* A;  // activations, fragment-ordered [64][K] bf16
-  const bf16* w;  // weights, fragment-ordered [N][K] bf16
-  int K;          // reduction length
-  int tiles;      // N / 32
-  int S;          // split-K slices
-  int kind;       // EPI_*
-};
 
 // ---- phases 0, 3, 5, 6: GEMM with a per-kind epilogue ----------------------
-__device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& j, int l, char* smem) {
+__device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& j, int l, lds_t* wt, char* smem) {
   f32x4* red = reinterpret_cast<f32x4*>(smem);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, fr = lane & 15;
   const int Dh = a.Dh, half = Dh / 2, H = a.H, nH = a.nH, qcols = nH * Dh, M = a.M, Wd = a.W;
-  const int klen = j.K / j.S, KS = j.K / 32, mgroups = (M + 15) / 16;
+  const int klen = j.K / j.S, KS = j.K / 32, nk_item = klen / 32, mgroups = (M + 15) / 16;
   const rsrc_t ra = rsrc(j.A, (u32)(64 * j.K * 2));
   const rsrc_t rq = rsrc(a.q), rk = rsrc(a.ks), rz = rsrc(a.z), rp = rsrc(a.part);
   const rsrc_t rv = rsrc(reinterpret_cast<const bf16*>(a.vpt) + (size_t)l * a.vpt_lstride);
@@ -269,8 +277,32 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
       cs[e] = (roped && row < M) ? a.rope[(size_t)row * half + d] : float2{1.f, 0.f};
       plv[e] = (qkv && !roped && row < M) ? a.prefix_len[row / H] : 0;
     }
-    f32x4 lo, hi;
-    gemm_item(ra, mgroups, j.w, KS, t * 32, s * klen, klen, red, lo, hi);
+    f32x4 acc[4][2];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[q][0] = acc[q][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int cs0 = 0; cs0 < nk_item; cs0 += WT_STEPS) {
+      const int nk = min(WT_STEPS, nk_item - cs0);
+      if (it != (int)blockIdx.x || cs0 != 0) {  // not loaded during the barrier
+        __syncthreads();                         // every wave is done with the tile
+        load_wtile(wt, j.w, KS, 2 * t, s * nk_item + cs0, nk, 0);
+      }
+      gemm_chunk(ra, mgroups, KS, s * nk_item + cs0, wt, nk, acc);
+    }
+    // reduce the four waves' K partial sums; wave w keeps m-subtile w
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      red[((wave * 4 + q) * 2 + 0) * 64 + lane] = acc[q][0];
+      red[((wave * 4 + q) * 2 + 1) * 64 + lane] = acc[q][1];
+    }
+    __syncthreads();
+    f32x4 lo = red[((0 * 4 + wave) * 2 + 0) * 64 + lane];
+    f32x4 hi = red[((0 * 4 + wave) * 2 + 1) * 64 + lane];
+#pragma unroll
+    for (int v = 1; v < NWV; ++v) {
+      lo += red[((v * 4 + wave) * 2 + 0) * 64 + lane];
+      hi += red[((v * 4 + wave) * 2 + 1) * 64 + lane];
+    }
+    __syncthreads();  // red and the tile are reused by the next item
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int row = wave * 16 + (lane >> 4) * 4 + e;
@@ -689,6 +721,7 @@ __device__ __forceinline__ GemmJob make_job(const PersistArgs& a, int p, int l) 
 template <int DH>
 __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[SMEM_BYTES];
+  __shared__ __attribute__((aligned(16))) char s_wt[WT_STEPS * 2 * 1024];  // weight tile of the current GEMM
   __shared__ __attribute__((aligned(16))) float s_hrow[MAX_W];  // residual row of the owned action row
   __shared__ __attribute__((aligned(16))) float s_bin[MAX_W];
   __shared__ float s_x[64];
@@ -707,6 +740,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     }
   }
   __syncthreads();
+  lds_t* wt = (lds_t*)s_wt;
   u32 epoch = 0;
   const int last_phase = a.n_steps * L * 8 - 1;
   // ph = -1 is the first step's in-projection; the later ones follow the final
@@ -747,13 +781,18 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
       phase_rows(a, r, xreg, s_hrow, s_bin, s_x, smem);
       if (r.final_step && k + 1 < a.n_steps) ki = k + 1;  // same workgroup, no barrier needed
     } else {
-      phase_gemm(a, make_job(a, p, l), l, smem);
+      phase_gemm(a, make_job(a, p, l), l, wt, smem);
     }
     if (ki >= 0 && owner) {
       const float* ti = a.table + (size_t)ki * a.R;
       inproj_row(a, ti, ti + W, s_hrow, s_bin, s_x, reinterpret_cast<float*>(smem));
     }
-    if (ph < last_phase) grid_sync(a, ++epoch, &s_abort);
+    if (ph < last_phase) {
+      const int pn = (ph + 1) % 8, ln = ((ph + 1) / 8) % L;  // the next phase
+      const bool gemm_next = pn == 0 || pn == 3 || pn == 5 || pn == 6;
+      const GemmJob nj = make_job(a, pn, ln);
+      grid_sync(a, ++epoch, &s_abort, gemm_next, nj, wt);
+    }
   }
   if (owner && t < A) a.x[(size_t)m * A + t] = xreg;
 }
