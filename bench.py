@@ -6,15 +6,21 @@ every layer attending to the resident prefix KV), on inputs already resident
 in HBM.  Prints one JSON line:
 
   value      action chunks/s = batch * steps / timed seconds
-  roofline   the dominant weight-streaming kernel's algorithmic bytes per
-             launch / its average launch duration (start/stop HIP events tied
-             to every dispatch of that kernel on the stream it runs on, in a
-             timing pass right after the timed region), against MI355X's
-             8 TB/s HBM peak; "kernels" gives the same for every kernel kind
-  cpu_baseline  the fp64 CPU oracle timed on the host cores on one denoise call
-                of rollout 0 (a bounded sample)
+  roofline   the dominant kernel's algorithmic bytes per launch / its average
+             launch duration (start/stop HIP events tied to every dispatch of
+             that kernel on the stream it runs on, in a timing pass right after
+             the timed region), against MI355X's 8 TB/s HBM peak.  With
+             batch * horizon <= 64 the whole call is one persistent kernel;
+             otherwise the largest GEMM kind.  "kernels" lists every kind that
+             ran.  "traffic" is the HBM bytes per launch measured with the
+             FETCH_SIZE / WRITE_SIZE counters (scaled by a plain copy of known
+             size, see --calibrate-copy) when the counters were taken on the
+             current kernel source, else null
+  cpu_baseline  the fp64 CPU oracle timed on the host cores, repeating the
+                denoise of rollout 0 for at least 10 s (a bounded sample)
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+       python bench.py --calibrate-copy MIB   (a plain device copy, for counter scaling)
 """
 from __future__ import annotations
 
@@ -32,6 +38,35 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 
 METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roofline"
+
+# HBM traffic per launch of the persistent kernel from the FETCH_SIZE and
+# WRITE_SIZE counters (rocprofv3 --pmc, one counter per run), keyed by the
+# sha256 of the kernel source they were measured on; the byte counts are the
+# counter readings times the copy calibration factor.
+MEASURED_TRAFFIC = {
+    # pi0.5 shape, batch 1: FETCH_SIZE 5815772.8 KiB x 1.99979 (a 256 MiB copy
+    # reads back 131085.2 KiB) + WRITE_SIZE 3059826.2 KiB x 1.0 (the copy's
+    # 262144 KiB), mean over 29 dispatches
+    ("746579a9f13a6325f27f823c85176054f11b3e2408756d21633aeacfd3e628ac", "pi05-b1"): 15042765340,
+}
+
+
+def kernel_source_hash():
+    import hashlib
+    with open(os.path.join(ROOT, "paper_2607_12659_amd", "csrc", "jpi_persist.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def calibrate_copy(mib):
+    """A plain device-to-device copy of known size (for scaling the counters)."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}), flush=True)
 
 
 def algorithmic_counts(wl):
@@ -73,12 +108,18 @@ def cpu_baseline(wl, weights, K, V, noise):
         threads = os.cpu_count()
     ex = oracle.Expert(wl.dims, weights)
     lens = wl.valid_lengths()[:1]
-    t0 = time.perf_counter()
-    oracle.denoise(ex, noise[:1], K[:, :1], V[:, :1], lens, wl.n_steps)
-    dt = time.perf_counter() - t0
-    return {"value": round(1.0 / dt, 4), "unit": "chunks/s", "cores": int(threads), "kind": "oracle",
-            "sample": "one %d-step denoise of rollout 0 of %s (fp64 numpy, BLAS threads=%d), %.1f s"
-                      % (wl.n_steps, wl.name, threads, dt)}
+    # Bounded sample: repeat the denoise of rollout 0 until at least 10 s of host time
+    # has passed (and at most 16 calls), then report calls per second.
+    calls, t0 = 0, time.perf_counter()
+    while True:
+        oracle.denoise(ex, noise[:1], K[:, :1], V[:, :1], lens, wl.n_steps)
+        calls += 1
+        dt = time.perf_counter() - t0
+        if dt >= 10.0 or calls >= 16:
+            break
+    return {"value": round(calls / dt, 4), "unit": "chunks/s", "cores": int(threads), "kind": "oracle",
+            "sample": "%d repeated %d-step denoise calls on rollout 0 of %s (fp64 numpy, BLAS threads=%d), "
+                      "%.1f s in total" % (calls, wl.n_steps, wl.name, threads, dt)}
 
 
 def main():
@@ -90,9 +131,13 @@ def main():
     ap.add_argument("--timed-kernel", default="auto",
                     choices=["auto", "persistent", "qkv", "attention", "oproj", "gateup", "down"])
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the denoise of one chunk runs on "
+        print("bench.py measures one GPU: libjpi has no multi-GPU path (the denoise of one chunk runs on "
               "one MI355X; rollouts would shard data-parallel with no exchange). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
@@ -215,7 +260,9 @@ def main():
         "roofline": {"bound": "hbm", "kernel": ("k_persist (whole denoise call)" if kname == "persistent"
                                                 else "GEMM (%s)" % kname), "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None, "bytes_per_launch": kbytes, "avg_launch_us": round(k_avg_us, 3),
+                     "traffic": (MEASURED_TRAFFIC.get((kernel_source_hash(), wl.name))
+                                 if kname == "persistent" else None),
+                     "bytes_per_launch": kbytes, "avg_launch_us": round(k_avg_us, 3),
                      "launches_timed": tot_n},
         "kernels": per_kind,
         "call_roofline": {"algorithmic_bytes": counts["bytes_per_call"], "achieved_GBs": round(call_gbs, 1),
