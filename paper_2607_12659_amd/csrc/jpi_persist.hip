@@ -72,8 +72,11 @@ constexpr int RMAX_S = 16;             // split-K slices summed by the row phase
 constexpr int MAX_GRID = 256;          // barrier flags are polled as 64 lanes x 4 lines
 constexpr int FLAG_STRIDE = 32;        // words between barrier flags: one 128-byte line per workgroup
 constexpr int FLAG_WORDS = MAX_GRID * FLAG_STRIDE;
-constexpr int CPT = 8;     // combine: chunks per thread per round trip
+constexpr int CPT = 16;    // combine: chunks per thread per round trip
 constexpr int OUT_G = 16;  // action-out projection: 16-byte weight granules per thread
+#ifndef A_BATCH
+#define A_BATCH 8  // k steps of activation fragments per wave in flight
+#endif
 
 enum : int { EPI_QKV = 0, EPI_GEGLU = 1, EPI_SLICE = 2 };
 
@@ -83,6 +86,8 @@ typedef u32 u32x4 __attribute__((ext_vector_type(4)));
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 typedef __attribute__((address_space(3))) char lds_t;  // LDS byte pointer (direct-to-LDS loads)
 typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
+typedef __attribute__((address_space(3))) float lds_f32;
+typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
 
 // Buffer resource over [base, base + bytes): loads beyond the range return
 // zero and stores beyond it are dropped.
@@ -107,6 +112,9 @@ __device__ __forceinline__ u32 poll4(rsrc_t r, u32 off) {
   return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, CPOL_DEV);
 }
 __device__ __forceinline__ void st4(rsrc_t r, u32 off, u32 v) { __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, CPOL_DEV); }
+__device__ __forceinline__ void st16(rsrc_t r, u32 off, u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, CPOL_DEV);
+}
 __device__ __forceinline__ void st8(rsrc_t r, u32 off, u32x2 v) {
   __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, CPOL_DEV);
 }
@@ -215,20 +223,27 @@ __device__ __forceinline__ void grid_sync(const PersistArgs& a, u32 epoch, u32* 
 __device__ __forceinline__ void gemm_chunk(rsrc_t ra, int mgroups, int KS, int ksA, const lds_t* wt, int nk,
                                            f32x4 (&acc)[4][2]) {
   using MF = Mfma<bf16>;
-  constexpr int BATCH = 8;
+  constexpr int BATCH = A_BATCH;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nsub = nk / NWV, kk0 = wave * nsub;
+  // Every workgroup reads the same activation rows.  The k range of each wave
+  // and the order of its k steps are rotated by the workgroup index so that
+  // the workgroups do not request the same lines at the same moment.
+  const int nsub = nk / NWV, kk0 = ((wave + (int)blockIdx.x) & (NWV - 1)) * nsub;
+  const int rot = nsub > 0 ? ((int)blockIdx.x >> 2) % nsub : 0;
   const u32 aoff = (u32)((ksA + kk0) * 64 + lane) * 16u;
   const u32 astep = (u32)KS * 1024u;  // bytes per 16-row group of A
   for (int s0 = 0; s0 < nsub; s0 += BATCH) {
     MF::frag af[BATCH][4];
 #pragma unroll
-    for (int c = 0; c < BATCH; ++c)
+    for (int c = 0; c < BATCH; ++c) {
+      int kc = s0 + c + rot;
+      kc = kc >= nsub ? kc - nsub : kc;
 #pragma unroll
       for (int a = 0; a < 4; ++a)
         af[c][a] = (s0 + c < nsub && a < mgroups)
-                       ? __builtin_bit_cast(MF::frag, ld16(ra, aoff + a * astep + (u32)(s0 + c) * 1024u))
+                       ? __builtin_bit_cast(MF::frag, ld16(ra, aoff + a * astep + (u32)kc * 1024u))
                        : MF::frag{};
+    }
     if (s0 == 0) {  // every wave's part of the tile has landed
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
@@ -236,7 +251,9 @@ __device__ __forceinline__ void gemm_chunk(rsrc_t ra, int mgroups, int KS, int k
 #pragma unroll
     for (int c = 0; c < BATCH; ++c) {
       if (s0 + c >= nsub) break;
-      const int kk = kk0 + s0 + c;
+      int kc = s0 + c + rot;
+      kc = kc >= nsub ? kc - nsub : kc;
+      const int kk = kk0 + kc;
       const MF::frag w0 = *(lds_frag*)(wt + (kk * 64 + lane) * 16);
       const MF::frag w1 = *(lds_frag*)(wt + ((nk + kk) * 64 + lane) * 16);
 #pragma unroll
@@ -341,7 +358,7 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
 
 // ---- phase 1: attention chunk partials ----------------------------------------
 template <int DH>
-__device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* smem) {
+__device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* smem, lds_t* wt) {
   using MF = Mfma<bf16>;
   constexpr int PAD = 8, LDK = DH + PAD, LDV = KC + PAD, LDP = KC + PAD;
   constexpr int NST = DH / MF::KSUB, NJ = KC / 16;
@@ -461,14 +478,31 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
       for (int nt = 0; nt < DH / 16; ++nt)
         o[nt] = MF::run(pa, MF::load(&Vt[(nt * 16 + fr) * LDV + st * MF::KSUB + fk]), o[nt]);
     }
+    // A lane holds dims nt*16 + fr of its four rows.  Each wave writes its 16
+    // rows to its quarter of the (idle) weight-tile buffer and reads them back
+    // row-major, so that every store instruction writes whole rows.
     const size_t slot = ((size_t)b * nH + hn) * C + c;
+    static_assert(4 * 16 * DH * 4 <= WT_STEPS * 2 * 1024, "attention transpose buffer");
+    lds_f32* tb = reinterpret_cast<lds_f32*>(wt) + w * 16 * DH;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+#pragma unroll
+      for (int nt = 0; nt < DH / 16; ++nt) tb[((lane >> 4) * 4 + e) * DH + nt * 16 + fr] = o[nt][e];
+    __syncthreads();
+    constexpr int RPI = 256 / DH;  // rows per wave store instruction
+#pragma unroll
+    for (int r0 = 0; r0 < 16; r0 += RPI) {
+      const int rr = r0 + (lane * 4) / DH, i = w * 16 + rr;
+      if (i < H) {
+        const f32x4 v = *reinterpret_cast<lds_f32x4*>(tb + rr * DH + (lane * 4) % DH);
+        st16(ro, (u32)(((slot * H + i) * DH + (lane * 4) % DH) * 4),
+             u32x4{f2u(v[0]), f2u(v[1]), f2u(v[2]), f2u(v[3])});
+      }
+    }
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int i = prow + e;
       if (i < H) {
-        const u32 base = (u32)(((slot * H + i) * DH + fr) * 4);
-#pragma unroll
-        for (int nt = 0; nt < DH / 16; ++nt) st4(ro, base + nt * 64u, f2u(o[nt][e]));
         if (fr == 0)
           st8(rml, (u32)((slot * H + i) * 8), u32x2{f2u(mrow[e]), f2u(lrow[e])});
       }
@@ -478,24 +512,28 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
 }
 
 // ---- phase 2: combine chunk partials -> o -------------------------------------
-// One (rollout, head, query row) per iteration.  Thread t owns output columns
-// 4*(t % (Dh/4)) .. +4 and the chunks c = t / (Dh/4) + G*u (G chunk groups);
-// each pass loads CPT chunks' partial outputs and (max, sum) pairs in one
-// round trip and folds them into a running (max, sum, acc); the G groups are
-// then merged through LDS.
+// Two (rollout, head, query row) items per workgroup at a time, one per half
+// of the threads, so that every chunk load of both rows is in flight together.
+// Within a half, nq = Dh/4 threads cover the Dh positions of a partial row
+// (4 each) and G groups of them split the chunks; each pass loads CPT chunks'
+// partial outputs and (max, sum) pairs in one round trip and folds them into
+// a running (max, sum, acc); the G groups are then merged through LDS.
 __device__ __forceinline__ void phase_combine(const PersistArgs& a, char* smem) {
+  constexpr int TPR = PT / 2;
   const int H = a.H, nH = a.nH, C = a.C, Dh = a.Dh;
-  const int nq = Dh / 4, G = PT / nq;
-  const int t = threadIdx.x, q4 = t % nq, g = t / nq;
+  const int nq = Dh / 4, G = TPR / nq;
+  const int t = threadIdx.x, hf = t / TPR, tr = t - hf * TPR, q4 = tr % nq, g = tr / nq;
   float* sm = reinterpret_cast<float*>(smem);  // [PT] max, [PT] sum, [PT][4] acc
   float* sl = sm + PT;
   f32x4* sacc = reinterpret_cast<f32x4*>(sl + PT);
   const rsrc_t ro = rsrc(a.opart), rml = rsrc(a.ml), rout = rsrc(a.o);
-  const int rows = a.B * nH * H;
-  for (int r = blockIdx.x; r < rows; r += gridDim.x) {
-    const int i = r % H, bh = r / H;
+  const int rows = a.B * nH * H, pairs = (rows + 1) / 2;
+  for (int pr = blockIdx.x; pr < pairs; pr += gridDim.x) {
+    const int r = 2 * pr + hf;
+    const bool live = r < rows;
+    const int i = live ? r % H : 0, bh = live ? r / H : 0;
     const int b = bh / nH, hn = bh - b * nH;
-    const int nch = (a.prefix_len[b] + H + KC - 1) / KC;
+    const int nch = live ? (a.prefix_len[b] + H + KC - 1) / KC : 0;
     const size_t slot0 = (size_t)bh * C;
     float m = -INFINITY, lsum = 0.f;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -527,16 +565,17 @@ __device__ __forceinline__ void phase_combine(const PersistArgs& a, char* smem) 
     sl[t] = lsum;
     sacc[t] = acc;
     __syncthreads();
-    if (g == 0) {
+    if (live && g == 0) {
+      const int b0 = hf * TPR + q4;
       float mx = -INFINITY;
-      for (int gg = 0; gg < G; ++gg) mx = fmaxf(mx, sm[gg * nq + q4]);
+      for (int gg = 0; gg < G; ++gg) mx = fmaxf(mx, sm[b0 + gg * nq]);
       float L = 0.f;
       f32x4 o4 = f32x4{0.f, 0.f, 0.f, 0.f};
       for (int gg = 0; gg < G; ++gg) {
-        const float mg = sm[gg * nq + q4];
+        const float mg = sm[b0 + gg * nq];
         const float wg = mg == -INFINITY ? 0.f : expf(mg - mx);
-        o4 += wg * sacc[gg * nq + q4];
-        L += wg * sl[gg * nq + q4];
+        o4 += wg * sacc[b0 + gg * nq];
+        L += wg * sl[b0 + gg * nq];
       }
       o4 *= 1.0f / L;
       st8(rout, frag_off(b * H + i, hn * Dh + q4 * 4, nH * Dh / 32) * 2u, pack4_bf16(o4));
@@ -754,7 +793,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     const float* mm = tk + (size_t)(2 * l + 1) * 3 * W;  // MLP modulation
     if (p < 0) {
     } else if (p == 1) {
-      phase_attn<DH>(a, l, smem);
+      phase_attn<DH>(a, l, smem, wt);
     } else if (p == 2) {
       phase_combine(a, smem);
     } else if (p == 4 || p == 7) {
