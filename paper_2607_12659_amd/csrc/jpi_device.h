@@ -48,16 +48,52 @@ struct Mfma<float> {
 template <typename T>
 __device__ __forceinline__ T from_f32(float v) { return static_cast<T>(v); }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+// Value of another lane of the same 16-lane row through a DPP operand
+// modifier (one VALU move; no LDS crossbar round trip).
+template <int CTRL>
+__device__ __forceinline__ float dpp_row(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+constexpr int DPP_QUAD_XOR1 = 0xb1;   // quad_perm [1,0,3,2]
+constexpr int DPP_QUAD_XOR2 = 0x4e;   // quad_perm [2,3,0,1]
+constexpr int DPP_HALF_MIRROR = 0x141;  // lane i <-> 7 - i within each half-row
+constexpr int DPP_MIRROR = 0x140;       // lane i <-> 15 - i within each row
+
+// Sum over the 16 lanes that share lane / 16 (one row group of an MFMA tile).
+// Every stage pairs lanes whose partial results are equal, so all 16 lanes
+// end with the same bits.
+__device__ __forceinline__ float group16_sum(float v) {
+  v += dpp_row<DPP_QUAD_XOR1>(v);
+  v += dpp_row<DPP_QUAD_XOR2>(v);
+  v += dpp_row<DPP_HALF_MIRROR>(v);
+  v += dpp_row<DPP_MIRROR>(v);
+  return v;
+}
+__device__ __forceinline__ float group16_max(float v) {
+  v = fmaxf(v, dpp_row<DPP_QUAD_XOR1>(v));
+  v = fmaxf(v, dpp_row<DPP_QUAD_XOR2>(v));
+  v = fmaxf(v, dpp_row<DPP_HALF_MIRROR>(v));
+  v = fmaxf(v, dpp_row<DPP_MIRROR>(v));
   return v;
 }
 
+// Whole-wave sum, the same in every lane: row sums, then the four rows in order.
+__device__ __forceinline__ float wave_sum(float v) {
+  v = group16_sum(v);
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return ((r0 + r1) + r2) + r3;
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = group16_max(v);
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
 
 __device__ __forceinline__ double wave_sum_d(double v) {
@@ -66,17 +102,6 @@ __device__ __forceinline__ double wave_sum_d(double v) {
   return v;
 }
 
-// Sum over the 16 lanes that share lane / 16 (one row group of an MFMA tile).
-__device__ __forceinline__ float group16_sum(float v) {
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-__device__ __forceinline__ float group16_max(float v) {
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
 
 // Block of 256 threads: fixed-order sum (wave sums, then the 4 wave totals in order).
 __device__ __forceinline__ float block_sum_256(float v, float* red) {

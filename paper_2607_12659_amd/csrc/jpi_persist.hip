@@ -86,8 +86,6 @@ typedef u32 u32x4 __attribute__((ext_vector_type(4)));
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 typedef __attribute__((address_space(3))) char lds_t;  // LDS byte pointer (direct-to-LDS loads)
 typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
-typedef __attribute__((address_space(3))) float lds_f32;
-typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
 
 // Buffer resource over [base, base + bytes): loads beyond the range return
 // zero and stores beyond it are dropped.
@@ -358,16 +356,19 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
 
 // ---- phase 1: attention chunk partials ----------------------------------------
 template <int DH>
-__device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* smem, lds_t* wt) {
+__device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* smem) {
+  // The workgroup stages the chunk's K and V^T in LDS with coalesced loads
+  // (one barrier); after that every wave works alone on its 16 query rows,
+  // with P and the partial output in registers.
   using MF = Mfma<bf16>;
-  constexpr int PAD = 8, LDK = DH + PAD, LDV = KC + PAD, LDP = KC + PAD;
-  constexpr int NST = DH / MF::KSUB, NJ = KC / 16;
+  constexpr int PAD = 8, LDK = DH + PAD, LDV = KC + PAD;
+  constexpr int NST = DH / MF::KSUB, NJ = KC / 16, NT = DH / 16;
   constexpr int KCH = KC * (DH / 8) / PT, VCH = DH * (KC / 8) / PT;
   static_assert(KCH >= 1 && VCH >= 1, "chunk too small for the workgroup");
-  static_assert((KC * LDK + DH * LDV + 64 * LDP) * 2 <= SMEM_BYTES, "attention LDS");
+  static_assert(KC == MF::KSUB, "one P.V step per chunk");
+  static_assert((KC * LDK + DH * LDV) * 2 <= SMEM_BYTES, "attention LDS");
   bf16* Ks = reinterpret_cast<bf16*>(smem);
   bf16* Vt = Ks + KC * LDK;
-  bf16* Ps = Vt + DH * LDV;  // [64][LDP]
   const int H = a.H, nH = a.nH, C = a.C;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int fr = lane & 15, fk = (lane >> 4) * MF::KPL;
@@ -419,7 +420,6 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
 #pragma unroll
     for (int st = 0; st < NST; ++st)
       qf[st] = w * 16 < H ? __builtin_bit_cast(MF::frag, ld16(rq, qoff + (u32)st * 1024u)) : MF::frag{};
-
 #pragma unroll
     for (int u = 0; u < KCH; ++u) {
       const int e = tid + u * PT, r = e / (DH / 8), cc = e - r * (DH / 8);
@@ -431,6 +431,11 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
       *reinterpret_cast<u32x4*>(&Vt[d * LDV + kc * 8]) = vr[u];
     }
     __syncthreads();
+    // S^T = K q^T with the operands swapped, so that a lane holds one query
+    // row (fr) and keys jj*16 + 4g + e (g = lane / 16): the softmax of a row
+    // needs only the four lanes that share fr, and P stays in registers as
+    // the B operand of O^T = V^T P^T.
+    const int g = lane >> 4;
     f32x4 sc[NJ];
 #pragma unroll
     for (int jj = 0; jj < NJ; ++jj) sc[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -438,74 +443,59 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
     for (int st = 0; st < NST; ++st)
 #pragma unroll
       for (int jj = 0; jj < NJ; ++jj)
-        sc[jj] = MF::run(qf[st], MF::load(&Ks[(jj * 16 + fr) * LDK + st * MF::KSUB + fk]), sc[jj]);
+        sc[jj] = MF::run(MF::load(&Ks[(jj * 16 + fr) * LDK + st * MF::KSUB + fk]), qf[st], sc[jj]);
     const float scale = 1.0f / sqrtf((float)DH);
-    float mrow[4], lrow[4];
+    float mx = -INFINITY;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      float mx = -INFINITY;
+    for (int jj = 0; jj < NJ; ++jj)
 #pragma unroll
-      for (int jj = 0; jj < NJ; ++jj) {
-        const int key = kbase + jj * 16 + fr;
+      for (int e = 0; e < 4; ++e) {
+        const int key = kbase + jj * 16 + 4 * g + e;
         const float v = key < nkeys ? sc[jj][e] * scale : -INFINITY;
         sc[jj][e] = v;
         mx = fmaxf(mx, v);
       }
-      mx = group16_max(mx);
-      float sum = 0.f;
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float sum = 0.f;
 #pragma unroll
-      for (int jj = 0; jj < NJ; ++jj) {
+    for (int jj = 0; jj < NJ; ++jj)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
         const float p = mx == -INFINITY ? 0.f : expf(sc[jj][e] - mx);
         sc[jj][e] = p;
         sum += p;
       }
-      mrow[e] = mx;
-      lrow[e] = group16_sum(sum);
-    }
-    const int prow = w * 16 + (lane >> 4) * 4;
-#pragma unroll
-    for (int jj = 0; jj < NJ; ++jj)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) Ps[(prow + e) * LDP + jj * 16 + fr] = static_cast<bf16>(sc[jj][e]);
-    __syncthreads();
-    f32x4 o[DH / 16];
-#pragma unroll
-    for (int nt = 0; nt < DH / 16; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int st = 0; st < KC / MF::KSUB; ++st) {
-      const MF::frag pa = MF::load(&Ps[(w * 16 + fr) * LDP + st * MF::KSUB + fk]);
-#pragma unroll
-      for (int nt = 0; nt < DH / 16; ++nt)
-        o[nt] = MF::run(pa, MF::load(&Vt[(nt * 16 + fr) * LDV + st * MF::KSUB + fk]), o[nt]);
-    }
-    // A lane holds dims nt*16 + fr of its four rows.  Each wave writes its 16
-    // rows to its quarter of the (idle) weight-tile buffer and reads them back
-    // row-major, so that every store instruction writes whole rows.
-    const size_t slot = ((size_t)b * nH + hn) * C + c;
-    static_assert(4 * 16 * DH * 4 <= WT_STEPS * 2 * 1024, "attention transpose buffer");
-    lds_f32* tb = reinterpret_cast<lds_f32*>(wt) + w * 16 * DH;
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-#pragma unroll
-      for (int nt = 0; nt < DH / 16; ++nt) tb[((lane >> 4) * 4 + e) * DH + nt * 16 + fr] = o[nt][e];
-    __syncthreads();
-    constexpr int RPI = 256 / DH;  // rows per wave store instruction
-#pragma unroll
-    for (int r0 = 0; r0 < 16; r0 += RPI) {
-      const int rr = r0 + (lane * 4) / DH, i = w * 16 + rr;
-      if (i < H) {
-        const f32x4 v = *reinterpret_cast<lds_f32x4*>(tb + rr * DH + (lane * 4) % DH);
-        st16(ro, (u32)(((slot * H + i) * DH + (lane * 4) % DH) * 4),
-             u32x4{f2u(v[0]), f2u(v[1]), f2u(v[2]), f2u(v[3])});
-      }
-    }
+    sum += __shfl_xor(sum, 16, 64);
+    sum += __shfl_xor(sum, 32, 64);
+    // contraction position 8g + j <-> key (j < 4 ? 4g + j : 16 + 4g + j - 4),
+    // the same order in P^T (registers) and in V^T (two 8-byte LDS reads)
+    static_assert(NJ == 2, "two 16-key halves per chunk");
+    MF::frag pb;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int i = prow + e;
-      if (i < H) {
-        if (fr == 0)
-          st8(rml, (u32)((slot * H + i) * 8), u32x2{f2u(mrow[e]), f2u(lrow[e])});
-      }
+      pb[e] = static_cast<bf16>(sc[0][e]);
+      pb[4 + e] = static_cast<bf16>(sc[1][e]);
+    }
+    f32x4 o[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const bf16* vrow = &Vt[(nt * 16 + fr) * LDV + 4 * g];
+      const u32x2 v0 = *reinterpret_cast<const u32x2*>(vrow);
+      const u32x2 v1 = *reinterpret_cast<const u32x2*>(vrow + 16);
+      const MF::frag va = __builtin_bit_cast(MF::frag, u32x4{v0[0], v0[1], v1[0], v1[1]});
+      o[nt] = MF::run(va, pb, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
+    // O^T: lane holds dims nt*16 + 4g .. +4 of query row fr: whole 16-byte
+    // pieces of a row-major partial row
+    const size_t slot = ((size_t)b * nH + hn) * C + c;
+    const int i = w * 16 + fr;
+    if (i < H) {
+      const u32 base = (u32)(((slot * H + i) * DH + 4 * g) * 4);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        st16(ro, base + (u32)nt * 64u, u32x4{f2u(o[nt][0]), f2u(o[nt][1]), f2u(o[nt][2]), f2u(o[nt][3])});
+      if (g == 0) st8(rml, (u32)((slot * H + i) * 8), u32x2{f2u(mx), f2u(sum)});
     }
     __syncthreads();  // LDS reused by the next item
   }
@@ -793,7 +783,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     const float* mm = tk + (size_t)(2 * l + 1) * 3 * W;  // MLP modulation
     if (p < 0) {
     } else if (p == 1) {
-      phase_attn<DH>(a, l, smem, wt);
+      phase_attn<DH>(a, l, smem);
     } else if (p == 2) {
       phase_combine(a, smem);
     } else if (p == 4 || p == 7) {
