@@ -168,40 +168,60 @@ __device__ __forceinline__ void load_wtile(lds_t* lds, const bf16* W, int KS, in
   }
 }
 
-// Grid barrier.  Each workgroup stores its arrival epoch into its own 128-byte
-// flag line; wave 0 of every workgroup then polls all lines (lane l reads the
-// lines of workgroups l, l+64, l+128, l+192 with independent loads).  If the
-// next phase is a GEMM, waves 1..3 meanwhile start the direct-to-LDS loads of
-// the workgroup's first weight tile so that their latency overlaps the wait;
-// the closing workgroup barrier does not wait for them (the GEMM does).
-__device__ __forceinline__ void grid_sync(const PersistArgs& a, u32 epoch, u32* s_abort, bool gemm_next,
-                                          const GemmJob& next, lds_t* wt) {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (gemm_next && (int)blockIdx.x < next.tiles * next.S) {
-    const int it = blockIdx.x, t = it % next.tiles, sl = it / next.tiles, nk_item = next.K / next.S / 32;
-    load_wtile(wt, next.w, next.K / 32, 2 * t, sl * nk_item, min(WT_STEPS, nk_item), 1);
+// Phase completion flags.  After phase ph a workgroup confirms its stores
+// (s_waitcnt vmcnt(0)) and writes ph + 2 into its own 128-byte flag line;
+// the values only grow within a launch.  A workgroup that has work in phase
+// ph first waits until the flags of the workgroups that produce its inputs
+// reach ph + 1 (they finished phase ph - 1).  Producer sets are one or two
+// ranges of workgroup indices; the row phases, which reduce the split-K slices
+// of every workgroup, wait for all of them.  Buffers are reused only after a
+// row phase that (through the producer chains) follows every reader of the
+// previous contents.
+struct Deps {
+  int lo0, hi0, lo1, hi1;  // workgroups [lo0, hi0) and [lo1, hi1)
+};
+__device__ __forceinline__ Deps deps_none() { return Deps{0, 0, 0, 0}; }
+__device__ __forceinline__ Deps deps_all() { return Deps{0, (int)gridDim.x, 0, 0}; }
+// workgroups that run items [i0, i1) of a phase whose item it runs on
+// workgroup it % grid
+__device__ __forceinline__ Deps deps_items(int i0, int i1) {
+  const int G = gridDim.x;
+  if (i1 - i0 >= G) return deps_all();
+  const int lo = i0 % G, hi = lo + (i1 - i0);
+  return hi <= G ? Deps{lo, hi, 0, 0} : Deps{lo, G, 0, hi - G};
+}
+
+// Wave 0 polls the producers' flags (lane l covers the l-th, l+64-th, ...
+// workgroup of the two ranges) until all reach `value`; waves 1..3 meanwhile
+// start the direct-to-LDS loads of the first weight tile of a GEMM phase.
+// Every wait is bounded: past SPIN_LIMIT polls the workgroup records an error
+// word and stops waiting, so the launch always terminates.
+__device__ __forceinline__ void wait_producers(const PersistArgs& a, const Deps& d, u32 value, u32* s_abort,
+                                               bool tile, const GemmJob& j, lds_t* wt) {
+  if (tile && (int)blockIdx.x < j.tiles * j.S) {
+    const int it = blockIdx.x, t = it % j.tiles, sl = it / j.tiles, nk_item = j.K / j.S / 32;
+    load_wtile(wt, j.w, j.K / 32, 2 * t, sl * nk_item, min(WT_STEPS, nk_item), 1);
   }
-  if (threadIdx.x < 64) {
+  const int n0 = d.hi0 - d.lo0, n = n0 + (d.hi1 - d.lo1);
+  if (threadIdx.x < 64 && n > 0 && *s_abort == 0u) {
     const rsrc_t rf = rsrc(a.flags);
-    if (threadIdx.x == 0) st4(rf, blockIdx.x * (FLAG_STRIDE * 4u), epoch);
-    if (*s_abort == 0u) {
-      const u32 g = gridDim.x;
-      for (u32 spins = 0;; ++spins) {
-        u32 f[4];
+    u32 off[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const u32 b = threadIdx.x + 64u * u;
-          f[u] = b < g ? poll4(rf, b * (FLAG_STRIDE * 4u)) : epoch;
+    for (int u = 0; u < 4; ++u) {
+      const int i = (int)threadIdx.x + 64 * u;
+      off[u] = (u32)(i < n0 ? d.lo0 + i : d.lo1 + (i - n0)) * (FLAG_STRIDE * 4u);
+    }
+    for (u32 spins = 0;; ++spins) {
+      u32 f[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) f[u] = (int)threadIdx.x + 64 * u < n ? poll4(rf, off[u]) : value;
+      if (__all(f[0] >= value && f[1] >= value && f[2] >= value && f[3] >= value)) break;
+      if (spins > SPIN_LIMIT) {
+        if (threadIdx.x == 0) {
+          *s_abort = 1u;
+          st4(rsrc(a.err), 0, 1u);
         }
-        if (__all(f[0] >= epoch && f[1] >= epoch && f[2] >= epoch && f[3] >= epoch)) break;
-        if (spins > SPIN_LIMIT) {
-          if (threadIdx.x == 0) {
-            *s_abort = 1u;
-            st4(rsrc(a.err), 0, 1u);
-          }
-          break;
-        }
+        break;
       }
     }
   }
@@ -210,11 +230,18 @@ __device__ __forceinline__ void grid_sync(const PersistArgs& a, u32 epoch, u32* 
   asm volatile("" ::: "memory");
 }
 
+// End of phase ph: every wave's stores are complete, then the flag.
+__device__ __forceinline__ void phase_done(const PersistArgs& a, u32 value) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) st4(rsrc(a.flags), blockIdx.x * (FLAG_STRIDE * 4u), value);
+}
+
 // ---------------------------------------------------------------------------
 // GEMM items: 32 output columns (two 16-row groups of W) x all 64 padded rows
 // x a K range of 32-wide k steps, split evenly over the waves.  The weight
 // part lives in the LDS tile (filled by direct-to-LDS loads: for a
-// workgroup's first item during the preceding grid barrier, otherwise here);
+// workgroup's first item while it waits for its producers, otherwise here);
 // A (fragment-ordered, read coherently) contributes its first `mgroups`
 // 16-row groups.  K ranges longer than the tile are processed in chunks.
 // ---------------------------------------------------------------------------
@@ -297,7 +324,7 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
     for (int q = 0; q < 4; ++q) acc[q][0] = acc[q][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int cs0 = 0; cs0 < nk_item; cs0 += WT_STEPS) {
       const int nk = min(WT_STEPS, nk_item - cs0);
-      if (it != (int)blockIdx.x || cs0 != 0) {  // not loaded during the barrier
+      if (it != (int)blockIdx.x || cs0 != 0) {  // not loaded during the wait
         __syncthreads();                         // every wave is done with the tile
         load_wtile(wt, j.w, KS, 2 * t, s * nk_item + cs0, nk, 0);
       }
@@ -747,6 +774,49 @@ __device__ __forceinline__ GemmJob make_job(const PersistArgs& a, int p, int l) 
   return GemmJob{a.z, lay + a.off_d, a.F, a.W / 32, a.s_d, EPI_SLICE};
 }
 
+// Producers of this workgroup's inputs in phase p of layer l (none if the
+// workgroup has no work in that phase).  Item layouts: GEMM item it = tile +
+// slice * tiles, attention item (rollout, head, chunk), combine item = a pair
+// of (rollout, head, query) rows; each runs on workgroup it % grid.
+__device__ __forceinline__ Deps phase_deps(const PersistArgs& a, int p, const GemmJob& j) {
+  const int G = gridDim.x, bid = blockIdx.x;
+  const int M = a.M, H = a.H, nH = a.nH, Dh = a.Dh, C = a.C;
+  if (p == 4 || p == 7) return bid < M ? deps_all() : deps_none();  // row phases: every slice producer
+  if (p == 0 || p == 5) return bid < j.tiles ? Deps{0, M, 0, 0} : deps_none();  // QKV, GateUp: the row owners
+  if (p == 1) {  // attention: the QKV tiles of this head, and of k and v if the chunk holds action keys
+    const int n_items = a.B * nH * C;
+    if (bid >= n_items) return deps_none();
+    if (n_items > G) return deps_all();
+    const int c = bid % C, hn = (bid / C) % nH, b = bid / (C * nH);
+    const int pl = a.prefix_len[b], kbase = c * KC;
+    if (kbase >= pl + H) return deps_none();
+    const int tq = Dh / 32;
+    if ((nH + 2) * tq > G) return deps_all();
+    const Deps q = deps_items(hn * tq, (hn + 1) * tq);
+    if (kbase + KC <= pl) return q;
+    const Deps kv = deps_items(nH * tq, (nH + 2) * tq);
+    return Deps{q.lo0, q.hi0, kv.lo0, kv.hi0};
+  }
+  if (p == 2) {  // combine: the attention chunks of the heads of its two rows
+    const int rows = a.B * nH * H, pairs = (rows + 1) / 2;
+    if (bid >= pairs) return deps_none();
+    if (pairs > G) return deps_all();
+    const int bh0 = (2 * bid) / H, bh1 = min(2 * bid + 1, rows - 1) / H;
+    return deps_items(bh0 * C, (bh1 + 1) * C);
+  }
+  const int n_items = j.tiles * j.S;
+  if (bid >= n_items) return deps_none();
+  if (n_items > G) return deps_all();
+  const int klen = j.K / j.S, s0 = (bid / j.tiles) * klen;
+  if (p == 3) {  // O-proj slice: the combine rows of the heads its K range covers, every rollout
+    const int hn0 = s0 / Dh, hn1 = (s0 + klen - 1) / Dh;
+    const int r0 = hn0 * H, r1 = ((a.B - 1) * nH + hn1) * H + H;  // rows [r0, r1) cover them
+    return deps_items(r0 / 2, (r1 + 1) / 2);
+  }
+  // Down slice: the GateUp tiles that wrote z columns [s0, s0 + klen) (16 per tile)
+  return deps_items(s0 / 16, (s0 + klen) / 16);
+}
+
 template <int DH>
 __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[SMEM_BYTES];
@@ -770,7 +840,6 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   }
   __syncthreads();
   lds_t* wt = (lds_t*)s_wt;
-  u32 epoch = 0;
   const int last_phase = a.n_steps * L * 8 - 1;
   // ph = -1 is the first step's in-projection; the later ones follow the final
   // row phase of the previous step in the same workgroup (no barrier between)
@@ -781,6 +850,10 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     const float* tk = a.table + (size_t)k * a.R;
     const float* am = tk + (size_t)(2 * l) * 3 * W;      // attention modulation: scale | shift | gate
     const float* mm = tk + (size_t)(2 * l + 1) * 3 * W;  // MLP modulation
+    const bool gemm = p == 0 || p == 3 || p == 5 || p == 6;
+    const GemmJob job = make_job(a, gemm ? p : 0, l);
+    if (ph >= 0)  // producers of this phase's inputs finished phase ph - 1
+      wait_producers(a, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, gemm, job, wt);
     if (p < 0) {
     } else if (p == 1) {
       phase_attn<DH>(a, l, smem);
@@ -810,18 +883,13 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
       phase_rows(a, r, xreg, s_hrow, s_bin, s_x, smem);
       if (r.final_step && k + 1 < a.n_steps) ki = k + 1;  // same workgroup, no barrier needed
     } else {
-      phase_gemm(a, make_job(a, p, l), l, wt, smem);
+      phase_gemm(a, job, l, wt, smem);
     }
     if (ki >= 0 && owner) {
       const float* ti = a.table + (size_t)ki * a.R;
       inproj_row(a, ti, ti + W, s_hrow, s_bin, s_x, reinterpret_cast<float*>(smem));
     }
-    if (ph < last_phase) {
-      const int pn = (ph + 1) % 8, ln = ((ph + 1) / 8) % L;  // the next phase
-      const bool gemm_next = pn == 0 || pn == 3 || pn == 5 || pn == 6;
-      const GemmJob nj = make_job(a, pn, ln);
-      grid_sync(a, ++epoch, &s_abort, gemm_next, nj, wt);
-    }
+    if (ph < last_phase) phase_done(a, (u32)(ph + 2));
   }
   if (owner && t < A) a.x[(size_t)m * A + t] = xreg;
 }
