@@ -383,7 +383,8 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
 
 // ---- phase 1: attention chunk partials ----------------------------------------
 template <int DH>
-__device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* smem) {
+__device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* smem, const Deps& deps, u32 value,
+                                           u32* s_abort, lds_t* wt) {
   // The workgroup stages the chunk's K and V^T in LDS with coalesced loads
   // (one barrier); after that every wave works alone on its 16 query rows,
   // with P and the partial output in registers.
@@ -403,6 +404,7 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
   const bf16* kpl = reinterpret_cast<const bf16*>(a.kp) + (size_t)l * a.kp_lstride;
   const bf16* vpl = reinterpret_cast<const bf16*>(a.vpt) + (size_t)l * a.vpt_lstride;
   const rsrc_t rv = rsrc(vpl), rks = rsrc(a.ks), rq = rsrc(a.q), ro = rsrc(a.opart), rml = rsrc(a.ml);
+  bool waited = false;
   for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
     const int c = it % C, hn = (it / C) % nH, b = it / (C * nH);
     const int pl = a.prefix_len[b];
@@ -412,33 +414,46 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
     const bf16* kp = kpl + (size_t)b * a.kp_bstride;
     const bf16* vb = vpl + (size_t)b * a.vpt_bstride;
     const u32 vboff = (u32)((size_t)b * a.vpt_bstride * 2);
+    // The prefix keys and values were bound before the launch (plain loads):
+    // they are loaded before waiting for this layer's QKV tiles.  The action
+    // keys and values and q come from those tiles (coherent loads, after the
+    // wait); keys past the end are zeroed so that stale memory never meets a
+    // zero probability.
     u32x4 kr[KCH], vr[VCH];
 #pragma unroll
     for (int u = 0; u < KCH; ++u) {
       const int e = tid + u * PT, r = e / (DH / 8), cc = e - r * (DH / 8);
       const int key = kbase + r;
-      if (key < pl) kr[u] = *reinterpret_cast<const u32x4*>(kp + (size_t)key * DH + cc * 8);
-      else if (key < nkeys) kr[u] = ld16(rks, (u32)((((size_t)b * H + (key - pl)) * DH + cc * 8) * 2));
-      else kr[u] = u32x4{0u, 0u, 0u, 0u};
+      kr[u] = key < pl ? *reinterpret_cast<const u32x4*>(kp + (size_t)key * DH + cc * 8) : u32x4{0u, 0u, 0u, 0u};
     }
-    // V^T rows: keys < prefix_len were bound before the launch (plain loads);
-    // the action keys were written by this launch (coherent loads); keys past
-    // the end are zeroed so that stale memory never meets a zero probability.
 #pragma unroll
     for (int u = 0; u < VCH; ++u) {
       const int e = tid + u * PT, d = e / (KC / 8), kc = e - d * (KC / 8);
       const int key0 = kbase + kc * 8;
-      if (key0 + 8 <= pl) {
-        vr[u] = *reinterpret_cast<const u32x4*>(vb + (size_t)d * a.vpt_dstride + key0);
-      } else if (key0 < nkeys) {
+      vr[u] = key0 + 8 <= pl ? *reinterpret_cast<const u32x4*>(vb + (size_t)d * a.vpt_dstride + key0)
+                             : u32x4{0u, 0u, 0u, 0u};
+    }
+    if (!waited) {  // (the producers of every item of this workgroup)
+      wait_producers(a, deps, value, s_abort, false, GemmJob{}, wt);
+      waited = true;
+    }
+#pragma unroll
+    for (int u = 0; u < KCH; ++u) {
+      const int e = tid + u * PT, r = e / (DH / 8), cc = e - r * (DH / 8);
+      const int key = kbase + r;
+      if (key >= pl && key < nkeys) kr[u] = ld16(rks, (u32)((((size_t)b * H + (key - pl)) * DH + cc * 8) * 2));
+    }
+#pragma unroll
+    for (int u = 0; u < VCH; ++u) {
+      const int e = tid + u * PT, d = e / (KC / 8), kc = e - d * (KC / 8);
+      const int key0 = kbase + kc * 8;
+      if (key0 + 8 > pl && key0 < nkeys) {
         u32x4 v = ld16(rv, vboff + (u32)(((size_t)d * a.vpt_dstride + key0) * 2));
         const int n_ok = nkeys - key0;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           v[q] &= (2 * q < n_ok ? 0x0000ffffu : 0u) | (2 * q + 1 < n_ok ? 0xffff0000u : 0u);
         vr[u] = v;
-      } else {
-        vr[u] = u32x4{0u, 0u, 0u, 0u};
       }
     }
     // wave w: query rows w*16 .. +16 of head hn (fragment-ordered; rows >= H are zero)
@@ -852,11 +867,12 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     const float* mm = tk + (size_t)(2 * l + 1) * 3 * W;  // MLP modulation
     const bool gemm = p == 0 || p == 3 || p == 5 || p == 6;
     const GemmJob job = make_job(a, gemm ? p : 0, l);
-    if (ph >= 0)  // producers of this phase's inputs finished phase ph - 1
-      wait_producers(a, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, gemm, job, wt);
+    // producers of this phase's inputs finished phase ph - 1 (attention waits
+    // inside, after loading the prefix part of its chunk)
+    if (ph >= 0 && p != 1) wait_producers(a, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, gemm, job, wt);
     if (p < 0) {
     } else if (p == 1) {
-      phase_attn<DH>(a, l, smem);
+      phase_attn<DH>(a, l, smem, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, wt);
     } else if (p == 2) {
       phase_combine(a, smem);
     } else if (p == 4 || p == 7) {
