@@ -44,10 +44,10 @@ METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roof
 # sha256 of the kernel source they were measured on; the byte counts are the
 # counter readings times the copy calibration factor.
 MEASURED_TRAFFIC = {
-    # pi0.5 shape, batch 1: FETCH_SIZE 5814361.3 KiB x 1.99980 (a 256 MiB copy
-    # reads back 131085.25 KiB) + WRITE_SIZE 3015096.3 KiB x 1.0 (the copy's
+    # pi0.5 shape, batch 1: FETCH_SIZE 5790465.9 KiB x 1.99980 (a 256 MiB copy
+    # reads back 131085.33 KiB) + WRITE_SIZE 3015096.2 KiB x 1.00000 (the copy's
     # 262144 KiB), mean over 29 dispatches
-    ("1e69478f021c7cdd502358d6e37a33a7c639cdfc514791dc337aae97f97be962", "pi05-b1"): 14994066926,
+    ("9619b67bf4ee72ea19371d6c1693f2dc4d5660517b3b41e01add07ccfda05cde", "pi05-b1"): 14945126545,
 }
 
 
