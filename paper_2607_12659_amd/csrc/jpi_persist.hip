@@ -211,11 +211,19 @@ __device__ __forceinline__ void wait_producers(const PersistArgs& a, const Deps&
       const int i = (int)threadIdx.x + 64 * u;
       off[u] = (u32)(i < n0 ? d.lo0 + i : d.lo1 + (i - n0)) * (FLAG_STRIDE * 4u);
     }
+    // flags only grow: a flag seen at `value` is not polled again, so the
+    // poll traffic shrinks to the producers that are still working
+    u32 pend = 0u;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) pend |= ((int)threadIdx.x + 64 * u < n ? 1u : 0u) << u;
     for (u32 spins = 0;; ++spins) {
       u32 f[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) f[u] = (int)threadIdx.x + 64 * u < n ? poll4(rf, off[u]) : value;
-      if (__all(f[0] >= value && f[1] >= value && f[2] >= value && f[3] >= value)) break;
+      for (int u = 0; u < 4; ++u) f[u] = (pend >> u) & 1u ? poll4(rf, off[u]) : value;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (f[u] >= value) pend &= ~(1u << u);
+      if (__all(pend == 0u)) break;
       if (spins > SPIN_LIMIT) {
         if (threadIdx.x == 0) {
           *s_abort = 1u;
