@@ -16,6 +16,8 @@ in HBM.  Prints one JSON line:
              FETCH_SIZE / WRITE_SIZE counters (scaled by a plain copy of known
              size, see --calibrate-copy) when the counters were taken on the
              current kernel source, else null
+  measured_peaks  second denominators from the same run: a plain device copy
+             (read + write GB/s) and a large bf16 GEMM (TFLOP/s) on this GPU
   cpu_baseline  the fp64 CPU oracle timed on the host cores, repeating the
                 denoise of rollout 0 for at least 10 s (a bounded sample)
 
@@ -67,6 +69,36 @@ def calibrate_copy(mib):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}), flush=True)
+
+
+def measured_peaks():
+    """Second denominators measured on this GPU in the same run: a plain device
+    copy of 1 GiB (read + write bytes per second) and a large plain bf16 GEMM
+    (8192^3, contiguous operands)."""
+    import torch
+    x = torch.ones(1 << 29, dtype=torch.bfloat16, device="cuda")
+    y = torch.empty_like(x)
+    a = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
+    b = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    t_copy = timed(lambda: y.copy_(x), 5)
+    t_gemm = timed(lambda: torch.matmul(a, b), 5)
+    del x, y, a, b
+    torch.cuda.empty_cache()
+    return {"copy_GBs": round(2.0 * (1 << 30) / t_copy / 1e9, 1),
+            "bf16_gemm_TFLOPs": round(2.0 * 8192 ** 3 / t_gemm / 1e12, 1),
+            "method": "torch copy of 1 GiB (read + write bytes); torch.matmul 8192^3 bf16"}
 
 
 def algorithmic_counts(wl):
@@ -271,6 +303,10 @@ def main():
                           "mfma_frac": round(call_tflops / mfma_peak, 4)},
     }
     ae.close()
+    mp = measured_peaks()
+    mp["hbm_frac_of_measured_copy"] = round(result["roofline"]["achieved"] / mp["copy_GBs"], 4) \
+        if result["roofline"]["unit"] == "GB/s" else None
+    result["measured_peaks"] = mp
     if not args.no_cpu:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(wl, weights, K, V, noise)

@@ -122,8 +122,8 @@ struct PersistArgs {
   void* q;                  // fragment-ordered [B][nH][64][Dh]
   void* ks;                 // [B][H][Dh]
   void* vst;                // [B][Dh][H]
-  float* opart;             // [B][nH][C][H][Dh]
-  float* ml;                // [B][nH][C][H][2]
+  float* opart;             // [B][nH][C][H][Dh] bf16: each chunk's output row / its probability sum
+  float* ml;                // [B][nH][C][H][2] (chunk max, probability sum)
   void* o;                  // fragment-ordered [64][nH*Dh]
   float* part;              // [max(s_o, s_d)][M][W]
   void* z;                  // fragment-ordered [64][F]

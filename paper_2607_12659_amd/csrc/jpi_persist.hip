@@ -100,6 +100,9 @@ __device__ __forceinline__ u32x4 ld16(rsrc_t r, u32 off) {
 // element 0 whatever the index.
 __device__ __forceinline__ u32 f2u(float v) { return __builtin_bit_cast(u32, v); }
 __device__ __forceinline__ float u2f(u32 v) { return __builtin_bit_cast(float, v); }
+__device__ __forceinline__ u32x2 ld8(rsrc_t r, u32 off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, CPOL_DEV);
+}
 __device__ __forceinline__ float2 ld8f(rsrc_t r, u32 off) {
   return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, CPOL_DEV));
 }
@@ -541,10 +544,12 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
     const size_t slot = ((size_t)b * nH + hn) * C + c;
     const int i = w * 16 + fr;
     if (i < H) {
-      const u32 base = (u32)(((slot * H + i) * DH + 4 * g) * 4);
+      // the chunk's output divided by its probability sum, in bf16 (the
+      // combine weights it by the sum again, in fp32)
+      const u32 base = (u32)(((slot * H + i) * DH + 4 * g) * 2);
+      const float rl = sum > 0.f ? 1.0f / sum : 0.f;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-        st16(ro, base + (u32)nt * 64u, u32x4{f2u(o[nt][0]), f2u(o[nt][1]), f2u(o[nt][2]), f2u(o[nt][3])});
+      for (int nt = 0; nt < NT; ++nt) st8(ro, base + (u32)nt * 32u, pack4_bf16(o[nt] * rl));
       if (g == 0) st8(rml, (u32)((slot * H + i) * 8), u32x2{f2u(mx), f2u(sum)});
     }
     __syncthreads();  // LDS reused by the next item
@@ -578,13 +583,13 @@ __device__ __forceinline__ void phase_combine(const PersistArgs& a, char* smem) 
     float m = -INFINITY, lsum = 0.f;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int c0 = g; c0 < nch; c0 += G * CPT) {
-      u32x4 ov[CPT];
+      u32x2 ov[CPT];
       float2 mv[CPT];  // (chunk max, chunk sum)
 #pragma unroll
       for (int u = 0; u < CPT; ++u) {
         const int c = c0 + G * u;
         const bool ok = c < nch;
-        ov[u] = ok ? ld16(ro, (u32)((((slot0 + c) * H + i) * Dh + q4 * 4) * 4)) : u32x4{0u, 0u, 0u, 0u};
+        ov[u] = ok ? ld8(ro, (u32)((((slot0 + c) * H + i) * Dh + q4 * 4) * 2)) : u32x2{0u, 0u};
         mv[u] = ok ? ld8f(rml, (u32)(((slot0 + c) * H + i) * 8)) : float2{-INFINITY, 0.f};
       }
       float mp = m;
@@ -596,8 +601,9 @@ __device__ __forceinline__ void phase_combine(const PersistArgs& a, char* smem) 
 #pragma unroll
       for (int u = 0; u < CPT; ++u) {
         const float wc = mv[u].x == -INFINITY ? 0.f : expf(mv[u].x - mp);
-        acc += wc * as_f4(ov[u]);
-        lsum += wc * mv[u].y;
+        const float wl = wc * mv[u].y;  // the chunk's row is normalised by its sum
+        acc += wl * f32x4{bf16_lo(ov[u][0]), bf16_hi(ov[u][0]), bf16_lo(ov[u][1]), bf16_hi(ov[u][1])};
+        lsum += wl;
       }
       m = mp;
     }
