@@ -75,7 +75,7 @@ constexpr int FLAG_WORDS = MAX_GRID * FLAG_STRIDE;
 constexpr int CPT = 16;    // combine: chunks per thread per round trip
 constexpr int OUT_G = 16;  // action-out projection: 16-byte weight granules per thread
 #ifndef A_BATCH
-#define A_BATCH 8  // k steps of activation fragments per wave in flight
+#define A_BATCH 4  // k steps of activation fragments per wave in flight (measured best)
 #endif
 
 enum : int { EPI_QKV = 0, EPI_GEGLU = 1, EPI_SLICE = 2 };
