@@ -46,10 +46,10 @@ METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roof
 # sha256 of the kernel source they were measured on; the byte counts are the
 # counter readings times the copy calibration factor.
 MEASURED_TRAFFIC = {
-    # pi0.5 shape, batch 1: FETCH_SIZE 5790465.9 KiB x 1.99980 (a 256 MiB copy
-    # reads back 131085.33 KiB) + WRITE_SIZE 3015096.2 KiB x 1.00000 (the copy's
+    # pi0.5 shape, batch 1: FETCH_SIZE 5274264.5 KiB x 1.99980 (a 256 MiB copy
+    # reads back 131085.17 KiB) + WRITE_SIZE 2007096.2 KiB x 1.00000 (the copy's
     # 262144 KiB), mean over 29 dispatches
-    ("9619b67bf4ee72ea19371d6c1693f2dc4d5660517b3b41e01add07ccfda05cde", "pi05-b1"): 14945126545,
+    ("a739f8a5171d283ab080a5fe625f5070a42dd3a0825a7eb849b95d6650b9a7c2", "pi05-b1"): 12855875392,
 }
 
 

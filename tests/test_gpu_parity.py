@@ -282,3 +282,51 @@ def test_persistent_matches_multikernel_pi05(pi05):
     assert rel_l2_per_rollout(a, b) <= 5e-3
     # graph replay determinism of the single-launch kernel
     assert np.array_equal(a, _run_env(ae, None, K, V, noise, 2))
+
+
+def test_persistent_repeated_calls_bitwise(pi05):
+    """The single-launch kernel orders its phases with per-workgroup completion
+    flags (each consumer waits only for its producers).  A missing dependency
+    would show as run-to-run variation, so repeated calls on two alternating
+    inputs must reproduce their first results bit for bit."""
+    from paper_2607_12659_amd.expert import to_device
+    torch = torch_cuda()
+    w, ae = pi05
+    wl = synth.WORKLOADS["pi05-b1"]
+    K, V = synth.make_prefix(wl)
+    n1 = synth.make_noise(wl)
+    n2 = np.ascontiguousarray(-n1[:, ::-1])
+    ref1 = run(ae, K, V, n1, wl.n_steps)
+    ref2 = run(ae, K, V, n2, wl.n_steps)
+    assert not np.array_equal(ref1, ref2)
+    d1 = to_device(np.ascontiguousarray(n1, np.float32))
+    d2 = to_device(np.ascontiguousarray(n2, np.float32))
+    print("case pi05-b1 x 24 alternating calls", flush=True)
+    for i in range(12):
+        for d, ref in ((d1, ref1), (d2, ref2)):
+            out = ae.denoise(d, wl.n_steps)
+            ae.sync()
+            torch.cuda.synchronize()
+            assert np.array_equal(out.cpu().numpy().astype(np.float64), ref), "call %d differs" % i
+
+
+def test_persistent_tiny_bf16_repeated_calls_bitwise():
+    """Ragged batch of three with committed rows: many short calls in a row."""
+    torch = torch_cuda()
+    wl = synth.WORKLOADS["tiny-fp32"].with_(dtype="bf16", batch=3, n_fixed=2, prefix_len=(64, 5, 41),
+                                            name="tiny-bf16-b3")
+    inp = Inputs(wl)
+    ae = make_expert(wl, inp.weights)
+    try:
+        ref = run(ae, inp.K, inp.V, inp.noise, wl.n_steps, prefix_len=inp.prefix_len,
+                  committed=inp.committed, n_fixed=2)
+        from paper_2607_12659_amd.expert import to_device
+        d = to_device(np.ascontiguousarray(inp.noise, np.float32))
+        print("case tiny-bf16-b3 x 40 calls", flush=True)
+        for i in range(40):
+            out = ae.denoise(d, wl.n_steps)
+            ae.sync()
+            torch.cuda.synchronize()
+            assert np.array_equal(out.cpu().numpy().astype(np.float64), ref), "call %d differs" % i
+    finally:
+        ae.close()
