@@ -164,8 +164,8 @@ jpi_status jpi_bind_state(jpi_ctx* ctx, const float* committed_dev, int n_fixed,
 jpi_status jpi_denoise(jpi_ctx* ctx, const float* noise_dev, int n_steps, float* actions_dev, void* stream);
 
 /* Synchronise `stream` and report asynchronous HIP errors as JPI_ERR_HIP,
- * including a barrier wait of the single-launch denoise kernel that timed
- * out (its output is then invalid). */
+ * including a wait of the single-launch denoise kernel for its producer
+ * workgroups that timed out (its output is then invalid). */
 jpi_status jpi_sync(jpi_ctx* ctx, void* stream);
 
 /* ---- kernel-level entry points used by the parity tests ------------------ */

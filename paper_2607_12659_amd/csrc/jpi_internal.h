@@ -127,16 +127,16 @@ struct PersistArgs {
   void* o;                  // fragment-ordered [64][nH*Dh]
   float* part;              // [max(s_o, s_d)][M][W]
   void* z;                  // fragment-ordered [64][F]
-  unsigned* flags;          // [grid][32] barrier arrival epochs
-  unsigned* err;            // set to 1 if a barrier wait timed out
+  unsigned* flags;          // [grid][32] completion flags: the last phase index + 2 each workgroup finished
+  unsigned* err;            // set to 1 if a wait for producers timed out
   hipEvent_t ev_start, ev_stop;
 };
 bool persist_supported(jpi_dtype dt, int M, int W, int nH, int Dh, int F, int H, int A, int Pmax);
 int persist_chunks(int P, int H);
 int persist_pick_split(int tiles, int K, int grid);
 int persist_block_threads();
-int persist_max_grid();    // largest grid the barrier supports
-int persist_flag_words();  // size of the barrier flag buffer in 32-bit words
+int persist_max_grid();    // largest grid the completion flags support
+int persist_flag_words();  // size of the completion flag buffer in 32-bit words
 // dst = fragment-ordered copy of the row-major bf16 matrix src [R][K]
 hipError_t launch_frag_order(const void* src, void* dst, int R, int K, hipStream_t s);
 hipError_t persist_occupancy(int Dh, int* blocks_per_cu);

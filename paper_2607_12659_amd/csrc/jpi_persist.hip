@@ -2,15 +2,18 @@
 // bf16 weights).  One workgroup per compute unit runs every Euler step of the
 // flow-matching loop and every layer of the action expert (paper: Appendix
 // "Model Architecture of pi series Models" for the expert, Section "System
-// Design" for running all denoising steps as one unrolled unit); phases are
-// separated by a grid-wide barrier.
+// Design" for running all denoising steps as one unrolled unit).  Phases are
+// ordered by per-workgroup completion flags: before a phase in which it has
+// work, a workgroup waits only for the workgroups that produce that work's
+// inputs (see phase_deps), so the per-head and per-slice chains of a layer
+// overlap.
 //
 // Phases of one layer (items are distributed over the workgroups):
 //   0 QKV     adaRMSNorm'd activations y x packed [q|k|v] weights, RoPE
 //             epilogue; the action rows' V goes into the transposed prefix V
 //             buffer right after each rollout's valid prefix
 //   1 ATTN    (rollout, head, 32-key chunk) items over prefix + action keys:
-//             per-chunk max / sum / unnormalised output
+//             per-chunk max, probability sum and output row / sum (bf16)
 //   2 COMB    chunk combine per (rollout, head, query row) -> o
 //   3 OPROJ   o x W_o, split-K slices -> part
 //   4 ROWS    row owner: residual += gate * sum of slices; MLP adaRMSNorm -> y
@@ -34,20 +37,20 @@
 // halves the load throughput of a compute unit.  Activation matrices are
 // padded to 64 rows; rows >= M are never written and stay zero.
 //
-// Row ownership: workgroup m < M owns action row m.  Its residual row, the
-// in-projection weights (transposed) and b_in live in LDS for the whole
-// launch and x[m][a] lives in a register of thread a.
+// Row ownership: workgroup m < M owns action row m.  Its residual row and
+// b_in live in LDS for the whole launch and x[m][a] lives in a register of
+// thread a.
 //
 // Memory model: data that one workgroup writes and another reads within the
 // launch (activations, slices, attention partials, the action rows' K and V,
-// barrier flags) is stored and loaded with device-scope coherent buffer
-// accesses (cache policy sc1); a barrier arrival is stored only after
+// completion flags) is stored and loaded with device-scope coherent buffer
+// accesses (cache policy sc1); a completion flag is stored only after
 // s_waitcnt vmcnt(0) confirms the workgroup's stores.  No agent-scope fences
 // are used (on gfx950 they serialise across the chip).  Weights, the prefix K,
 // the prefix part of the transposed V, the modulation table and the RoPE
 // table are read-only during the launch and use plain loads.
 //
-// Every barrier wait is bounded: after SPIN_LIMIT polls the workgroup records
+// Every wait is bounded: after SPIN_LIMIT polls the workgroup records
 // an error word and stops waiting, so a launch always terminates; the host
 // reports the error from jpi_sync.
 #include <algorithm>
@@ -69,8 +72,8 @@ constexpr int SMEM_BYTES = 42496;      // per-phase scratch (attention staging a
 constexpr int MAX_W = 2048;            // model width held in LDS by a row owner
 constexpr int WT_STEPS = 32;           // weight tile in LDS: 32-wide k steps of a 32-row tile (64 KB)
 constexpr int RMAX_S = 16;             // split-K slices summed by the row phases
-constexpr int MAX_GRID = 256;          // barrier flags are polled as 64 lanes x 4 lines
-constexpr int FLAG_STRIDE = 32;        // words between barrier flags: one 128-byte line per workgroup
+constexpr int MAX_GRID = 256;          // completion flags are polled as 64 lanes x 4 lines
+constexpr int FLAG_STRIDE = 32;        // words between completion flags: one 128-byte line per workgroup
 constexpr int FLAG_WORDS = MAX_GRID * FLAG_STRIDE;
 constexpr int CPT = 16;    // combine: chunks per thread per round trip
 constexpr int OUT_G = 16;  // action-out projection: 16-byte weight granules per thread
@@ -397,7 +400,7 @@ template <int DH>
 __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* smem, const Deps& deps, u32 value,
                                            u32* s_abort, lds_t* wt) {
   // The workgroup stages the chunk's K and V^T in LDS with coalesced loads
-  // (one barrier); after that every wave works alone on its 16 query rows,
+  // (one workgroup barrier); after that every wave works alone on its 16 query rows,
   // with P and the partial output in registers.
   using MF = Mfma<bf16>;
   constexpr int PAD = 8, LDK = DH + PAD, LDV = KC + PAD;
@@ -871,7 +874,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   lds_t* wt = (lds_t*)s_wt;
   const int last_phase = a.n_steps * L * 8 - 1;
   // ph = -1 is the first step's in-projection; the later ones follow the final
-  // row phase of the previous step in the same workgroup (no barrier between)
+  // row phase of the previous step in the same workgroup (no wait between)
   for (int ph = -1; ph <= last_phase; ++ph) {
     // in-projection + first norm of step ki (one call site for every step)
     int ki = ph < 0 ? 0 : -1;
@@ -911,7 +914,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
         }
       }
       phase_rows(a, r, xreg, s_hrow, s_bin, s_x, smem);
-      if (r.final_step && k + 1 < a.n_steps) ki = k + 1;  // same workgroup, no barrier needed
+      if (r.final_step && k + 1 < a.n_steps) ki = k + 1;  // same workgroup, no wait needed
     } else {
       phase_gemm(a, job, l, wt, smem);
     }

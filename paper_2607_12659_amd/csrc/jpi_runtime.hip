@@ -106,8 +106,8 @@ struct jpi_ctx {
   std::map<GraphKey, hipGraphExec_t> graphs;
   hipStream_t cap_stream = nullptr;
   // single-launch (persistent) path
-  unsigned* pflags = nullptr;  // barrier arrival lines (one per workgroup) + release line
-  unsigned* perr = nullptr;    // barrier timeout word
+  unsigned* pflags = nullptr;  // completion flag lines of the single-launch kernel (one per workgroup)
+  unsigned* perr = nullptr;    // set when a wait for producers timed out
   int persist_occ = -1;        // workgroups per CU the persistent kernel fits (-1: not queried)
   void* w_frag = nullptr;      // layer weights with every matrix fragment-ordered
   bool frag_ready = false;     // w_frag matches w_layers
@@ -988,7 +988,7 @@ jpi_status jpi_sync(jpi_ctx* c, void* stream) {
   HIPCHK(c, hipMemcpy(&perr, c->perr, sizeof(perr), hipMemcpyDeviceToHost));
   if (perr != 0) {
     HIPCHK(c, hipMemset(c->perr, 0, sizeof(perr)));
-    return fail(c, JPI_ERR_HIP, "single-launch denoise: a grid barrier wait timed out; the output is invalid");
+    return fail(c, JPI_ERR_HIP, "single-launch denoise: a wait for producer workgroups timed out; the output is invalid");
   }
   return JPI_OK;
 }
