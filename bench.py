@@ -49,14 +49,21 @@ MEASURED_TRAFFIC = {
     # pi0.5 shape, batch 1: FETCH_SIZE 5274264.5 KiB x 1.99980 (a 256 MiB copy
     # reads back 131085.17 KiB) + WRITE_SIZE 2007096.2 KiB x 1.00000 (the copy's
     # 262144 KiB), mean over 29 dispatches
-    ("a739f8a5171d283ab080a5fe625f5070a42dd3a0825a7eb849b95d6650b9a7c2", "pi05-b1"): 12855875392,
+    ("f40321efb8dc85dc30d3e2cd99221187d67baeddc6568681346d6a2593fd6a48", "pi05-b1"): 12855875392,
 }
 
 
 def kernel_source_hash():
+    """sha256 of the single-launch kernel's code: the source with its comments
+    and whitespace removed, so that the recorded traffic stays attached to the
+    code it was measured on and nothing else."""
     import hashlib
-    with open(os.path.join(ROOT, "paper_2607_12659_amd", "csrc", "jpi_persist.hip"), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    import re
+    with open(os.path.join(ROOT, "paper_2607_12659_amd", "csrc", "jpi_persist.hip")) as f:
+        src = f.read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    return hashlib.sha256("".join(src.split()).encode()).hexdigest()
 
 
 def calibrate_copy(mib):
