@@ -25,7 +25,8 @@ struct EpiParams {
   // EPI_QKV: packed columns [q heads | k | v]; RoPE on q and k
   void* q;               // [B][nH][H][Dh]
   void* ks;              // [B][H][Dh]
-  void* vst;             // [B][Dh][H] (v stored transposed)
+  void* vst;             // [B][Dh][vst_ld] (v stored transposed)
+  int vst_ld;            // row stride of vst in elements (>= horizon)
   const float2* rope;    // [B][H][Dh/2] (cos, sin) at position prefix_len[b] + i
   int n_heads, head_dim, horizon;
   // EPI_GEGLU: packed columns in 32-wide groups [gate 16 | up 16]
@@ -76,7 +77,8 @@ hipError_t launch_resid_norm(jpi_dtype dt, const RowLaunch& r, bool final_step, 
 struct AttnLaunch {
   const void* q;          // [B][nH][H][Dh]
   const void* ks;         // [B][H][Dh]
-  const void* vst;        // [B][Dh][H]   suffix V, transposed
+  const void* vst;        // [B][Dh][vst_ld]   suffix V, transposed
+  int64_t vst_ld;         // row stride of vst in elements: >= H, a multiple of 8 on the bf16 path
   const void* kp;         // prefix K: rollout b at kp + b*kp_bstride, key j at + j*Dh
   const void* vpt;        // prefix V transposed: rollout b at vpt + b*vpt_bstride, dim d at + d*vpt_dstride
   int64_t kp_bstride, vpt_bstride, vpt_dstride;  // elements; vpt_dstride a multiple of 8
@@ -87,6 +89,7 @@ struct AttnLaunch {
   float* lpart;           // [B][nH][n_chunks][H]
   void* out;              // [B*H][nH*Dh] of dtype, or fp32 if out_f32
   int out_f32;
+  int n_cu;               // compute units of the device (sizes the bf16 key ranges)
   hipEvent_t ev_start, ev_stop;  // optional: start of the chunk pass, end of the combine
 };
 int attn_chunk(jpi_dtype dt);
@@ -96,6 +99,11 @@ int attn_max_prefix(jpi_dtype dt, int H);
 hipError_t launch_transpose(jpi_dtype dt, const void* src, void* dst, int rows, int cols, int64_t sld, int64_t dld,
                             int64_t sz, int64_t dz, int nmat, hipStream_t s);
 hipError_t launch_attention(jpi_dtype dt, const AttnLaunch& a, hipStream_t s);
+// bf16 attention (jpi_flash.hip): S key ranges per 128-row query tile; with
+// S > 1 the partials live in a.opart (flash_scratch_bytes(...) bytes)
+int flash_splits(int B, int nH, int H, int P, int n_cu);
+size_t flash_scratch_bytes(int B, int nH, int H, int Dh, int S);
+hipError_t launch_flash(const AttnLaunch& a, int S, hipStream_t s);
 
 // Persistent single-launch denoise (jpi_persist.hip), M <= 64, bf16.
 struct PersistArgs {

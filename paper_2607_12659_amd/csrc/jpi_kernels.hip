@@ -56,9 +56,9 @@ __device__ __forceinline__ void epilogue_pair(const EpiParams& ep, float* out_f3
       dst[d + half] = from_f32<T>(r_hi);
     } else {
       const int within = col_lo - qcols - Dh;  // v: natural order, stored transposed [b][d][i]
-      T* dst = reinterpret_cast<T*>(ep.vst) + (size_t)b * Dh * H + i;
-      dst[(size_t)within * H] = from_f32<T>(lo);
-      dst[(size_t)(within + 16) * H] = from_f32<T>(hi);
+      T* dst = reinterpret_cast<T*>(ep.vst) + (size_t)b * Dh * ep.vst_ld + i;
+      dst[(size_t)within * ep.vst_ld] = from_f32<T>(lo);
+      dst[(size_t)(within + 16) * ep.vst_ld] = from_f32<T>(hi);
     }
   }
 }
@@ -539,7 +539,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnLaunch a) {
   const T* kp = reinterpret_cast<const T*>(a.kp) + (size_t)b * a.kp_bstride;
   const T* vpt = reinterpret_cast<const T*>(a.vpt) + (size_t)b * a.vpt_bstride;
   const T* ksb = reinterpret_cast<const T*>(a.ks) + (size_t)b * H * DH;
-  const T* vstb = reinterpret_cast<const T*>(a.vst) + (size_t)b * DH * H;
+  const T* vstb = reinterpret_cast<const T*>(a.vst) + (size_t)b * DH * a.vst_ld;
 
   // issue every global load of the chunk before the first LDS store
   uint4 kr[KCH], vr[VCH];
@@ -562,7 +562,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnLaunch a) {
       for (int j = 0; j < VEC; ++j) {
         const int key = key0 + j;
         tmp[j] = key < pl ? vpt[(size_t)d * a.vpt_dstride + key]
-                          : (key < nkeys ? vstb[(size_t)d * H + (key - pl)] : from_f32<T>(0.f));
+                          : (key < nkeys ? vstb[(size_t)d * a.vst_ld + (key - pl)] : from_f32<T>(0.f));
       }
       __builtin_memcpy(&vr[it], tmp, 16);
     }
@@ -721,11 +721,11 @@ static hipError_t launch_attention_t(const AttnLaunch& a, hipStream_t s) {
 
 hipError_t launch_attention(jpi_dtype dt, const AttnLaunch& a, hipStream_t s) {
   if (dt == JPI_BF16) {
-    switch (a.Dh) {
-      case 64: return launch_attention_t<bf16, 64>(a, s);
-      case 128: return launch_attention_t<bf16, 128>(a, s);
-      case 256: return launch_attention_t<bf16, 256>(a, s);
-    }
+    // key ranges are bounded by the chunk count the opart scratch is sized for
+    const int nch = attn_n_chunks(dt, a.P, a.H);
+    int S = flash_splits(a.B, a.nH, a.H, a.P, a.n_cu > 0 ? a.n_cu : 256);
+    S = S < nch ? S : nch;
+    return launch_flash(a, S, s);
   } else {
     switch (a.Dh) {
       case 64: return launch_attention_t<float, 64>(a, s);

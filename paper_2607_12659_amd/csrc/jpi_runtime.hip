@@ -371,7 +371,7 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   ALLOC(c->y, M * W * es);
   ALLOC(c->q, M * nH * Dh * es);
   ALLOC(c->ks, M * Dh * es);
-  ALLOC(c->vst, M * Dh * es);
+  ALLOC(c->vst, (size_t)c->Bmax * Dh * ((c->H + 7) / 8 * 8) * es);  // rows padded to 8 elements
   ALLOC(c->o, M * nH * Dh * es);
   ALLOC(c->z, M * F * es);
   ALLOC(c->pflags, (size_t)persist_flag_words() * sizeof(unsigned));
@@ -826,6 +826,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       g.ep.q = c->q;
       g.ep.ks = c->ks;
       g.ep.vst = c->vst;
+      g.ep.vst_ld = (H + 7) / 8 * 8;
       g.ep.rope = c->rope_tab;
       g.ep.n_heads = nH;
       g.ep.head_dim = Dh;
@@ -837,6 +838,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       a.q = c->q;
       a.ks = c->ks;
       a.vst = c->vst;
+      a.vst_ld = (H + 7) / 8 * 8;
       a.kp = (const char*)c->kp + (size_t)l * c->Bmax * c->Pmax * Dh * es;
       a.vpt = (const char*)c->vpt + (size_t)l * c->Bmax * c->Ppad * Dh * es;
       a.kp_bstride = (int64_t)c->Pmax * Dh;
@@ -853,6 +855,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       a.lpart = a.mpart + (size_t)batch * nH * nch * H;
       a.out = c->o;
       a.out_f32 = 0;
+      a.n_cu = c->n_cu;
       timing(JPI_KERNEL_ATTENTION, &a.ev_start, &a.ev_stop);
       ENQ(launch_attention(c->dt, a, s));
       // O projection (split-K slices) -> gated residual + MLP adaRMSNorm
@@ -1079,7 +1082,8 @@ jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, co
   hipError_t ea = hipMalloc((void**)&dlen, batch * sizeof(int));
   if (ea == hipSuccess) ea = hipMalloc((void**)&part, np * sizeof(float));
   if (ea == hipSuccess) ea = hipMalloc(&vpt, (size_t)batch * Dh * Ppad * es);
-  if (ea == hipSuccess) ea = hipMalloc(&vst, (size_t)batch * Dh * H * es);
+  const int Hs = (H + 7) / 8 * 8;  // V^T rows padded to 8 elements
+  if (ea == hipSuccess) ea = hipMalloc(&vst, (size_t)batch * Dh * Hs * es);
   auto cleanup = [&]() {
     if (dlen) (void)hipFree(dlen);
     if (part) (void)hipFree(part);
@@ -1096,6 +1100,7 @@ jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, co
   a.q = q;
   a.ks = ks;
   a.vst = vst;
+  a.vst_ld = Hs;
   a.kp = kp ? kp : ks;
   a.vpt = vpt;
   a.kp_bstride = (int64_t)P * Dh;
@@ -1112,10 +1117,16 @@ jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, co
   a.lpart = a.mpart + (size_t)batch * n_heads * nch * H;
   a.out = out;
   a.out_f32 = 1;
+  {
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+      a.n_cu = ncu;
+  }
   hipError_t e = hipMemcpyAsync(dlen, prefix_len_host, batch * sizeof(int), hipMemcpyHostToDevice, s);
   if (e == hipSuccess && P > 0)
     e = launch_transpose(dt, vp, vpt, P, Dh, Dh, Ppad, (int64_t)P * Dh, (int64_t)Dh * Ppad, batch, s);
-  if (e == hipSuccess) e = launch_transpose(dt, vs, vst, H, Dh, Dh, H, (int64_t)H * Dh, (int64_t)Dh * H, batch, s);
+  if (e == hipSuccess) e = launch_transpose(dt, vs, vst, H, Dh, Dh, Hs, (int64_t)H * Dh, (int64_t)Dh * Hs, batch, s);
   if (e == hipSuccess) e = launch_attention(dt, a, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   cleanup();

@@ -89,13 +89,15 @@ def test_gemm_splitk_is_deterministic():
     assert np.array_equal(r1, r2)
 
 
-def _attention(dt, B, nH, H, P, Dh, lens, seed=0, nan_masked=False, zero_q=False):
+def _attention(dt, B, nH, H, P, Dh, lens, seed=0, nan_masked=False, zero_q=False, loud_key=None):
     torch = torch_cuda()
     from paper_2607_12659_amd import jpi
     rng = np.random.default_rng(seed)
     q = rng.normal(size=(B, nH, H, Dh)) * (0.0 if zero_q else 1.0)
     ks, vs = rng.normal(size=(B, H, Dh)), rng.normal(size=(B, H, Dh))
     kp, vp = rng.normal(size=(B, P, Dh)), rng.normal(size=(B, P, Dh))
+    if loud_key is not None:
+        kp[:, loud_key] *= 200.0  # scores of about +-200 against ~ +-3 for the other keys
     if nan_masked:
         for b in range(B):
             kp[b, lens[b]:] = np.nan
@@ -116,13 +118,29 @@ def _attention(dt, B, nH, H, P, Dh, lens, seed=0, nan_masked=False, zero_q=False
 
 
 @pytest.mark.parametrize("B,nH,H,P,Dh,lens", [(2, 8, 50, 816, 256, [816, 301]), (1, 8, 50, 1600, 256, [1600]),
-                                              (3, 4, 10, 64, 64, [64, 0, 17]), (1, 2, 70, 130, 128, [129])])
+                                              (3, 4, 10, 64, 64, [64, 0, 17]), (1, 2, 70, 130, 128, [129]),
+                                              (5, 8, 37, 300, 256, [300, 1, 0, 63, 64]),
+                                              (16, 8, 50, 816, 256, [816] * 15 + [5]),
+                                              (64, 8, 50, 1600, 256, [1600] * 63 + [777])])
 def test_attention_bf16(B, nH, H, P, Dh, lens):
+    # covers one and several key ranges per query tile, action blocks with a
+    # ragged tail (H = 37, 70), empty and one-key prefixes, and the batch-64 shape
     from paper_2607_12659_amd import jpi
     got, ref, _ = _attention(jpi.JPI_BF16, B, nH, H, P, Dh, lens)
     # probabilities enter the PV product rounded to bf16 (relative 2^-9 each)
     assert np.abs(got - ref).max() < 1e-2, np.abs(got - ref).max()
     assert np.sqrt(((got - ref) ** 2).mean()) < 2e-3
+
+
+@pytest.mark.parametrize("B", [1, 16, 64])
+def test_attention_bf16_late_dominant_key(B):
+    # one prefix key far into the sequence scores hundreds of nats above the
+    # keys seen before it: the rows where it wins must come out as its value
+    # row (the kernel's probability reference has to move up for them)
+    from paper_2607_12659_amd import jpi
+    got, ref, _ = _attention(jpi.JPI_BF16, B, 8, 50, 816, 256, [816] * B, seed=5, loud_key=700)
+    assert np.isfinite(got).all()
+    assert np.abs(got - ref).max() < 1e-2, np.abs(got - ref).max()
 
 
 @pytest.mark.parametrize("B,nH,H,P,Dh,lens", [(2, 8, 50, 816, 256, [816, 301]), (1, 4, 10, 64, 64, [64]),
