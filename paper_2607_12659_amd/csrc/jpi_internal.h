@@ -39,6 +39,7 @@ struct GemmLaunch {
   const void* W;         // [N][K]
   int M, N, K;
   int splitk;            // > 1 only with EPI_STORE_F32
+  int n_cu;              // compute units of the device (tile choice); 0 = assume 256
   EpiKind epi;
   EpiParams ep;
   hipEvent_t ev_start, ev_stop;  // optional: timestamps of this launch (measurement)

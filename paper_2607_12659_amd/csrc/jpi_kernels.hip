@@ -310,7 +310,15 @@ hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s) {
     if (dt == JPI_BF16) return launch_skinny_t<bf16>(g, s);
     return launch_skinny_t<float>(g, s);
   }
-  if (dt == JPI_BF16) return launch_gemm_t<bf16, 128, 128>(g, s);
+  if (dt == JPI_BF16) {
+    // 128 x 128 tiles unless that leaves the grid short of the compute units
+    // and the epilogue cannot be split over K
+    const int n_cu = g.n_cu > 0 ? g.n_cu : 256;
+    auto tiles = [&](int bm, int bn) { return ((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * g.splitk; };
+    if (tiles(128, 128) >= n_cu || g.epi == EPI_STORE_F32) return launch_gemm_t<bf16, 128, 128>(g, s);
+    if (tiles(128, 64) >= n_cu) return launch_gemm_t<bf16, 128, 64>(g, s);
+    return launch_gemm_t<bf16, 64, 64>(g, s);
+  }
   return launch_gemm_t<float, 64, 64>(g, s);
 }
 

@@ -832,6 +832,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       g.ep.head_dim = Dh;
       g.ep.horizon = H;
       timing(JPI_KERNEL_QKV, &g.ev_start, &g.ev_stop);
+      g.n_cu = c->n_cu;
       ENQ(launch_gemm(c->dt, g, s));
       // attention
       AttnLaunch a{};
@@ -869,6 +870,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       g.epi = EPI_STORE_F32;
       g.ep.out_f32 = c->partial;
       timing(JPI_KERNEL_OPROJ, &g.ev_start, &g.ev_stop);
+      g.n_cu = c->n_cu;
       ENQ(launch_gemm(c->dt, g, s));
       RowLaunch r{};
       r.part = c->partial;
@@ -894,6 +896,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       g.ep.z = c->z;
       g.ep.mlp_dim = F;
       timing(JPI_KERNEL_GATEUP, &g.ev_start, &g.ev_stop);
+      g.n_cu = c->n_cu;
       ENQ(launch_gemm(c->dt, g, s));
       // Down (split-K slices) -> gated residual + next norm (or final head + Euler)
       g = GemmLaunch{};
@@ -906,6 +909,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       g.epi = EPI_STORE_F32;
       g.ep.out_f32 = c->partial;
       timing(JPI_KERNEL_DOWN, &g.ev_start, &g.ev_stop);
+      g.n_cu = c->n_cu;
       ENQ(launch_gemm(c->dt, g, s));
       r.S = p.s_d;
       r.gate = mm + 2 * W;
