@@ -20,7 +20,8 @@ JPI_F32, JPI_BF16 = 0, 1
 
 EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create", "jpi_destroy", "jpi_set_weight",
             "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
-            "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time"]
+            "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
+            "jpi_sched_run", "jpi_sched_sim_hooks"]
 JPI_KERNEL_NONE, JPI_KERNEL_QKV, JPI_KERNEL_ATTENTION, JPI_KERNEL_OPROJ, JPI_KERNEL_GATEUP, JPI_KERNEL_DOWN, \
     JPI_KERNEL_PERSISTENT = range(-1, 6)
 
@@ -31,6 +32,42 @@ class jpi_config(ctypes.Structure):
                 ("action_dim", ctypes.c_int), ("horizon", ctypes.c_int), ("max_batch", ctypes.c_int),
                 ("max_prefix", ctypes.c_int), ("dtype", ctypes.c_int), ("rms_eps", ctypes.c_float),
                 ("rope_base", ctypes.c_float)]
+
+
+# include/jpi_sched.h
+class jpi_sched_config(ctypes.Structure):
+    _fields_ = [("theta", ctypes.c_double), ("delta", ctypes.c_int), ("delta_ae", ctypes.c_int),
+                ("chunk_len", ctypes.c_int), ("action_ms", ctypes.c_double), ("iterations", ctypes.c_int64)]
+
+
+SCHED_VLM_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(ctypes.c_double))
+SCHED_CORR_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double))
+SCHED_ACT_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                ctypes.POINTER(ctypes.c_double))
+
+
+class jpi_sched_hooks(ctypes.Structure):
+    _fields_ = [("vlm", SCHED_VLM_FN), ("corr", SCHED_CORR_FN), ("act", SCHED_ACT_FN), ("user", ctypes.c_void_p)]
+
+
+class jpi_sched_event(ctypes.Structure):
+    _fields_ = [("t", ctypes.c_int64), ("vlm", ctypes.c_int), ("n_committed", ctypes.c_int),
+                ("conf_in", ctypes.c_double), ("conf_out", ctypes.c_double), ("ms", ctypes.c_double),
+                ("executed", ctypes.c_int64), ("starved", ctypes.c_int64)]
+
+
+class jpi_sched_stats(ctypes.Structure):
+    _fields_ = [("iterations", ctypes.c_int64), ("vlm_calls", ctypes.c_int64), ("startup_ms", ctypes.c_double),
+                ("total_ms", ctypes.c_double), ("reaction_ms", ctypes.c_double), ("control_hz", ctypes.c_double),
+                ("vlm_fraction", ctypes.c_double), ("actions_executed", ctypes.c_int64),
+                ("actions_starved", ctypes.c_int64)]
+
+
+class jpi_sched_sim(ctypes.Structure):
+    _fields_ = [("vit_ms", ctypes.c_double), ("llm_ms", ctypes.c_double), ("corr_ms", ctypes.c_double),
+                ("ae_ms", ctypes.c_double), ("conf", ctypes.POINTER(ctypes.c_double)), ("n_conf", ctypes.c_int64),
+                ("corr_calls", ctypes.c_int64), ("vlm_calls", ctypes.c_int64), ("act_calls", ctypes.c_int64)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -62,6 +99,9 @@ _sig = {
     "jpi_debug_attention": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
     "jpi_debug_time_kernel": (_i, [_vp, _i]),
     "jpi_debug_kernel_time": (_i, [_vp, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_i)]),
+    "jpi_sched_run": (_i, [ctypes.POINTER(jpi_sched_config), ctypes.POINTER(jpi_sched_hooks),
+                           ctypes.POINTER(jpi_sched_stats), ctypes.POINTER(jpi_sched_event), _i64]),
+    "jpi_sched_sim_hooks": (_i, [ctypes.POINTER(jpi_sched_sim), ctypes.POINTER(jpi_sched_hooks)]),
 }
 for _name, (_res, _args) in _sig.items():
     _fn = getattr(_lib, _name)
@@ -173,6 +213,18 @@ def jpi_debug_kernel_time(ctx):
     ms, n = ctypes.c_float(), _i()
     st = _lib.jpi_debug_kernel_time(ctx, ctypes.byref(ms), ctypes.byref(n))
     return st, ms.value, n.value
+
+
+def jpi_sched_run(cfg: jpi_sched_config, hooks: jpi_sched_hooks, trace_cap: int = 0):
+    """Returns (status, stats, events); events holds the first trace_cap iterations."""
+    stats = jpi_sched_stats()
+    trace = (jpi_sched_event * trace_cap)() if trace_cap > 0 else None
+    st = _lib.jpi_sched_run(ctypes.byref(cfg), ctypes.byref(hooks), ctypes.byref(stats), trace, trace_cap)
+    return st, stats, (list(trace) if trace is not None else [])
+
+
+def jpi_sched_sim_hooks(sim: jpi_sched_sim, hooks: jpi_sched_hooks) -> int:
+    return _lib.jpi_sched_sim_hooks(ctypes.byref(sim), ctypes.byref(hooks))
 
 
 class JpiError(RuntimeError):
