@@ -161,6 +161,100 @@ def cpu_baseline(wl, weights, K, V, noise):
                       "%.1f s in total" % (calls, wl.n_steps, wl.name, threads, dt)}
 
 
+def prefill_flops(vd, batch, prefix):
+    """Matrix and attention flops of one VLM prefill (every layer)."""
+    W, nH, Dh, F, M = vd.width, vd.n_heads, vd.head_dim, vd.mlp_dim, batch * prefix
+    per_layer = 2.0 * M * W * (nH + 2) * Dh + 4.0 * batch * nH * prefix * prefix * Dh + 2.0 * M * nH * Dh * W \
+        + 2.0 * M * W * 2 * F + 2.0 * M * F * W
+    return vd.n_layers * per_layer
+
+
+def bench_prefill(args, vwl):
+    """VLM prefill (Gemma-2B shape) writing its KV in place into a pi0.5 expert
+    context: one step = one prefill of every layer over the whole prefix."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2607_12659_amd import jpi
+    from paper_2607_12659_amd.expert import ActionExpert, to_device
+
+    vd = vwl.dims
+    print("bench: workload %s, generating %.2f B synthetic parameters" % (
+        vwl.name, sum(int(np.prod(s)) for _, s, _ in synth.vlm_weight_specs(vd)) / 1e9), file=sys.stderr, flush=True)
+    vw = synth.make_vlm_weights(vwl)
+    emb = synth.make_embeddings(vwl)
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    cfg = jpi.jpi_vlm_config(n_layers=vd.n_layers, width=vd.width, n_heads=vd.n_heads, n_kv_heads=vd.n_kv_heads,
+                             head_dim=vd.head_dim, mlp_dim=vd.mlp_dim, max_batch=vwl.batch, max_prefix=vwl.prefix,
+                             dtype=jpi.JPI_BF16, rms_eps=1e-6, rope_base=1e4)
+    st, vlm = jpi.jpi_vlm_create(cfg)
+    jpi.check(st)
+    for name, arr in vw.items():
+        arr = np.ascontiguousarray(arr)
+        st = jpi.jpi_vlm_set_weight(vlm, name, arr, arr.size, jpi.JPI_BF16 if arr.dtype == np.uint16 else jpi.JPI_F32, 0)
+        if st != jpi.JPI_OK:
+            raise RuntimeError(jpi.jpi_vlm_last_error(vlm))
+    del vw
+    if jpi.jpi_vlm_finalize_weights(vlm) != jpi.JPI_OK:
+        raise RuntimeError(jpi.jpi_vlm_last_error(vlm))
+    ewl = synth.WORKLOADS["pi05-b1"]
+    ae = ActionExpert(ewl.dims, ewl.dtype, vwl.batch, vwl.prefix)
+    ae.load_weights(synth.make_weights(ewl))
+    e_dev = to_device(np.ascontiguousarray(emb, np.float32))
+
+    def once():
+        st = jpi.jpi_vlm_prefill(vlm, e_dev, vwl.batch, vwl.prefix, ae.ctx, None, stream)
+        if st != jpi.JPI_OK:
+            raise RuntimeError(jpi.jpi_vlm_last_error(vlm))
+
+    for _ in range(args.warmup):
+        once()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        once()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    fl = prefill_flops(vd, vwl.batch, vwl.prefix)
+    tflops = fl / (ms * 1e-3) / 1e12
+    # the expert consumes the KV in place: one denoise right after the prefill
+    noise = to_device(np.ascontiguousarray(synth.make_noise(ewl), np.float32))
+    out = ae.denoise(noise, ewl.n_steps)
+    ae.sync()
+    finite = bool(torch.isfinite(out).all().item())
+    cpu = None
+    if not args.no_cpu:
+        import oracle
+        vd1 = synth.VlmDims(**{**vd.__dict__, "n_layers": 1})
+        w1 = synth.make_vlm_weights(vwl, n_layers=1)
+        t0 = time.time()
+        oracle.vlm_prefill(vd1, w1, emb[0])
+        dt = time.time() - t0
+        cpu = {"value": vwl.prefix / (dt * vd.n_layers), "unit": "tokens/s", "cores": os.cpu_count(),
+               "kind": "oracle", "sample": "one of the %d layers of the fp64 oracle prefill over %d tokens "
+               "(%.1f s), scaled to the whole stack" % (vd.n_layers, vwl.prefix, dt)}
+    result = {
+        "metric": "VLM prefill tokens/sec (Gemma-2B shape, prefix KV written in place into the action expert)",
+        "value": round(vwl.batch * vwl.prefix / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": vwl.name, "batch": vwl.batch, "prefix_tokens": vwl.prefix, "layers": vd.n_layers,
+                   "width": vd.width, "heads": vd.n_heads, "kv_heads": vd.n_kv_heads, "head_dim": vd.head_dim,
+                   "mlp_dim": vd.mlp_dim},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                     "flops_per_launch": fl, "avg_launch_us": round(ms * 1e3, 1)},
+        "cpu_baseline": cpu, "expert_after_handoff_finite": finite,
+    }
+    ae.close()
+    jpi.jpi_vlm_destroy(vlm)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -188,6 +282,9 @@ def main():
     from paper_2607_12659_amd import jpi
     from paper_2607_12659_amd.expert import ActionExpert, to_device
 
+    if args.workload in synth.VLM_WORKLOADS:
+        bench_prefill(args, synth.VLM_WORKLOADS[args.workload])
+        return
     wl = synth.WORKLOADS[args.workload]
     print("bench: workload %s, generating inputs" % wl.name, file=sys.stderr, flush=True)
     weights = synth.make_weights(wl)

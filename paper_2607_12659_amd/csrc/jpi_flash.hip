@@ -290,7 +290,8 @@ __global__ __launch_bounds__(512) void k_flash(AttnLaunch a, int S, int nqt, voi
     return;
   }
 
-  src.k_act = rsrc(reinterpret_cast<const bf16*>(a.ks) + (size_t)b * H * DH, (int64_t)H * DH * 2);
+  src.k_act = rsrc(reinterpret_cast<const bf16*>(a.ks) + (size_t)b * (a.ks_bstride ? a.ks_bstride : (int64_t)H * DH),
+                   (int64_t)H * DH * 2);
   src.v_act = rsrc(reinterpret_cast<const bf16*>(a.vst) + (size_t)b * DH * a.vst_ld, (int64_t)DH * a.vst_ld * 2);
   src.k_pre = rsrc(reinterpret_cast<const bf16*>(a.kp) + (size_t)b * a.kp_bstride, (int64_t)pl * DH * 2);
   src.v_pre = rsrc(reinterpret_cast<const bf16*>(a.vpt) + (size_t)b * a.vpt_bstride, (int64_t)DH * a.vpt_dstride * 2);

@@ -24,7 +24,8 @@ struct EpiParams {
   float* out_f32;
   // EPI_QKV: packed columns [q heads | k | v]; RoPE on q and k
   void* q;               // [B][nH][H][Dh]
-  void* ks;              // [B][H][Dh]
+  void* ks;              // [B][H][Dh], rollout b at ks + b * ks_bstride elements
+  int64_t ks_bstride;    // 0 means H * Dh
   void* vst;             // [B][Dh][vst_ld] (v stored transposed)
   int vst_ld;            // row stride of vst in elements (>= horizon)
   const float2* rope;    // [B][H][Dh/2] (cos, sin) at position prefix_len[b] + i
@@ -77,7 +78,8 @@ hipError_t launch_resid_norm(jpi_dtype dt, const RowLaunch& r, bool final_step, 
 
 struct AttnLaunch {
   const void* q;          // [B][nH][H][Dh]
-  const void* ks;         // [B][H][Dh]
+  const void* ks;         // [B][H][Dh], rollout b at ks + b * ks_bstride elements
+  int64_t ks_bstride;     // 0 means H * Dh
   const void* vst;        // [B][Dh][vst_ld]   suffix V, transposed
   int64_t vst_ld;         // row stride of vst in elements: >= H, a multiple of 8 on the bf16 path
   const void* kp;         // prefix K: rollout b at kp + b*kp_bstride, key j at + j*Dh
@@ -150,6 +152,26 @@ int persist_flag_words();  // size of the completion flag buffer in 32-bit words
 hipError_t launch_frag_order(const void* src, void* dst, int R, int K, hipStream_t s);
 hipError_t persist_occupancy(int Dh, int* blocks_per_cu);
 hipError_t launch_persist(const PersistArgs& a, int grid, hipStream_t s);
+
+// The resident prefix buffers of an action-expert context, for a producer
+// that writes them in place (the VLM prefill).  ae_prefix_target checks that
+// the producer's shape fits (L, Dh, dtype, batch, prefix) and returns the
+// buffers; ae_prefix_bound records them as bound with prefix_len = prefix for
+// rollouts 0..batch-1 (the caller has enqueued the writes, the prefix_len
+// fill and the rope table on its stream).
+struct AePrefixTarget {
+  void* kp;             // K [L][Bmax][Pmax][Dh]
+  void* vpt;            // V^T [L][Bmax][Dh][Ppad]
+  int64_t kp_lstride, kp_bstride, vpt_lstride, vpt_bstride;
+  int vpt_ld;           // Ppad
+  int* prefix_len;      // device [Bmax]
+  float2* rope_tab;     // device [Bmax][H][Dh/2]: the expert's own rows' positions
+  int H;                // the expert's horizon
+  float rope_base;
+};
+jpi_status ae_prefix_target(jpi_ctx* c, int L, int Dh, jpi_dtype dt, int batch, int prefix, AePrefixTarget* t,
+                            const char** why);
+jpi_status ae_prefix_bound(jpi_ctx* c, int batch, int prefix);
 
 hipError_t launch_time_embed(const float* t, float* emb, int n, int W, hipStream_t s);
 // out[m][n] = act(sum_k in[m][k] w[n][k] + b[n]), fp64 accumulation; act 0 = none, 1 = swish

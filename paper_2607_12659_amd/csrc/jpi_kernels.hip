@@ -50,8 +50,9 @@ __device__ __forceinline__ void epilogue_pair(const EpiParams& ep, float* out_f3
       const float2 cs = ep.rope[((size_t)b * H + i) * half + d];
       const float r_lo = lo * cs.x - hi * cs.y;
       const float r_hi = lo * cs.y + hi * cs.x;
+      const size_t kbs = ep.ks_bstride ? (size_t)ep.ks_bstride : (size_t)H * Dh;
       T* dst = hn >= 0 ? reinterpret_cast<T*>(ep.q) + (((size_t)b * ep.n_heads + hn) * H + i) * Dh
-                       : reinterpret_cast<T*>(ep.ks) + ((size_t)b * H + i) * Dh;
+                       : reinterpret_cast<T*>(ep.ks) + b * kbs + (size_t)i * Dh;
       dst[d] = from_f32<T>(r_lo);
       dst[d + half] = from_f32<T>(r_hi);
     } else {
@@ -546,7 +547,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnLaunch a) {
 
   const T* kp = reinterpret_cast<const T*>(a.kp) + (size_t)b * a.kp_bstride;
   const T* vpt = reinterpret_cast<const T*>(a.vpt) + (size_t)b * a.vpt_bstride;
-  const T* ksb = reinterpret_cast<const T*>(a.ks) + (size_t)b * H * DH;
+  const T* ksb = reinterpret_cast<const T*>(a.ks) + (size_t)b * (a.ks_bstride ? a.ks_bstride : (int64_t)H * DH);
   const T* vstb = reinterpret_cast<const T*>(a.vst) + (size_t)b * DH * a.vst_ld;
 
   // issue every global load of the chunk before the first LDS store

@@ -1139,3 +1139,43 @@ jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, co
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// resident prefix buffers for an in-place producer (the VLM prefill)
+// ---------------------------------------------------------------------------
+jpi_status jpi::ae_prefix_target(jpi_ctx* c, int L, int Dh, jpi_dtype dt, int batch, int prefix,
+                                 AePrefixTarget* t, const char** why) {
+  *why = nullptr;
+  if (!c || !t) {
+    *why = "action-expert context is NULL";
+    return JPI_ERR_ARG;
+  }
+  if (c->L != L || c->Dh != Dh || c->dt != dt) {
+    *why = "the action expert's layer count, head_dim or dtype differs from the producer's";
+    return JPI_ERR_SHAPE;
+  }
+  if (batch < 1 || batch > c->Bmax || prefix < 1 || prefix > c->Pmax) {
+    *why = "batch or prefix exceeds the action expert's max_batch / max_prefix";
+    return JPI_ERR_SHAPE;
+  }
+  t->kp = c->kp;
+  t->vpt = c->vpt;
+  t->kp_bstride = (int64_t)c->Pmax * Dh;
+  t->kp_lstride = (int64_t)c->Bmax * t->kp_bstride;
+  t->vpt_ld = c->Ppad;
+  t->vpt_bstride = (int64_t)Dh * c->Ppad;
+  t->vpt_lstride = (int64_t)c->Bmax * t->vpt_bstride;
+  t->prefix_len = c->d_prefix_len;
+  t->rope_tab = c->rope_tab;
+  t->H = c->H;
+  t->rope_base = c->cfg.rope_base;
+  return JPI_OK;
+}
+
+jpi_status jpi::ae_prefix_bound(jpi_ctx* c, int batch, int prefix) {
+  if (c->batch != batch) c->n_fixed = 0;  // committed rows were bound for another batch
+  c->batch = batch;
+  c->prefix = prefix;
+  c->prefix_bound = true;
+  return JPI_OK;
+}

@@ -21,7 +21,8 @@ JPI_F32, JPI_BF16 = 0, 1
 EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create", "jpi_destroy", "jpi_set_weight",
             "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
             "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
-            "jpi_sched_run", "jpi_sched_sim_hooks"]
+            "jpi_sched_run", "jpi_sched_sim_hooks", "jpi_vlm_create", "jpi_vlm_destroy", "jpi_vlm_set_weight",
+            "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error"]
 JPI_KERNEL_NONE, JPI_KERNEL_QKV, JPI_KERNEL_ATTENTION, JPI_KERNEL_OPROJ, JPI_KERNEL_GATEUP, JPI_KERNEL_DOWN, \
     JPI_KERNEL_PERSISTENT = range(-1, 6)
 
@@ -32,6 +33,14 @@ class jpi_config(ctypes.Structure):
                 ("action_dim", ctypes.c_int), ("horizon", ctypes.c_int), ("max_batch", ctypes.c_int),
                 ("max_prefix", ctypes.c_int), ("dtype", ctypes.c_int), ("rms_eps", ctypes.c_float),
                 ("rope_base", ctypes.c_float)]
+
+
+# include/jpi_vlm.h
+class jpi_vlm_config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int), ("width", ctypes.c_int), ("n_heads", ctypes.c_int),
+                ("n_kv_heads", ctypes.c_int), ("head_dim", ctypes.c_int), ("mlp_dim", ctypes.c_int),
+                ("max_batch", ctypes.c_int), ("max_prefix", ctypes.c_int), ("dtype", ctypes.c_int),
+                ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float)]
 
 
 # include/jpi_sched.h
@@ -102,6 +111,12 @@ _sig = {
     "jpi_sched_run": (_i, [ctypes.POINTER(jpi_sched_config), ctypes.POINTER(jpi_sched_hooks),
                            ctypes.POINTER(jpi_sched_stats), ctypes.POINTER(jpi_sched_event), _i64]),
     "jpi_sched_sim_hooks": (_i, [ctypes.POINTER(jpi_sched_sim), ctypes.POINTER(jpi_sched_hooks)]),
+    "jpi_vlm_create": (_i, [ctypes.POINTER(jpi_vlm_config), _i, ctypes.POINTER(_vp)]),
+    "jpi_vlm_destroy": (_i, [_vp]),
+    "jpi_vlm_set_weight": (_i, [_vp, ctypes.c_char_p, _vp, _i64, _i, _i, _vp]),
+    "jpi_vlm_finalize_weights": (_i, [_vp, _vp]),
+    "jpi_vlm_prefill": (_i, [_vp, _vp, _i, _i, _vp, _vp, _vp]),
+    "jpi_vlm_last_error": (ctypes.c_char_p, [_vp]),
 }
 for _name, (_res, _args) in _sig.items():
     _fn = getattr(_lib, _name)
@@ -225,6 +240,32 @@ def jpi_sched_run(cfg: jpi_sched_config, hooks: jpi_sched_hooks, trace_cap: int 
 
 def jpi_sched_sim_hooks(sim: jpi_sched_sim, hooks: jpi_sched_hooks) -> int:
     return _lib.jpi_sched_sim_hooks(ctypes.byref(sim), ctypes.byref(hooks))
+
+
+def jpi_vlm_create(cfg: jpi_vlm_config, device: int = 0):
+    out = ctypes.c_void_p()
+    st = _lib.jpi_vlm_create(ctypes.byref(cfg), device, ctypes.byref(out))
+    return st, out
+
+
+def jpi_vlm_destroy(vlm) -> int:
+    return _lib.jpi_vlm_destroy(vlm)
+
+
+def jpi_vlm_set_weight(vlm, name: str, data, n_elems: int, dtype: int, is_device: int, stream=None) -> int:
+    return _lib.jpi_vlm_set_weight(vlm, name.encode(), addr(data), n_elems, dtype, is_device, stream_handle(stream))
+
+
+def jpi_vlm_finalize_weights(vlm, stream=None) -> int:
+    return _lib.jpi_vlm_finalize_weights(vlm, stream_handle(stream))
+
+
+def jpi_vlm_prefill(vlm, emb, batch: int, prefix: int, ae_ctx, hidden_out=None, stream=None) -> int:
+    return _lib.jpi_vlm_prefill(vlm, addr(emb), batch, prefix, ae_ctx, addr(hidden_out), stream_handle(stream))
+
+
+def jpi_vlm_last_error(vlm) -> str:
+    return _lib.jpi_vlm_last_error(vlm).decode()
 
 
 class JpiError(RuntimeError):

@@ -62,3 +62,45 @@ def rel_l2_per_rollout(got, ref):
     num = np.sqrt(((got - ref) ** 2).reshape(got.shape[0], -1).sum(1))
     den = np.sqrt((ref ** 2).reshape(ref.shape[0], -1).sum(1))
     return float((num / den).max())
+
+
+class Vlm:
+    """A jpi_vlm context loaded with synthetic weights (bf16)."""
+
+    def __init__(self, vd, weights, max_batch, max_prefix):
+        torch = torch_cuda()
+        from paper_2607_12659_amd import jpi
+        self.jpi = jpi
+        cfg = jpi.jpi_vlm_config(n_layers=vd.n_layers, width=vd.width, n_heads=vd.n_heads, n_kv_heads=vd.n_kv_heads,
+                                 head_dim=vd.head_dim, mlp_dim=vd.mlp_dim, max_batch=max_batch,
+                                 max_prefix=max_prefix, dtype=jpi.JPI_BF16, rms_eps=1e-6, rope_base=1e4)
+        st, self.ctx = jpi.jpi_vlm_create(cfg)
+        assert st == jpi.JPI_OK, st
+        for name, arr in weights.items():
+            arr = np.ascontiguousarray(arr)
+            dt = jpi.JPI_BF16 if arr.dtype == np.uint16 else jpi.JPI_F32
+            st = jpi.jpi_vlm_set_weight(self.ctx, name, arr, arr.size, dt, 0)
+            assert st == jpi.JPI_OK, (name, jpi.jpi_vlm_last_error(self.ctx))
+        assert jpi.jpi_vlm_finalize_weights(self.ctx) == jpi.JPI_OK, jpi.jpi_vlm_last_error(self.ctx)
+        self.torch = torch
+
+    def prefill(self, emb_dev, batch, prefix, ae, hidden=None):
+        st = self.jpi.jpi_vlm_prefill(self.ctx, emb_dev, batch, prefix, ae.ctx, hidden)
+        assert st == self.jpi.JPI_OK, self.jpi.jpi_vlm_last_error(self.ctx)
+
+    def close(self):
+        self.jpi.jpi_vlm_destroy(self.ctx)
+
+
+def device_view_i16(ptr, shape):
+    """torch int16 view of device memory at ptr (zero-copy, read through the array interface)."""
+    import torch
+
+    class _A:
+        __cuda_array_interface__ = {"shape": tuple(shape), "typestr": "<i2", "data": (int(ptr), False), "version": 2}
+
+    return torch.as_tensor(_A(), device="cuda")
+
+
+def bf16_bits_to_f64(bits):
+    return (np.ascontiguousarray(bits).view(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
