@@ -176,14 +176,15 @@ def bench_prefill(args, vwl):
     import torch
 
     import synth
+    import synth.vlm as synth_vlm
     from paper_2607_12659_amd import jpi
     from paper_2607_12659_amd.expert import ActionExpert, to_device
 
     vd = vwl.dims
     print("bench: workload %s, generating %.2f B synthetic parameters" % (
-        vwl.name, sum(int(np.prod(s)) for _, s, _ in synth.vlm_weight_specs(vd)) / 1e9), file=sys.stderr, flush=True)
-    vw = synth.make_vlm_weights(vwl)
-    emb = synth.make_embeddings(vwl)
+        vwl.name, sum(int(np.prod(s)) for _, s, _ in synth_vlm.vlm_weight_specs(vd)) / 1e9), file=sys.stderr, flush=True)
+    vw = synth_vlm.make_vlm_weights(vwl)
+    emb = synth_vlm.make_embeddings(vwl)
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     cfg = jpi.jpi_vlm_config(n_layers=vd.n_layers, width=vd.width, n_heads=vd.n_heads, n_kv_heads=vd.n_kv_heads,
@@ -229,8 +230,8 @@ def bench_prefill(args, vwl):
     cpu = None
     if not args.no_cpu:
         import oracle
-        vd1 = synth.VlmDims(**{**vd.__dict__, "n_layers": 1})
-        w1 = synth.make_vlm_weights(vwl, n_layers=1)
+        vd1 = synth_vlm.VlmDims(**{**vd.__dict__, "n_layers": 1})
+        w1 = synth_vlm.make_vlm_weights(vwl, n_layers=1)
         t0 = time.time()
         oracle.vlm_prefill(vd1, w1, emb[0])
         dt = time.time() - t0
@@ -279,11 +280,12 @@ def main():
     import torch
 
     import synth
+    import synth.vlm as synth_vlm
     from paper_2607_12659_amd import jpi
     from paper_2607_12659_amd.expert import ActionExpert, to_device
 
-    if args.workload in synth.VLM_WORKLOADS:
-        bench_prefill(args, synth.VLM_WORKLOADS[args.workload])
+    if args.workload in synth_vlm.VLM_WORKLOADS:
+        bench_prefill(args, synth_vlm.VLM_WORKLOADS[args.workload])
         return
     wl = synth.WORKLOADS[args.workload]
     print("bench: workload %s, generating inputs" % wl.name, file=sys.stderr, flush=True)

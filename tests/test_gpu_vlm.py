@@ -11,6 +11,7 @@ import pytest
 
 import oracle
 import synth
+import synth.vlm as synth_vlm
 from gpu_util import (Vlm, bf16_bits_to_f64, device_view_i16, make_expert, rel_l2_per_rollout, run, torch_cuda)
 
 pytestmark = pytest.mark.gpu
@@ -49,8 +50,8 @@ def _check_prefill(vwl, n_layers=None, denoise=True):
     from paper_2607_12659_amd.expert import to_device
     vd = vwl.dims if n_layers is None else vwl.dims.__class__(**{**vwl.dims.__dict__, "n_layers": n_layers})
     print("case %s layers %d prefix %d" % (vwl.name, vd.n_layers, vwl.prefix), flush=True)
-    vw = synth.make_vlm_weights(vwl, n_layers=vd.n_layers)
-    emb = synth.make_embeddings(vwl)
+    vw = synth_vlm.make_vlm_weights(vwl, n_layers=vd.n_layers)
+    emb = synth_vlm.make_embeddings(vwl)
     K_o, V_o, hid_o = oracle.vlm_prefill(vd, vw, emb[0])
     vlm = Vlm(vd, vw, 1, vwl.prefix)
     # an action expert with the same layer count and head_dim (its own width)
@@ -96,12 +97,12 @@ def _check_prefill(vwl, n_layers=None, denoise=True):
 
 
 def test_vlm_tiny_prefill_and_handoff():
-    _check_prefill(synth.VLM_WORKLOADS["vlm-tiny"])
+    _check_prefill(synth_vlm.VLM_WORKLOADS["vlm-tiny"])
 
 
 def test_vlm_gemma_width_two_layers():
     # full Gemma-2B width, MLP and head shape, the first two layers, 816 tokens
-    _check_prefill(synth.VLM_WORKLOADS["gemma2b-p816"], n_layers=2, denoise=False)
+    _check_prefill(synth_vlm.VLM_WORKLOADS["gemma2b-p816"], n_layers=2, denoise=False)
 
 
 def test_vlm_full_gemma_into_pi05_expert():
@@ -109,13 +110,13 @@ def test_vlm_full_gemma_into_pi05_expert():
     # across two prefills, the expert's actions are finite and repeat exactly
     torch = torch_cuda()
     from paper_2607_12659_amd.expert import to_device
-    vwl = synth.VLM_WORKLOADS["gemma2b-p816"]
+    vwl = synth_vlm.VLM_WORKLOADS["gemma2b-p816"]
     print("case gemma2b-p816 full into pi05 expert", flush=True)
-    vlm = Vlm(vwl.dims, synth.make_vlm_weights(vwl), 1, vwl.prefix)
+    vlm = Vlm(vwl.dims, synth_vlm.make_vlm_weights(vwl), 1, vwl.prefix)
     ewl = synth.WORKLOADS["pi05-b1"]
     ae = make_expert(ewl, synth.make_weights(ewl), max_batch=1, max_prefix=vwl.prefix)
     try:
-        emb = to_device(np.ascontiguousarray(synth.make_embeddings(vwl), np.float32))
+        emb = to_device(np.ascontiguousarray(synth_vlm.make_embeddings(vwl), np.float32))
         noise = to_device(np.ascontiguousarray(synth.make_noise(ewl), np.float32))
         outs, ks = [], []
         for _ in range(2):

@@ -13,16 +13,17 @@ import pytest
 
 import oracle
 import synth
+import synth.vlm as synth_vlm
 
 
 def _dims(L=2, W=8, nH=2, Dh=4, F=8):
-    return synth.VlmDims(n_layers=L, width=W, n_heads=nH, n_kv_heads=1, head_dim=Dh, mlp_dim=F)
+    return synth_vlm.VlmDims(n_layers=L, width=W, n_heads=nH, n_kv_heads=1, head_dim=Dh, mlp_dim=F)
 
 
 def _weights(d, seed=3, std=0.3):
     rng = np.random.default_rng(seed)
     w = {}
-    for name, shape, is_mat in synth.vlm_weight_specs(d):
+    for name, shape, is_mat in synth_vlm.vlm_weight_specs(d):
         w[name] = rng.normal(size=shape) * std
     return w
 
