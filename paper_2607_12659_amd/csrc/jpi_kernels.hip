@@ -65,12 +65,16 @@ __device__ __forceinline__ void epilogue_pair(const EpiParams& ep, float* out_f3
 }
 
 // ---- tiled GEMM for M > 64: workgroup tile BM x BN, 4 waves in 2 x 2, K
-// staged through LDS in BK slices with register double buffering ----------
+// staged through LDS in BK slices with register double buffering.  An LDS
+// row is one 128-byte slice row (8 chunks of 16 bytes); chunk c of row r is
+// stored at position c ^ ((r >> 1) & 7), so that the 16 lanes of an LDS
+// cycle touch distinct banks both when a slice is written (two rows of 8
+// chunks) and when MFMA fragments are read (16 rows, one chunk each) --------
 template <typename T, int BM, int BN>
 struct GemmShape {
   static constexpr int BK = sizeof(T) == 2 ? 64 : 32;
   static constexpr int VEC = 16 / sizeof(T);      // elements per 16-byte chunk
-  static constexpr int LDK = BK + VEC;            // padded LDS row (bank spread)
+  static constexpr int LDK = BK;                  // LDS row: 128 bytes, chunks swizzled
   static constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
   static constexpr int TM = WM / 16, TN = WN / 16;
   static constexpr int CPR = BK / VEC;            // 16-byte chunks per tile row
@@ -78,6 +82,9 @@ struct GemmShape {
   static constexpr int W_CH = BN * CPR / 256;
   static_assert(TN % 2 == 0, "epilogues pair n-subtiles 2t and 2t+1");
   static_assert(A_CH >= 1 && W_CH >= 1, "tile too small for 256 threads");
+  static_assert(CPR == 8, "the swizzle permutes 8 chunks per row");
+  // element offset of (row r, chunk c) in a tile
+  static __device__ __forceinline__ int at(int r, int c) { return r * LDK + ((c ^ ((r >> 1) & 7)) * VEC); }
 };
 
 template <typename T, int BM, int BN, EpiKind EPI>
@@ -119,12 +126,12 @@ __global__ __launch_bounds__(256) void k_gemm(GemmLaunch g) {
 #pragma unroll
     for (int c = 0; c < S::A_CH; ++c) {
       const int e = tid + c * 256, r = e / S::CPR, cc = e - r * S::CPR;
-      *reinterpret_cast<uint4*>(&As[buf][r * S::LDK + cc * S::VEC]) = ra[c];
+      *reinterpret_cast<uint4*>(&As[buf][S::at(r, cc)]) = ra[c];
     }
 #pragma unroll
     for (int c = 0; c < S::W_CH; ++c) {
       const int e = tid + c * 256, r = e / S::CPR, cc = e - r * S::CPR;
-      *reinterpret_cast<uint4*>(&Ws[buf][r * S::LDK + cc * S::VEC]) = rw[c];
+      *reinterpret_cast<uint4*>(&Ws[buf][S::at(r, cc)]) = rw[c];
     }
   };
 
@@ -141,15 +148,15 @@ __global__ __launch_bounds__(256) void k_gemm(GemmLaunch g) {
   for (int kt = 0; kt < nkt; ++kt) {
     const int buf = kt & 1;
     if (kt + 1 < nkt) gload(kt + 1);
-    const T* as = As[buf] + (wm * S::WM + fr) * S::LDK + fk;
-    const T* ws = Ws[buf] + (wn * S::WN + fr) * S::LDK + fk;
 #pragma unroll
     for (int kk = 0; kk < S::BK; kk += MF::KSUB) {
+      // lane reads k values kk + fk .. + KPL of its row: one chunk (bf16) or part of one (fp32)
+      const int kc = (kk + fk) / S::VEC, ke = (kk + fk) % S::VEC;
       typename MF::frag af[S::TM], bfr[S::TN];
 #pragma unroll
-      for (int a = 0; a < S::TM; ++a) af[a] = MF::load(as + a * 16 * S::LDK + kk);
+      for (int a = 0; a < S::TM; ++a) af[a] = MF::load(As[buf] + S::at(wm * S::WM + a * 16 + fr, kc) + ke);
 #pragma unroll
-      for (int b = 0; b < S::TN; ++b) bfr[b] = MF::load(ws + b * 16 * S::LDK + kk);
+      for (int b = 0; b < S::TN; ++b) bfr[b] = MF::load(Ws[buf] + S::at(wn * S::WN + b * 16 + fr, kc) + ke);
 #pragma unroll
       for (int a = 0; a < S::TM; ++a)
 #pragma unroll
