@@ -178,6 +178,106 @@ __global__ __launch_bounds__(256) void k_gemm(GemmLaunch g) {
         epilogue_pair<T, EPI>(g.ep, out, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i], acc[a][b + 1][i]);
 }
 
+// ---- large bf16 GEMM tiles: 256 x 256 per workgroup, 8 waves in 2 x 4
+// (wave tile 128 x 64), the same swizzled 128-byte LDS rows and register
+// double buffering as k_gemm.  A K slice moves 64 KB for four times the
+// products of a 128 x 128 tile, half the bytes per product. ------------------
+struct BigShape {
+  static constexpr int BM = 256, BN = 256, BK = 64, VEC = 8, CPR = 8, NT = 512;
+  static constexpr int WM = 128, WN = 64, TM = WM / 16, TN = WN / 16;
+  static constexpr int A_CH = BM * CPR / NT, W_CH = BN * CPR / NT;  // 16-byte chunks per thread
+  static __device__ __forceinline__ int at(int r, int c) { return r * BK + ((c ^ ((r >> 1) & 7)) * VEC); }
+};
+
+template <EpiKind EPI>
+__global__ __launch_bounds__(512) void k_gemm_big(GemmLaunch g) {
+  using S = BigShape;
+  using MF = Mfma<bf16>;
+  __shared__ __attribute__((aligned(16))) bf16 As[2][S::BM * S::BK];
+  __shared__ __attribute__((aligned(16))) bf16 Ws[2][S::BN * S::BK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int m0 = blockIdx.y * S::BM, n0 = blockIdx.x * S::BN;
+  const int M = g.M, N = g.N, K = g.K;
+  const int kper = K / g.splitk, kbeg = blockIdx.z * kper, nkt = kper / S::BK;
+  const bf16* A = reinterpret_cast<const bf16*>(g.A);
+  const bf16* W = reinterpret_cast<const bf16*>(g.W);
+  uint4 ra[S::A_CH], rw[S::W_CH];
+  auto gload = [&](int kt) {
+    const int k0 = kbeg + kt * S::BK;
+#pragma unroll
+    for (int c = 0; c < S::A_CH; ++c) {
+      const int e = tid + c * S::NT, r = e / S::CPR, cc = e - r * S::CPR, row = m0 + r;
+      ra[c] = row < M ? *reinterpret_cast<const uint4*>(A + (size_t)row * K + k0 + cc * S::VEC) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int c = 0; c < S::W_CH; ++c) {
+      const int e = tid + c * S::NT, r = e / S::CPR, cc = e - r * S::CPR, n = n0 + r;
+      rw[c] = n < N ? *reinterpret_cast<const uint4*>(W + (size_t)n * K + k0 + cc * S::VEC) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < S::A_CH; ++c) {
+      const int e = tid + c * S::NT, r = e / S::CPR, cc = e - r * S::CPR;
+      *reinterpret_cast<uint4*>(&As[buf][S::at(r, cc)]) = ra[c];
+    }
+#pragma unroll
+    for (int c = 0; c < S::W_CH; ++c) {
+      const int e = tid + c * S::NT, r = e / S::CPR, cc = e - r * S::CPR;
+      *reinterpret_cast<uint4*>(&Ws[buf][S::at(r, cc)]) = rw[c];
+    }
+  };
+  f32x4 acc[S::TM][S::TN];
+#pragma unroll
+  for (int a = 0; a < S::TM; ++a)
+#pragma unroll
+    for (int b = 0; b < S::TN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int fr = lane & 15, fk = (lane >> 4) * MF::KPL;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nkt; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nkt) gload(kt + 1);
+#pragma unroll
+    for (int kk = 0; kk < S::BK; kk += MF::KSUB) {
+      const int kc = (kk + fk) / S::VEC;
+      MF::frag af[S::TM], bfr[S::TN];
+#pragma unroll
+      for (int a = 0; a < S::TM; ++a) af[a] = MF::load(As[buf] + S::at(wm * S::WM + a * 16 + fr, kc));
+#pragma unroll
+      for (int b = 0; b < S::TN; ++b) bfr[b] = MF::load(Ws[buf] + S::at(wn * S::WN + b * 16 + fr, kc));
+#pragma unroll
+      for (int a = 0; a < S::TM; ++a)
+#pragma unroll
+        for (int b = 0; b < S::TN; ++b) acc[a][b] = MF::run(af[a], bfr[b], acc[a][b]);
+    }
+    if (kt + 1 < nkt) sstore(buf ^ 1);
+    __syncthreads();
+  }
+  const int rbase = m0 + wm * S::WM + (lane >> 4) * 4;
+  const int cbase = n0 + wn * S::WN + fr;
+  float* out = g.ep.out_f32 ? g.ep.out_f32 + (size_t)blockIdx.z * M * N : nullptr;
+#pragma unroll
+  for (int a = 0; a < S::TM; ++a)
+#pragma unroll
+    for (int b = 0; b < S::TN; b += 2)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        epilogue_pair<bf16, EPI>(g.ep, out, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i], acc[a][b + 1][i]);
+}
+
+static hipError_t launch_big(const GemmLaunch& g, hipStream_t s) {
+  dim3 grid((g.N + BigShape::BN - 1) / BigShape::BN, (g.M + BigShape::BM - 1) / BigShape::BM, g.splitk);
+  switch (g.epi) {
+    case EPI_STORE_F32: JPI_LAUNCH((k_gemm_big<EPI_STORE_F32>), grid, dim3(512), 0, s, g.ev_start, g.ev_stop, g); break;
+    case EPI_QKV: JPI_LAUNCH((k_gemm_big<EPI_QKV>), grid, dim3(512), 0, s, g.ev_start, g.ev_stop, g); break;
+    case EPI_GEGLU: JPI_LAUNCH((k_gemm_big<EPI_GEGLU>), grid, dim3(512), 0, s, g.ev_start, g.ev_stop, g); break;
+  }
+  return hipGetLastError();
+}
+
 // ---- skinny GEMM for M <= 64 (weight streaming): a workgroup owns 32 output
 // columns and one K slice; its 4 waves split the slice four ways.  Each wave
 // issues its weight fragments (16 bytes per lane per 16x32 tile) and
@@ -319,10 +419,11 @@ hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s) {
     return launch_skinny_t<float>(g, s);
   }
   if (dt == JPI_BF16) {
-    // 128 x 128 tiles unless that leaves the grid short of the compute units
-    // and the epilogue cannot be split over K
+    // 256 x 256 tiles when they alone cover the compute units, else 128 x 128
+    // unless that leaves the grid short and the epilogue cannot be split over K
     const int n_cu = g.n_cu > 0 ? g.n_cu : 256;
     auto tiles = [&](int bm, int bn) { return ((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * g.splitk; };
+    if (tiles(256, 256) >= n_cu) return launch_big(g, s);
     if (tiles(128, 128) >= n_cu || g.epi == EPI_STORE_F32) return launch_gemm_t<bf16, 128, 128>(g, s);
     if (tiles(128, 64) >= n_cu) return launch_gemm_t<bf16, 128, 64>(g, s);
     return launch_gemm_t<bf16, 64, 64>(g, s);
