@@ -1,4 +1,5 @@
-"""CPU oracle (fp64) of the action-expert denoiser and of the VLM prefill.
+"""CPU oracle (fp64) of the action-expert denoiser, the VLM prefill and the
+future correction module.
 
 TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
 and the ``cpu_baseline`` leg of ``bench.py``, never by the GPU path.
@@ -8,7 +9,8 @@ from .actionexpert import (Expert, ada_rms_norm, attention_bruteforce, denoise, 
                            softmax_rows, step_times, swish, time_conditioning,
                            timestep_embedding, velocity, widen)
 from .vlm import prefill as vlm_prefill
+from . import correction
 
 __all__ = ["Expert", "ada_rms_norm", "attention_bruteforce", "denoise", "gelu_tanh", "integrate",
            "modulation", "prefix_self_attention", "rms_normalize", "rope", "softmax_rows",
-           "step_times", "swish", "time_conditioning", "timestep_embedding", "velocity", "widen", "vlm_prefill"]
+           "step_times", "swish", "time_conditioning", "timestep_embedding", "velocity", "widen", "vlm_prefill", "correction"]

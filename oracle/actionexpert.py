@@ -38,6 +38,14 @@ R8  Each action query sees prefix keys j < prefix_len and all H action keys;
     masked prefix slots are never read.
 R9  Committed rows (i < n_fixed) are ordinary tokens that share the global t
     and are never Euler-updated.
+R10 The correction item (T' tokens already in the expert's width, Section
+    "Foresight-Aligned Asynchronous Correction") enters as T' extra suffix
+    tokens placed ahead of the action tokens: correction token j sits at RoPE
+    position prefix_len + j and action token i at prefix_len + T' + i.  The
+    correction tokens skip the action in-projection, go through every layer
+    with the step's modulation, attend to and are attended by all suffix
+    tokens, restart from the given values at every step, and give no
+    velocity (only action tokens are Euler-updated).
 R13 Rollouts are independent (own prefix KV, own prefix_len).
 
 All arithmetic is fp64.  bf16 inputs arrive as bit patterns and are widened
@@ -203,38 +211,45 @@ def modulation(ex: Expert, name: str, cond):
     return tuple(m[i * ex.W:(i + 1) * ex.W] for i in range(m.shape[0] // ex.W))
 
 
-def velocity(ex: Expert, x, t: float, Kp, Vp, prefix_len):
+def velocity(ex: Expert, x, t: float, Kp, Vp, prefix_len, corr=None):
     """v(x, t) for a batch of independent rollouts.
 
     x: [B][H][A]; Kp, Vp: [L][B][P][Dh] (any dtype, widened here);
-    prefix_len: [B].  Returns v [B][H][A].
+    prefix_len: [B]; corr: [B][T'][W] correction tokens or None (reading
+    R10).  Returns v [B][H][A].
     """
     w = ex.w
     B, H, A = x.shape
     W, nH, Dh, L = ex.W, ex.nH, ex.Dh, ex.L
+    C = 0 if corr is None else np.asarray(corr).shape[1]
+    S = C + H                                                                  # suffix tokens per rollout
     cond = time_conditioning(ex, t)
-    h = x.reshape(B * H, A) @ w["action_in.w"].T + w["action_in.b"]          # [BH][W]
+    act = x.reshape(B, H, A) @ w["action_in.w"].T + w["action_in.b"]           # [B][H][W]
+    if C:
+        act = np.concatenate([widen(corr).reshape(B, C, W), act], axis=1)      # reading R10
+    h = act.reshape(B * S, W)
     for l in range(L):
         p = "layers.%d." % l
         scale, shift, gate = modulation(ex, p + "attn_mod", cond)
         y = ada_rms_norm(h, scale, shift)
-        q = (y @ w[p + "q.w"].T).reshape(B, H, nH, Dh)
-        ks = (y @ w[p + "k.w"].T).reshape(B, H, Dh)
-        vs = (y @ w[p + "v.w"].T).reshape(B, H, Dh)
-        o = np.empty((B, H, nH * Dh))
+        q = (y @ w[p + "q.w"].T).reshape(B, S, nH, Dh)
+        ks = (y @ w[p + "k.w"].T).reshape(B, S, Dh)
+        vs = (y @ w[p + "v.w"].T).reshape(B, S, Dh)
+        o = np.empty((B, S, nH * Dh))
         for b in range(B):
             pl = int(prefix_len[b])
-            pos = pl + np.arange(H)                                            # reading R7
-            qb = rope(np.transpose(q[b], (1, 0, 2)), pos)                      # [nH][H][Dh]
+            pos = pl + np.arange(S)                                            # readings R7, R10
+            qb = rope(np.transpose(q[b], (1, 0, 2)), pos)                      # [nH][S][Dh]
             kb = rope(ks[b], pos)
             ob = prefix_self_attention(qb, widen(Kp[l, b]), widen(Vp[l, b]), pl, kb, vs[b])
-            o[b] = np.transpose(ob, (1, 0, 2)).reshape(H, nH * Dh)
-        h = h + gate * (o.reshape(B * H, nH * Dh) @ w[p + "o.w"].T)
+            o[b] = np.transpose(ob, (1, 0, 2)).reshape(S, nH * Dh)
+        h = h + gate * (o.reshape(B * S, nH * Dh) @ w[p + "o.w"].T)
         scale, shift, gate = modulation(ex, p + "mlp_mod", cond)
         y = ada_rms_norm(h, scale, shift)
         z = gelu_tanh(y @ w[p + "gate.w"].T) * (y @ w[p + "up.w"].T)
         h = h + gate * (z @ w[p + "down.w"].T)
     scale, shift = modulation(ex, "final_mod", cond)
+    h = h.reshape(B, S, W)[:, C:, :].reshape(B * H, W)                          # action tokens only
     v = ada_rms_norm(h, scale, shift) @ w["action_out.w"].T + w["action_out.b"]
     return v.reshape(B, H, A)
 
@@ -263,13 +278,15 @@ def integrate(x1, n_fixed: int, n_steps: int, vel_fn):
     return x
 
 
-def denoise(ex: Expert, noise, Kp, Vp, prefix_len, n_steps: int, committed=None, n_fixed: int = 0):
+def denoise(ex: Expert, noise, Kp, Vp, prefix_len, n_steps: int, committed=None, n_fixed: int = 0,
+            corr=None):
     """The whole hot path: action chunk from noise by N Euler steps.
 
-    noise: [B][H][A]; committed: [B][n_fixed][A] or None.  Returns fp64 [B][H][A].
+    noise: [B][H][A]; committed: [B][n_fixed][A] or None; corr: [B][T'][W]
+    correction tokens or None (reading R10).  Returns fp64 [B][H][A].
     """
     x = np.array(noise, dtype=np.float64)
     if n_fixed:
         x[:, :n_fixed, :] = np.asarray(committed, dtype=np.float64)
     return integrate(x, n_fixed, n_steps,
-                     lambda xx, t: velocity(ex, xx, t, Kp, Vp, prefix_len))
+                     lambda xx, t: velocity(ex, xx, t, Kp, Vp, prefix_len, corr))

@@ -23,6 +23,7 @@ sys.path.insert(0, ROOT)
 
 import oracle  # noqa: E402
 import synth  # noqa: E402
+from synth import correction as synth_corr  # noqa: E402
 
 # name -> (workload key, overrides, rollouts evaluated)
 CASES = {
@@ -35,7 +36,12 @@ CASES = {
     "pi05-f32-b1": ("pi05-b1", {"dtype": "f32", "name": "pi05-f32-b1"}, None),
     # ragged prefix lengths (masked slots) over two rollouts
     "pi05-b2-ragged": ("pi05-b8", {"batch": 2, "prefix_len": (816, 301), "name": "pi05-b2-ragged"}, None),
+    # the correction item of the future correction module (4 tokens) ahead of the
+    # action tokens, with the committed rows of the same call
+    "pi05-b1-committed10-corr4": ("pi05-b1-committed10", {"name": "pi05-b1-committed10-corr4"}, None),
 }
+# cases whose expert call also gets correction tokens: name -> tokens per rollout
+CORR_TOKENS = {"pi05-b1-committed10-corr4": 4}
 
 
 def source_hash(*paths):
@@ -60,9 +66,11 @@ def make(name):
     noise = synth.make_noise(wl, rl)
     com = synth.make_committed(wl, rl) if wl.n_fixed else None
     lens = [wl.valid_lengths()[b] for b in rl]
+    n_corr = CORR_TOKENS.get(name, 0)
+    corr = synth_corr.make_item(wl.seed, wl.batch, n_corr, wl.dims.width, rl) if n_corr else None
     ex = oracle.Expert(wl.dims, w)
     t1 = time.time()
-    out = oracle.denoise(ex, noise, K, V, lens, wl.n_steps, committed=com, n_fixed=wl.n_fixed)
+    out = oracle.denoise(ex, noise, K, V, lens, wl.n_steps, committed=com, n_fixed=wl.n_fixed, corr=corr)
     t2 = time.time()
     np.save(os.path.join(HERE, name + ".npy"), out, allow_pickle=False)
     meta = {"workload": wl.name, "base_workload": CASES[name][0], "overrides": {k: list(v) if isinstance(v, tuple) else v
@@ -73,7 +81,10 @@ def make(name):
             "synth_sha256": source_hash(os.path.join(ROOT, "synth", "synth.c"),
                                         os.path.join(ROOT, "synth", "__init__.py")),
             "oracle_seconds": round(t2 - t1, 2), "setup_seconds": round(t1 - t0, 2),
+            "n_corr": n_corr,
             "made_by": "tests/golden/make_golden.py (oracle + synth only)"}
+    if n_corr:
+        meta["item_sha256"] = source_hash(os.path.join(ROOT, "synth", "correction.py"))
     with open(os.path.join(HERE, name + ".json"), "w") as f:
         json.dump(meta, f, indent=1)
     print("%s: oracle %.1fs setup %.1fs" % (name, t2 - t1, t1 - t0), flush=True)

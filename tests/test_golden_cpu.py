@@ -37,6 +37,8 @@ def test_golden_made_by_current_sources(name, meta):
         "oracle changed since %s was generated: rerun tests/golden/make_golden.py" % name
     assert meta["synth_sha256"] == make_golden.source_hash(os.path.join(ROOT, "synth", "synth.c"),
                                                            os.path.join(ROOT, "synth", "__init__.py"))
+    if meta.get("n_corr"):
+        assert meta["item_sha256"] == make_golden.source_hash(os.path.join(ROOT, "synth", "correction.py"))
     arr = np.load(os.path.join(HERE, "golden", name + ".npy"), allow_pickle=False)
     assert arr.shape == (len(meta["rollouts"]), 50, 32) and np.isfinite(arr).all()
 

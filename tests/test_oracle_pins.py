@@ -203,9 +203,10 @@ def _small(seed=99, P=6, B=2, dtype="f32"):
     return wl, w, K, V, synth.make_noise(wl)
 
 
-def _bruteforce_velocity(w, d, x, t, Kp, Vp, plen):
+def _bruteforce_velocity(w, d, x, t, Kp, Vp, plen, corr=()):
     """Scalar-loop velocity for one rollout, written from the same readings
-    with explicit [out][in] indexing (a second, independent formulation)."""
+    with explicit [out][in] indexing (a second, independent formulation).
+    ``corr`` holds correction tokens, which occupy the first suffix slots."""
     W, H, A, nH, Dh, F = d.width, d.horizon, d.action_dim, d.n_heads, d.head_dim, d.mlp_dim
     g = {k: np.asarray(synth.bf16_bits_to_f32(v) if v.dtype == np.uint16 else v, dtype=np.float64)
          for k, v in w.items()}
@@ -237,7 +238,9 @@ def _bruteforce_velocity(w, d, x, t, Kp, Vp, plen):
             out[j + hd] = vec[j] * math.sin(a) + vec[j + hd] * math.cos(a)
         return out
 
-    h = [lin("action_in.w", x[i], "action_in.b") for i in range(H)]
+    C = len(corr)
+    h = [list(map(float, corr[j])) for j in range(C)] + [lin("action_in.w", x[i], "action_in.b") for i in range(H)]
+    H = C + d.horizon                       # every suffix token goes through the layers
     for l in range(d.n_layers):
         p = "layers.%d." % l
         m = lin(p + "attn_mod.w", cond, p + "attn_mod.b")
@@ -271,7 +274,7 @@ def _bruteforce_velocity(w, d, x, t, Kp, Vp, plen):
             dn = lin(p + "down.w", z)
             h[i] = [h[i][c_] + gt[c_] * dn[c_] for c_ in range(W)]
     m = lin("final_mod.w", cond, "final_mod.b")
-    return np.array([lin("action_out.w", norm(h[i], m[:W], m[W:]), "action_out.b") for i in range(H)])
+    return np.array([lin("action_out.w", norm(h[i], m[:W], m[W:]), "action_out.b") for i in range(C, H)])
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -358,6 +361,84 @@ def test_prefix_kv_matters():
     a = oracle.denoise(ex, noise, K, V, [8, 8], 3)
     b = oracle.denoise(ex, noise, K, V * 1.5, [8, 8], 3)
     assert np.abs(a - b).max() > 1e-3
+
+
+# ---------------------------------------------------------------------------
+# correction tokens in the expert (reading R10)
+# ---------------------------------------------------------------------------
+def _corr(B=2, C=3, seed=21):
+    return np.random.default_rng(seed).normal(size=(B, C, SMALL.width))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_velocity_with_correction_matches_scalar_bruteforce(dtype):
+    wl, w, K, V, noise = _small(dtype=dtype)
+    ex = oracle.Expert(SMALL, w)
+    corr = _corr()
+    plens = [6, 2]
+    v = oracle.velocity(ex, noise, 0.3, K, V, plens, corr)
+    for b in range(2):
+        ref = _bruteforce_velocity(w, SMALL, noise[b].astype(np.float64), 0.3, oracle.widen(K[:, b]),
+                                   oracle.widen(V[:, b]), plens[b], corr[b])
+        np.testing.assert_allclose(v[b], ref, rtol=1e-10, atol=1e-12)
+
+
+def test_one_layer_correction_tokens_act_as_extra_prefix_keys():
+    """With one layer the correction tokens reach the action tokens only
+    through their layer-0 keys and values, so the velocity equals the one
+    without them over a prefix extended by those keys (rotated at the slots
+    prefix_len + j) and values, with the action tokens at the same positions."""
+    d1 = synth.Dims(n_layers=1, width=16, n_heads=2, n_kv_heads=1, head_dim=8, mlp_dim=24,
+                    action_dim=3, horizon=4)
+    wl = synth.Workload("one", d1, prefix=6, batch=2, n_steps=3, n_fixed=0, dtype="f32", seed=5)
+    w = synth.make_weights(wl, std=0.3)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    ex = oracle.Expert(d1, w)
+    corr = _corr()
+    C, t, plens = corr.shape[1], 0.55, [6, 4]
+    v = oracle.velocity(ex, noise, t, K, V, plens, corr)
+    cond = oracle.time_conditioning(ex, t)
+    g = {k: np.asarray(val, np.float64) for k, val in w.items()}
+    m = g["layers.0.attn_mod.w"] @ cond + g["layers.0.attn_mod.b"]
+    W = d1.width
+    K2 = np.zeros((1, 2, 6 + C, d1.head_dim))
+    V2 = np.zeros_like(K2)
+    for b in range(2):
+        pl = plens[b]
+        rms = np.sqrt(np.mean(corr[b] ** 2, axis=1, keepdims=True) + 1e-6)
+        y = corr[b] / rms * (1 + m[:W]) + m[W:2 * W]
+        kc = y @ g["layers.0.k.w"].T
+        ang = (pl + np.arange(C))[:, None] * 1e4 ** (-np.arange(4) / 4.0)[None, :]
+        kr = np.concatenate([kc[:, :4] * np.cos(ang) - kc[:, 4:] * np.sin(ang),
+                             kc[:, :4] * np.sin(ang) + kc[:, 4:] * np.cos(ang)], axis=1)
+        K2[0, b, :pl] = K[0, b, :pl]
+        V2[0, b, :pl] = V[0, b, :pl]
+        K2[0, b, pl:pl + C] = kr
+        V2[0, b, pl:pl + C] = y @ g["layers.0.v.w"].T
+    ref = oracle.velocity(ex, noise, t, K2, V2, [p + C for p in plens])
+    np.testing.assert_allclose(v, ref, rtol=1e-11, atol=1e-12)
+
+
+def test_correction_tokens_constant_field_committed_and_influence():
+    wl, w, K, V, noise = _small()
+    corr = _corr()
+    ex = oracle.Expert(SMALL, w)
+    com = np.random.default_rng(8).normal(size=(2, 1, 3))
+    a = oracle.denoise(ex, noise, K, V, [6, 6], 3, committed=com, n_fixed=1, corr=corr)
+    assert np.array_equal(a[:, :1], com)
+    b = oracle.denoise(ex, noise, K, V, [6, 6], 3, committed=com, n_fixed=1, corr=corr * 1.5)
+    assert np.abs(a - b).max() > 1e-3
+    # no correction tokens at all is the expert without them
+    e = oracle.denoise(ex, noise, K, V, [6, 6], 3, corr=np.zeros((2, 0, SMALL.width)))
+    assert np.array_equal(e, oracle.denoise(ex, noise, K, V, [6, 6], 3))
+    # the velocity is read from action tokens only: a constant field stays exact
+    w["action_out.w"][:] = 0.0
+    c = np.array([0.5, -0.25, 1.0], np.float32)
+    w["action_out.b"][:] = c
+    ex = oracle.Expert(SMALL, w)
+    out = oracle.denoise(ex, noise, K, V, [6, 6], 4, corr=corr)
+    np.testing.assert_allclose(out, noise - c.astype(np.float64), rtol=0, atol=1e-12)
 
 
 def test_workload_shapes_match_paper_table():
