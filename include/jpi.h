@@ -38,8 +38,8 @@
  *     Work is enqueued asynchronously; synchronise the stream (or call
  *     jpi_sync) before reading outputs on the host.
  *   - A context is not thread-safe; use one context per stream.
- *   - Matrices are row-major [out][in] (y = x W^T); activation rows are
- *     m = b*horizon + i.  bf16 data is passed as raw 16-bit patterns.
+ *   - Matrices are row-major [out][in] (y = x W^T); action chunks are
+ *     [batch][horizon][A].  bf16 data is passed as raw 16-bit patterns.
  */
 #ifndef JPI_H_
 #define JPI_H_
@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define JPI_ABI_VERSION 1
+#define JPI_ABI_VERSION 2
 
 typedef enum {
   JPI_OK = 0,
@@ -79,6 +79,7 @@ typedef struct {
   jpi_dtype dtype;  /* storage type of matrices, prefix KV and activations */
   float rms_eps;    /* 1e-6 */
   float rope_base;  /* 1e4 */
+  int max_corr;     /* correction tokens per rollout, upper bound (0: none; at most 64) */
 } jpi_config;
 
 typedef struct jpi_ctx jpi_ctx;
@@ -144,12 +145,25 @@ jpi_status jpi_prefix_buffers(jpi_ctx* ctx, void** k_out, void** v_out);
 jpi_status jpi_bind_prefix(jpi_ctx* ctx, const void* k, const void* v, const int32_t* prefix_len_host,
                            int batch, int prefix, void* stream);
 
-/* Bind the per-call state besides the prefix: n_fixed committed action rows
- * (Algorithm 1: actions already committed for execution while the next chunk
- * is inferred).  committed_dev: device [batch][n_fixed][A] fp32 (may be NULL
- * if n_fixed == 0), copied stream-ordered.  n_fixed in [0, horizon).  The
- * correction tokens (corr_tokens, n_corr) are reserved; n_corr must be 0
- * (JPI_ERR_UNSUPPORTED otherwise).  Must follow jpi_bind_prefix (batch). */
+/* Bind the per-call state besides the prefix (Algorithm 1: f_act(h, B_kv)).
+ *   - n_fixed committed action rows: actions already committed for execution
+ *     while the next chunk is inferred.  committed_dev: device
+ *     [batch][n_fixed][A] fp32 (may be NULL if n_fixed == 0).  n_fixed in
+ *     [0, horizon).
+ *   - n_corr correction tokens h (Section "Foresight-Aligned Asynchronous
+ *     Correction": the correction item the future correction module hands to
+ *     the action expert).  corr_tokens: device [batch][n_corr][W] fp32 (may
+ *     be NULL if n_corr == 0), n_corr in [0, max_corr].  They enter every
+ *     step as extra suffix tokens ahead of the action tokens: token j at RoPE
+ *     position prefix_len + j, action token i at prefix_len + n_corr + i; they
+ *     skip the action in-projection, go through every layer with the step's
+ *     modulation, attend to and are attended by all suffix tokens, restart
+ *     from the given values at every step and are never Euler-updated.
+ * Both are copied stream-ordered into context buffers.  Must follow
+ * jpi_bind_prefix, which sets the batch (binding a prefix with a different
+ * batch clears both).  With n_corr > 0 the multi-kernel path runs (the
+ * single-launch kernel covers the action rows alone).  Errors: JPI_ERR_ARG
+ * (NULL ctx or data, counts out of range), JPI_ERR_STATE (no prefix bound). */
 jpi_status jpi_bind_state(jpi_ctx* ctx, const float* committed_dev, int n_fixed, const void* corr_tokens,
                           int n_corr, void* stream);
 
@@ -157,7 +171,7 @@ jpi_status jpi_bind_state(jpi_ctx* ctx, const float* committed_dev, int n_fixed,
  * take the committed values), then n_steps Euler steps of the velocity field
  * run, and x is written to actions_dev.  noise_dev, actions_dev: device
  * [batch][H][A] fp32 (may alias).  Stream-ordered and asynchronous.  The first
- * call per (batch, prefix, n_steps, n_fixed, prefix lengths) builds the
+ * call per (batch, prefix, n_steps, n_fixed, n_corr) builds the
  * modulation tables for the N step times and captures the N-step loop into a
  * HIP graph; later calls replay it.  Errors: JPI_ERR_STATE (weights not
  * finalized or no prefix bound), JPI_ERR_ARG (NULL, n_steps < 1). */

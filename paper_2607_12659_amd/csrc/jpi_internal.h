@@ -2,6 +2,8 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include <vector>
 #include <stdint.h>
 
 #include <hip/hip_ext.h>
@@ -67,13 +69,15 @@ struct RowLaunch {
   // final_step only: action-out projection and Euler update
   const void* w_out;     // [A][W]
   const float* b_out;    // [A]
-  float* x;              // [M][A]
+  float* x;              // [B][horizon][A]
   int A, horizon, n_fixed;
+  int n_lead;            // correction rows ahead of each rollout's action rows (rows m = b*(n_lead+horizon)+r)
   float dt;
 };
+// corr: [B][n_lead][W] correction tokens (rows r < n_lead of each rollout), may be NULL when n_lead == 0
 hipError_t launch_inproj_norm(jpi_dtype dt, const float* x, const void* w_in, const float* b_in, float* h,
                               const float* scale, const float* shift, void* y, int M, int W, int A, float eps,
-                              hipStream_t s);
+                              const float* corr, int n_lead, int horizon, hipStream_t s);
 hipError_t launch_resid_norm(jpi_dtype dt, const RowLaunch& r, bool final_step, hipStream_t s);
 
 struct AttnLaunch {
@@ -166,12 +170,50 @@ struct AePrefixTarget {
   int vpt_ld;           // Ppad
   int* prefix_len;      // device [Bmax]
   float2* rope_tab;     // device [Bmax][H][Dh/2]: the expert's own rows' positions
-  int H;                // the expert's horizon
+  int H;                // suffix rows per rollout the rope table covers (correction tokens + horizon)
   float rope_base;
 };
 jpi_status ae_prefix_target(jpi_ctx* c, int L, int Dh, jpi_dtype dt, int batch, int prefix, AePrefixTarget* t,
                             const char** why);
-jpi_status ae_prefix_bound(jpi_ctx* c, int batch, int prefix);
+jpi_status ae_prefix_bound(jpi_ctx* c, int batch, int prefix, int rope_rows);
+
+// ---- pre-norm decoder blocks with constant modulation (VLM prefill, correction module)
+// Packed layer (bf16, the expert's layout): [q heads | k | v] rows (q and k in
+// RoPE pack order) | O [W][nH Dh] | gate/up rows interleaved in 32-row groups | Down [W][F].
+enum BlockMatrix { BM_Q, BM_K, BM_V, BM_GATE, BM_UP };
+int block_pack_row(BlockMatrix kind, int r, int n_heads, int Dh);  // packed row of source row r
+// dst row map[r] <- row r of data (host or device), then synchronise s
+hipError_t upload_rows(void* dst, const std::vector<int>& map, int row_bytes, const void* data, bool is_device,
+                       hipStream_t s);
+struct BlockLaunch {
+  int B, H, W, nH, Dh, F, n_cu;  // B rollouts of H rows each
+  const char* w;                 // packed layer
+  size_t off_o, off_gu, off_d;   // element offsets inside it
+  float* h;                      // [M][W] residual stream, updated in place
+  void* y;                       // [M][W] bf16: in the attention norm of h, out next_norm of the result
+  void *q, *o, *z;               // [M][nH Dh], [M][nH Dh], [M][F] bf16 scratch
+  float* partial;                // [max(s_o, s_d)][M][W]
+  int s_o, s_d;                  // split-K of the O and Down projections
+  float* opart;                  // attention scratch
+  void* ks;                      // own keys (rotated), rollout b at ks + b * ks_bstride
+  int64_t ks_bstride;            // 0 means H * Dh
+  void* vst;                     // own values transposed [B][Dh][vst_ld]
+  int vst_ld;
+  const void *kp, *vpt;          // earlier keys [B][..][Dh] and values transposed [B][Dh][vpt_dstride]
+  int64_t kp_bstride, vpt_bstride;
+  int vpt_dstride;
+  const int* prefix_len;         // device [B]: earlier keys each row sees
+  int P;                         // bound on prefix_len
+  const float2* rope;            // [B][H][Dh/2] (an identity table for no rotation)
+  const float *mlp_norm, *next_norm, *ones, *zeros;
+  float eps;
+};
+hipError_t enqueue_block(const BlockLaunch& b, hipStream_t s);
+hipError_t launch_norm_rows(const float* h, const float* w, void* y, int M, int W, float eps, hipStream_t s);
+hipError_t launch_fill_i32(int* p, int n, int v, hipStream_t s);
+hipError_t launch_fill_f32(float* p, int n, float v, hipStream_t s);
+hipError_t launch_identity_rope(float2* tab, int n, hipStream_t s);
+hipError_t launch_bcast_rows(const float* src, float* dst, int M, int period, int W, hipStream_t s);
 
 hipError_t launch_time_embed(const float* t, float* emb, int n, int W, hipStream_t s);
 // out[m][n] = act(sum_k in[m][k] w[n][k] + b[n]), fp64 accumulation; act 0 = none, 1 = swish

@@ -30,6 +30,10 @@ __device__ __forceinline__ void epilogue_pair(const EpiParams& ep, float* out_f3
                                               float lo, float hi) {
   if (row >= M) return;
   const int col_hi = col_lo + 16;
+  // packed 32-column groups never straddle N (a multiple of 32 for these epilogues)
+  if constexpr (EPI != EPI_STORE_F32) {
+    if (col_lo >= N) return;
+  }
   if constexpr (EPI == EPI_STORE_F32) {
     if (col_lo < N) out_f32[(size_t)row * N + col_lo] = lo;
     if (col_hi < N) out_f32[(size_t)row * N + col_hi] = hi;
@@ -448,10 +452,14 @@ hipError_t launch_sum_slices(const float* P, float* C, int S, size_t MN, hipStre
 // ===========================================================================
 // Row kernels (one workgroup of 256 threads per activation row m).
 //
-// k_inproj_norm:  h = x W_in^T + b_in;  y = adaRMSNorm(h; scale, shift)
+// Each rollout's sequence is n_lead correction rows followed by `horizon`
+// action rows (m = b * (n_lead + horizon) + r); the correction rows carry
+// given tokens of the expert's width and produce no velocity.
+// k_inproj_norm:  h = x W_in^T + b_in (action rows) or the correction token;
+//                 y = adaRMSNorm(h; scale, shift)
 // k_resid_norm:   h += gate * sum_z P[z][m];  y = adaRMSNorm(h; scale, shift)
-//   FINAL variant: v = adaRMSNorm(h; s_f, b_f) W_out^T + b_out and
-//                  x[m] += dt * v for rows i >= n_fixed
+//   FINAL variant (action rows only): v = adaRMSNorm(h; s_f, b_f) W_out^T + b_out
+//                  and x[b][i] += dt * v for action rows i >= n_fixed
 // adaRMSNorm(h) = h / sqrt(mean(h^2) + eps) * (1 + scale) + shift.
 // ===========================================================================
 constexpr int ROW_MAX_W = 4096;
@@ -467,19 +475,30 @@ template <typename T>
 __global__ __launch_bounds__(256) void k_inproj_norm(const float* __restrict__ x, const T* __restrict__ w_in,
                                                      const float* __restrict__ b_in, float* __restrict__ h,
                                                      const float* __restrict__ scale, const float* __restrict__ shift,
-                                                     T* __restrict__ y, int W, int A, float eps) {
+                                                     T* __restrict__ y, int W, int A, float eps,
+                                                     const float* __restrict__ corr, int n_lead, int horizon) {
   __shared__ float hs[ROW_MAX_W];
   __shared__ float xs[256];
   __shared__ float red[4];
-  const int m = blockIdx.x;
-  for (int a = threadIdx.x; a < A; a += 256) xs[a] = x[(size_t)m * A + a];
-  __syncthreads();
-  for (int n = threadIdx.x; n < W; n += 256) {
-    float acc = 0.f;
-    for (int a = 0; a < A; ++a) acc = fmaf(xs[a], static_cast<float>(w_in[(size_t)n * A + a]), acc);
-    const float v = acc + b_in[n];
-    hs[n] = v;
-    h[(size_t)m * W + n] = v;
+  const int m = blockIdx.x, S = n_lead + horizon, b = m / S, i = m % S;
+  if (i < n_lead) {
+    const float* cr = corr + ((size_t)b * n_lead + i) * W;
+    for (int n = threadIdx.x; n < W; n += 256) {
+      const float v = cr[n];
+      hs[n] = v;
+      h[(size_t)m * W + n] = v;
+    }
+  } else {
+    const float* xr = x + ((size_t)b * horizon + (i - n_lead)) * A;
+    for (int a = threadIdx.x; a < A; a += 256) xs[a] = xr[a];
+    __syncthreads();
+    for (int n = threadIdx.x; n < W; n += 256) {
+      float acc = 0.f;
+      for (int a = 0; a < A; ++a) acc = fmaf(xs[a], static_cast<float>(w_in[(size_t)n * A + a]), acc);
+      const float v = acc + b_in[n];
+      hs[n] = v;
+      h[(size_t)m * W + n] = v;
+    }
   }
   __syncthreads();
   const float r = row_rstd(hs, W, eps, red);
@@ -497,6 +516,10 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
   __shared__ float dots[4][ROW_MAX_A];
   const int m = blockIdx.x, W = r.W, S = r.S;
   const size_t MW = (size_t)r.M * W;
+  // the last layer's correction rows feed nothing (the next step restarts them)
+  if constexpr (FINAL) {
+    if (m % (r.n_lead + r.horizon) < r.n_lead) return;
+  }
   float* hr = r.h + (size_t)m * W;
   const float* pr = r.part + (size_t)m * W;
   // four columns per thread per pass; all split-K slices loaded before summing
@@ -557,30 +580,33 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
       }
     }
     __syncthreads();
-    const int i = m % r.horizon;
+    const int seq = r.n_lead + r.horizon, b = m / seq, i = m % seq - r.n_lead;
     if (threadIdx.x < r.A && i >= r.n_fixed) {
       const int a = threadIdx.x;
       const float v = ((dots[0][a] + dots[1][a]) + dots[2][a]) + dots[3][a] + r.b_out[a];
-      r.x[(size_t)m * r.A + a] += r.dt * v;
+      r.x[((size_t)b * r.horizon + i) * r.A + a] += r.dt * v;
     }
   }
 }
 
 hipError_t launch_inproj_norm(jpi_dtype dt, const float* x, const void* w_in, const float* b_in, float* h,
                               const float* scale, const float* shift, void* y, int M, int W, int A, float eps,
-                              hipStream_t s) {
-  if (W > ROW_MAX_W || A > 256) return hipErrorInvalidValue;
+                              const float* corr, int n_lead, int horizon, hipStream_t s) {
+  if (W > ROW_MAX_W || A > 256 || horizon < 1 || n_lead < 0 || (n_lead > 0 && !corr) || M % (n_lead + horizon))
+    return hipErrorInvalidValue;
   if (dt == JPI_BF16)
     hipLaunchKernelGGL(k_inproj_norm<bf16>, dim3(M), dim3(256), 0, s, x, (const bf16*)w_in, b_in, h, scale, shift,
-                       (bf16*)y, W, A, eps);
+                       (bf16*)y, W, A, eps, corr, n_lead, horizon);
   else
     hipLaunchKernelGGL(k_inproj_norm<float>, dim3(M), dim3(256), 0, s, x, (const float*)w_in, b_in, h, scale, shift,
-                       (float*)y, W, A, eps);
+                       (float*)y, W, A, eps, corr, n_lead, horizon);
   return hipGetLastError();
 }
 
 hipError_t launch_resid_norm(jpi_dtype dt, const RowLaunch& r, bool final_step, hipStream_t s) {
-  if (r.W > ROW_MAX_W || r.S > ROW_MAX_S || r.S < 1 || (final_step && r.A > ROW_MAX_A)) return hipErrorInvalidValue;
+  if (r.W > ROW_MAX_W || r.S > ROW_MAX_S || r.S < 1) return hipErrorInvalidValue;
+  if (final_step && (r.A > ROW_MAX_A || r.horizon < 1 || r.n_lead < 0 || r.M % (r.n_lead + r.horizon)))
+    return hipErrorInvalidValue;
   if (dt == JPI_BF16) {
     if (final_step) hipLaunchKernelGGL((k_resid_norm<bf16, true>), dim3(r.M), dim3(256), 0, s, r);
     else hipLaunchKernelGGL((k_resid_norm<bf16, false>), dim3(r.M), dim3(256), 0, s, r);

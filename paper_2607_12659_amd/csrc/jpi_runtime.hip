@@ -49,11 +49,11 @@ bool kind_is_matrix(int k) {
 }
 
 struct GraphKey {
-  int batch, prefix, n_steps, n_fixed;
+  int batch, prefix, n_steps, n_fixed, n_corr;
   bool persist;  // the single-launch path and the multi-kernel path capture different graphs
   bool operator<(const GraphKey& o) const {
-    return std::tie(batch, prefix, n_steps, n_fixed, persist) <
-           std::tie(o.batch, o.prefix, o.n_steps, o.n_fixed, o.persist);
+    return std::tie(batch, prefix, n_steps, n_fixed, n_corr, persist) <
+           std::tie(o.batch, o.prefix, o.n_steps, o.n_fixed, o.n_corr, o.persist);
   }
 };
 
@@ -73,6 +73,7 @@ struct jpi_ctx {
   int device = 0, n_cu = 0;
   std::string err;
   int L, W, nH, Dh, F, A, H, Bmax, Pmax, Mmax;
+  int Cmax;  // correction tokens per rollout, upper bound
   jpi_dtype dt;
   size_t esz;
   int R;  // modulation rows (6L+2)W
@@ -91,9 +92,12 @@ struct jpi_ctx {
   int* h_prefix_len = nullptr;  // pinned staging
   int batch = 0, prefix = 0;
   bool prefix_bound = false;
-  float2* rope_tab = nullptr;
+  float2* rope_tab = nullptr;  // [batch][n_corr + H][Dh/2] at positions prefix_len + r
+  int rope_rows = 0;           // suffix rows per rollout the table was built for
   float* committed = nullptr;
   int n_fixed = 0;
+  float* corr = nullptr;       // [Bmax][Cmax][W] correction tokens
+  int n_corr = 0;
   // activations
   float *x = nullptr, *h = nullptr;
   void *y = nullptr, *q = nullptr, *ks = nullptr, *vst = nullptr, *o = nullptr, *z = nullptr;
@@ -261,7 +265,7 @@ jpi_status jpi_destroy(jpi_ctx* c) {
   drop_tables(c);
   drop_events(c);
   void* bufs[] = {c->w_layers, c->w_in, c->w_t0, c->w_t1, c->w_mod, c->w_out, c->b_in, c->b_t0, c->b_t1, c->b_mod,
-                  c->b_out, c->kp, c->vp, c->vpt, c->d_prefix_len, c->rope_tab, c->committed, c->x, c->h, c->y, c->q, c->ks,
+                  c->b_out, c->kp, c->vp, c->vpt, c->d_prefix_len, c->rope_tab, c->committed, c->corr, c->x, c->h, c->y, c->q, c->ks,
                   c->vst, c->o, c->z, c->partial, c->opart, c->pflags, c->perr, c->w_frag, c->ysw, c->osw,
                   c->zsw, c->qsw};
   for (void* p : bufs)
@@ -280,6 +284,8 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   if (g.n_layers < 1 || g.width < 1 || g.n_heads < 1 || g.n_kv_heads < 1 || g.head_dim < 1 || g.mlp_dim < 1 ||
       g.action_dim < 1 || g.horizon < 1 || g.max_batch < 1 || g.max_prefix < 0)
     return fail(nullptr, JPI_ERR_ARG, "jpi_create: every dimension must be positive");
+  if (g.max_corr < 0 || g.max_corr > 64) return fail(nullptr, JPI_ERR_ARG, "jpi_create: max_corr outside [0, 64]");
+  const int seq_max = g.horizon + g.max_corr;  // suffix rows per rollout
   if (g.n_kv_heads != 1 || g.n_heads % g.n_kv_heads != 0)
     return fail(nullptr, JPI_ERR_ARG, "jpi_create: this version implements exactly one shared KV head");
   if (g.head_dim != 64 && g.head_dim != 128 && g.head_dim != 256)
@@ -289,11 +295,11 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   if (g.dtype != JPI_F32 && g.dtype != JPI_BF16) return fail(nullptr, JPI_ERR_ARG, "jpi_create: bad dtype");
   if (!(g.rms_eps > 0.f) || !(g.rope_base > 1.f))
     return fail(nullptr, JPI_ERR_ARG, "jpi_create: rms_eps must be > 0 and rope_base > 1");
-  if ((long long)g.max_batch * g.horizon > (1 << 20))
-    return fail(nullptr, JPI_ERR_ARG, "jpi_create: max_batch*horizon too large");
-  if (g.max_prefix > attn_max_prefix(g.dtype, g.horizon))
+  if ((long long)g.max_batch * seq_max > (1 << 20))
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: max_batch*(horizon+max_corr) too large");
+  if (g.max_prefix > attn_max_prefix(g.dtype, seq_max))
     return fail(nullptr, JPI_ERR_ARG, "jpi_create: max_prefix above " +
-                                          std::to_string(attn_max_prefix(g.dtype, g.horizon)));
+                                          std::to_string(attn_max_prefix(g.dtype, seq_max)));
   if (g.action_dim > 64) return fail(nullptr, JPI_ERR_ARG, "jpi_create: action_dim above 64");
   if (g.width > 4096) return fail(nullptr, JPI_ERR_ARG, "jpi_create: width above 4096");
 
@@ -314,7 +320,8 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   c->H = g.horizon;
   c->Bmax = g.max_batch;
   c->Pmax = g.max_prefix;
-  c->Mmax = g.max_batch * g.horizon;
+  c->Cmax = g.max_corr;
+  c->Mmax = g.max_batch * seq_max;
   c->dt = g.dtype;
   c->esz = g.dtype == JPI_BF16 ? 2 : 4;
   c->R = (6 * c->L + 2) * c->W;
@@ -361,17 +368,18 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   ALLOC(c->vp, kv_elems * es);
   // room for the action keys after the longest prefix (the single-launch
   // path stores the action rows' V there), rounded to 16-byte rows
-  c->Ppad = (c->Pmax + c->H + 7) / 8 * 8;
+  c->Ppad = (c->Pmax + seq_max + 7) / 8 * 8;
   ALLOC(c->vpt, (size_t)c->L * c->Bmax * (size_t)c->Ppad * Dh * es);
   ALLOC(c->d_prefix_len, c->Bmax * 4);
   ALLOC(c->rope_tab, M * (Dh / 2) * sizeof(float2));
   ALLOC(c->committed, M * A * 4);
+  ALLOC(c->corr, std::max<size_t>(1, (size_t)c->Bmax * c->Cmax * W) * 4);
   ALLOC(c->x, M * A * 4);
   ALLOC(c->h, M * W * 4);
   ALLOC(c->y, M * W * es);
   ALLOC(c->q, M * nH * Dh * es);
   ALLOC(c->ks, M * Dh * es);
-  ALLOC(c->vst, (size_t)c->Bmax * Dh * ((c->H + 7) / 8 * 8) * es);  // rows padded to 8 elements
+  ALLOC(c->vst, (size_t)c->Bmax * Dh * ((seq_max + 7) / 8 * 8) * es);  // rows padded to 8 elements
   ALLOC(c->o, M * nH * Dh * es);
   ALLOC(c->z, M * F * es);
   ALLOC(c->pflags, (size_t)persist_flag_words() * sizeof(unsigned));
@@ -561,8 +569,9 @@ jpi_status jpi_bind_prefix(jpi_ctx* c, const void* k, const void* v, const int32
   }
   memcpy(c->h_prefix_len, lens.data(), batch * sizeof(int));
   HIPCHK(c, hipMemcpyAsync(c->d_prefix_len, c->h_prefix_len, batch * sizeof(int), hipMemcpyHostToDevice, s));
-  HIPCHK(c, launch_rope_table(c->d_prefix_len, c->rope_tab, batch, c->H, c->Dh, c->cfg.rope_base, s));
-  if (c->batch != batch) c->n_fixed = 0;  // committed rows were bound for another batch
+  if (c->batch != batch) c->n_fixed = c->n_corr = 0;  // state rows were bound for another batch
+  HIPCHK(c, launch_rope_table(c->d_prefix_len, c->rope_tab, batch, c->H + c->n_corr, c->Dh, c->cfg.rope_base, s));
+  c->rope_rows = c->H + c->n_corr;
   c->batch = batch;
   c->prefix = prefix;
   c->prefix_bound = true;
@@ -571,18 +580,24 @@ jpi_status jpi_bind_prefix(jpi_ctx* c, const void* k, const void* v, const int32
 
 jpi_status jpi_bind_state(jpi_ctx* c, const float* committed_dev, int n_fixed, const void* corr_tokens, int n_corr,
                           void* stream) {
-  (void)corr_tokens;
   if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_bind_state: ctx is NULL");
-  if (n_corr != 0) return fail(c, JPI_ERR_UNSUPPORTED, "jpi_bind_state: correction tokens are not supported yet");
   if (!c->prefix_bound) return fail(c, JPI_ERR_STATE, "jpi_bind_state: bind the prefix first (it sets the batch)");
   if (n_fixed < 0 || n_fixed >= c->H)
     return fail(c, JPI_ERR_ARG, "jpi_bind_state: n_fixed must be in [0, horizon)");
   if (n_fixed > 0 && !committed_dev) return fail(c, JPI_ERR_ARG, "jpi_bind_state: committed is NULL");
+  if (n_corr < 0 || n_corr > c->Cmax)
+    return fail(c, JPI_ERR_ARG, "jpi_bind_state: n_corr must be in [0, max_corr=" + std::to_string(c->Cmax) + "]");
+  if (n_corr > 0 && !corr_tokens) return fail(c, JPI_ERR_ARG, "jpi_bind_state: corr_tokens is NULL");
   HIPCHK(c, hipSetDevice(c->device));
+  hipStream_t s = (hipStream_t)stream;
   if (n_fixed > 0)
     HIPCHK(c, hipMemcpyAsync(c->committed, committed_dev, (size_t)c->batch * n_fixed * c->A * sizeof(float),
-                             hipMemcpyDeviceToDevice, (hipStream_t)stream));
+                             hipMemcpyDeviceToDevice, s));
+  if (n_corr > 0)
+    HIPCHK(c, hipMemcpyAsync(c->corr, corr_tokens, (size_t)c->batch * n_corr * c->W * sizeof(float),
+                             hipMemcpyDeviceToDevice, s));
   c->n_fixed = n_fixed;
+  c->n_corr = n_corr;
   return JPI_OK;
 }
 
@@ -629,6 +644,7 @@ struct StepGemms {
 bool use_persist(jpi_ctx* c, int batch) {
   const char* e = getenv("JPI_PERSIST");
   if (e && e[0] == '0') return false;
+  if (c->n_corr > 0) return false;  // the single-launch kernel has action rows only
   if (!persist_supported(c->dt, batch * c->H, c->W, c->nH, c->Dh, c->F, c->H, c->A, c->Pmax)) return false;
   if (c->n_cu > persist_max_grid()) return false;
   if (c->persist_occ < 0) {
@@ -644,7 +660,7 @@ bool use_persist(jpi_ctx* c, int batch) {
 
 StepGemms plan_gemms(jpi_ctx* c, int batch) {
   StepGemms p;
-  p.M = batch * c->H;
+  p.M = batch * (c->H + c->n_corr);
   p.persist = use_persist(c, batch);
   if (p.persist) {
     p.s_o = persist_pick_split(c->W / 32, c->nH * c->Dh, c->n_cu);
@@ -668,8 +684,9 @@ jpi_status ensure_scratch(jpi_ctx* c, int batch, int prefix) {
     c->partial_cap = need;
     changed = true;
   }
-  const size_t nch = p.persist ? (size_t)persist_chunks(prefix, c->H) : (size_t)attn_n_chunks(c->dt, prefix, c->H);
-  const size_t attn = (size_t)batch * c->nH * nch * c->H * (c->Dh + 2);
+  const int S = c->H + c->n_corr;
+  const size_t nch = p.persist ? (size_t)persist_chunks(prefix, S) : (size_t)attn_n_chunks(c->dt, prefix, S);
+  const size_t attn = (size_t)batch * c->nH * nch * S * (c->Dh + 2);
   if (attn > c->attn_cap) {
     if (c->opart) (void)hipFree(c->opart);
     c->opart = nullptr;
@@ -721,11 +738,12 @@ jpi_status ensure_frag(jpi_ctx* c, hipStream_t s) {
 
 // Enqueue the whole N-step loop on stream s (eagerly or under capture).
 hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_t s) {
-  const int batch = c->batch, prefix = c->prefix, H = c->H;
+  const int batch = c->batch, prefix = c->prefix, H = c->H, C = c->n_corr;
+  const int S = C + H;  // suffix rows per rollout: correction tokens, then action tokens
   const StepGemms p = plan_gemms(c, batch);
   const int M = p.M, W = c->W, Dh = c->Dh, nH = c->nH, F = c->F, L = c->L;
   const size_t es = c->esz;
-  const int nch = attn_n_chunks(c->dt, prefix, H);
+  const int nch = attn_n_chunks(c->dt, prefix, S);
   const float eps = c->cfg.rms_eps;
   const float dt_step = -1.0f / (float)n_steps;
   hipError_t e;
@@ -809,7 +827,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
   for (int k = 0; k < n_steps; ++k) {
     const float* tk = table + (size_t)k * c->R;
     const float* fm = tk + (size_t)(6 * L) * W;
-    ENQ(launch_inproj_norm(c->dt, c->x, c->w_in, c->b_in, c->h, tk, tk + W, c->y, M, W, c->A, eps, s));
+    ENQ(launch_inproj_norm(c->dt, c->x, c->w_in, c->b_in, c->h, tk, tk + W, c->y, M, W, c->A, eps, c->corr, C, H, s));
     for (int l = 0; l < L; ++l) {
       const char* lay = (const char*)c->w_layers + (size_t)l * c->layer_elems * es;
       const float* am = tk + (size_t)(2 * l) * 3 * W;
@@ -826,11 +844,11 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       g.ep.q = c->q;
       g.ep.ks = c->ks;
       g.ep.vst = c->vst;
-      g.ep.vst_ld = (H + 7) / 8 * 8;
+      g.ep.vst_ld = (S + 7) / 8 * 8;
       g.ep.rope = c->rope_tab;
       g.ep.n_heads = nH;
       g.ep.head_dim = Dh;
-      g.ep.horizon = H;
+      g.ep.horizon = S;
       timing(JPI_KERNEL_QKV, &g.ev_start, &g.ev_stop);
       g.n_cu = c->n_cu;
       ENQ(launch_gemm(c->dt, g, s));
@@ -839,7 +857,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       a.q = c->q;
       a.ks = c->ks;
       a.vst = c->vst;
-      a.vst_ld = (H + 7) / 8 * 8;
+      a.vst_ld = (S + 7) / 8 * 8;
       a.kp = (const char*)c->kp + (size_t)l * c->Bmax * c->Pmax * Dh * es;
       a.vpt = (const char*)c->vpt + (size_t)l * c->Bmax * c->Ppad * Dh * es;
       a.kp_bstride = (int64_t)c->Pmax * Dh;
@@ -848,12 +866,12 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       a.prefix_len = c->d_prefix_len;
       a.B = batch;
       a.nH = nH;
-      a.H = H;
+      a.H = S;
       a.P = prefix;
       a.Dh = Dh;
       a.opart = c->opart;
-      a.mpart = c->opart + (size_t)batch * nH * nch * H * Dh;
-      a.lpart = a.mpart + (size_t)batch * nH * nch * H;
+      a.mpart = c->opart + (size_t)batch * nH * nch * S * Dh;
+      a.lpart = a.mpart + (size_t)batch * nH * nch * S;
       a.out = c->o;
       a.out_f32 = 0;
       a.n_cu = c->n_cu;
@@ -926,6 +944,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
         r.x = c->x;
         r.A = c->A;
         r.horizon = H;
+        r.n_lead = C;
         r.n_fixed = c->n_fixed;
         r.dt = dt_step;
       }
@@ -958,10 +977,14 @@ jpi_status jpi_denoise(jpi_ctx* c, const float* noise_dev, int n_steps, float* a
   TRY(ensure_scratch(c, c->batch, c->prefix));
   if (use_persist(c, c->batch)) TRY(ensure_frag(c, s));
   HIPCHK(c, launch_init_x(noise_dev, c->committed, c->x, c->batch, c->H, c->A, c->n_fixed, s));
+  if (c->rope_rows != c->H + c->n_corr) {  // the suffix length changed since the table was built
+    HIPCHK(c, launch_rope_table(c->d_prefix_len, c->rope_tab, c->batch, c->H + c->n_corr, c->Dh, c->cfg.rope_base, s));
+    c->rope_rows = c->H + c->n_corr;
+  }
   if (eager_mode() || c->timed_kind >= 0) {
     HIPCHK(c, enqueue_steps(c, table, n_steps, s));
   } else {
-    const GraphKey key{c->batch, c->prefix, n_steps, c->n_fixed, use_persist(c, c->batch)};
+    const GraphKey key{c->batch, c->prefix, n_steps, c->n_fixed, c->n_corr, use_persist(c, c->batch)};
     auto it = c->graphs.find(key);
     if (it == c->graphs.end()) {
       hipGraph_t graph = nullptr;
@@ -1167,13 +1190,14 @@ jpi_status jpi::ae_prefix_target(jpi_ctx* c, int L, int Dh, jpi_dtype dt, int ba
   t->vpt_lstride = (int64_t)c->Bmax * t->vpt_bstride;
   t->prefix_len = c->d_prefix_len;
   t->rope_tab = c->rope_tab;
-  t->H = c->H;
+  t->H = c->H + c->n_corr;
   t->rope_base = c->cfg.rope_base;
   return JPI_OK;
 }
 
-jpi_status jpi::ae_prefix_bound(jpi_ctx* c, int batch, int prefix) {
-  if (c->batch != batch) c->n_fixed = 0;  // committed rows were bound for another batch
+jpi_status jpi::ae_prefix_bound(jpi_ctx* c, int batch, int prefix, int rope_rows) {
+  if (c->batch != batch) c->n_fixed = c->n_corr = 0;  // state rows were bound for another batch
+  c->rope_rows = rope_rows;  // jpi_denoise rebuilds the table if the suffix length differs
   c->batch = batch;
   c->prefix = prefix;
   c->prefix_bound = true;

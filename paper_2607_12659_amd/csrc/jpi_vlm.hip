@@ -23,47 +23,9 @@ using namespace jpi;
 
 namespace {
 
-// y[m] = bf16(h[m] / rms(h[m]) * (1 + w)), one workgroup per row
-__global__ __launch_bounds__(256) void k_norm_rows(const float* __restrict__ h, const float* __restrict__ w,
-                                                   bf16* __restrict__ y, int W, float eps) {
-  __shared__ float red[4];
-  const float* hr = h + (size_t)blockIdx.x * W;
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < W; i += 256) ss += hr[i] * hr[i];
-  ss = block_sum_256(ss, red);
-  const float r = 1.0f / sqrtf(ss / (float)W + eps);
-  bf16* yr = y + (size_t)blockIdx.x * W;
-  for (int i = threadIdx.x; i < W; i += 256) yr[i] = static_cast<bf16>(hr[i] * r * (1.0f + w[i]));
-}
-
-__global__ void k_fill_i32(int* p, int n, int v) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = v;
-}
-
-__global__ void k_fill_f32(float* p, int n, float v) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = v;
-}
-
-// dst row map[r] <- src row r (row_bytes each, a multiple of 4)
-__global__ void k_scatter(const char* __restrict__ src, char* __restrict__ dst, const int* __restrict__ map,
-                          int row_bytes) {
-  const char* s = src + (size_t)blockIdx.x * row_bytes;
-  char* d = dst + (size_t)map[blockIdx.x] * row_bytes;
-  for (int i = threadIdx.x * 4; i < row_bytes; i += blockDim.x * 4)
-    *reinterpret_cast<int*>(d + i) = *reinterpret_cast<const int*>(s + i);
-}
-
 enum VKind { V_ATTN_NORM, V_Q, V_K, V_V, V_O, V_MLP_NORM, V_GATE, V_UP, V_DOWN, V_NLAYER, V_FINAL_NORM = V_NLAYER };
 const char* vkind_suffix[V_NLAYER + 1] = {"attn_norm.w", "q.w", "k.w", "v.w", "o.w", "mlp_norm.w",
                                           "gate.w", "up.w", "down.w", "final_norm.w"};
-
-// packed row of q / k source row r: RoPE pairs (d, d + Dh/2) in one 32-row group
-int rope_row(int r, int Dh) {
-  const int half = Dh / 2, dd = r % Dh, head = r / Dh, hi = dd >= half ? 1 : 0, d = dd - hi * half;
-  return head * Dh + (d / 16) * 32 + hi * 16 + (d % 16);
-}
 
 }  // namespace
 
@@ -178,9 +140,11 @@ jpi_status jpi_vlm_create(const jpi_vlm_config* cfg, int device, jpi_vlm** out) 
     jpi_vlm_destroy(v);
     return JPI_ERR_OOM;
   }
-  hipLaunchKernelGGL(k_fill_f32, dim3((W + 255) / 256), dim3(256), 0, 0, v->ones, (int)W, 1.0f);
-  hipLaunchKernelGGL(k_fill_f32, dim3((W + 255) / 256), dim3(256), 0, 0, v->zeros, (int)W, 0.0f);
-  hipLaunchKernelGGL(k_fill_i32, dim3((v->Bmax + 255) / 256), dim3(256), 0, 0, v->zero_len, v->Bmax, 0);
+  if (launch_fill_f32(v->ones, (int)W, 1.0f, 0) != hipSuccess || launch_fill_f32(v->zeros, (int)W, 0.0f, 0) != hipSuccess ||
+      launch_fill_i32(v->zero_len, v->Bmax, 0, 0) != hipSuccess) {
+    jpi_vlm_destroy(v);
+    return JPI_ERR_HIP;
+  }
   if (hipDeviceSynchronize() != hipSuccess) {
     jpi_vlm_destroy(v);
     return JPI_ERR_HIP;
@@ -238,34 +202,10 @@ jpi_status jpi_vlm_set_weight(jpi_vlm* v, const char* name, const void* data, in
     // row-permuted copies: q/k rows in RoPE pack order after q heads, v rows
     // natural; gate/up rows interleaved in 32-row groups [gate 16 | up 16]
     char* base = kind == V_GATE || kind == V_UP ? lay + v->off_gu * 2 : lay;
-    const int rows = (int)(n_elems / W);
-    std::vector<int> map(rows);
-    for (int r = 0; r < rows; ++r) {
-      if (kind == V_Q) map[r] = rope_row(r, (int)Dh);
-      else if (kind == V_K) map[r] = (int)(nH * Dh) + rope_row(r, (int)Dh);
-      else if (kind == V_V) map[r] = (int)((nH + 1) * Dh) + r;
-      else map[r] = (r / 16) * 32 + (kind == V_UP ? 16 : 0) + (r % 16);
-    }
-    void *src = const_cast<void*>(data), *tmp = nullptr, *dmap = nullptr;
-    if (hipMalloc(&dmap, rows * sizeof(int)) != hipSuccess) return vfail(v, JPI_ERR_OOM, "jpi_vlm_set_weight: map");
-    if (!is_device && hipMalloc(&tmp, (size_t)n_elems * 2) != hipSuccess) {
-      (void)hipFree(dmap);
-      return vfail(v, JPI_ERR_OOM, "jpi_vlm_set_weight: staging");
-    }
-    hipError_t e = hipSuccess;
-    if (tmp) {
-      e = hipMemcpyAsync(tmp, data, (size_t)n_elems * 2, hipMemcpyHostToDevice, s);
-      src = tmp;
-    }
-    if (e == hipSuccess) e = hipMemcpyAsync(dmap, map.data(), rows * sizeof(int), hipMemcpyHostToDevice, s);
-    if (e == hipSuccess) {
-      hipLaunchKernelGGL(k_scatter, dim3(rows), dim3(256), 0, s, (const char*)src, base, (const int*)dmap,
-                         (int)(W * 2));
-      e = hipGetLastError();
-    }
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    (void)hipFree(dmap);
-    if (tmp) (void)hipFree(tmp);
+    const BlockMatrix bm = kind == V_Q ? BM_Q : kind == V_K ? BM_K : kind == V_V ? BM_V : kind == V_GATE ? BM_GATE : BM_UP;
+    std::vector<int> map((size_t)(n_elems / W));
+    for (size_t r = 0; r < map.size(); ++r) map[r] = block_pack_row(bm, (int)r, (int)nH, (int)Dh);
+    const hipError_t e = upload_rows(base, map, (int)(W * 2), data, is_device != 0, s);
     if (e != hipSuccess) return vfail(v, JPI_ERR_HIP, std::string("jpi_vlm_set_weight: ") + hipGetErrorString(e));
   }
   VCHK(v, hipStreamSynchronize(s));
@@ -305,110 +245,55 @@ jpi_status jpi_vlm_prefill(jpi_vlm* v, const float* emb, int batch, int prefix, 
   const float* nrm = v->norms;
 
   VCHK(v, hipMemcpyAsync(v->h, emb, (size_t)M * W * 4, hipMemcpyDeviceToDevice, s));
-  hipLaunchKernelGGL(k_norm_rows, dim3(M), dim3(256), 0, s, v->h, nrm, (bf16*)v->y, W, eps);
-  VCHK(v, hipGetLastError());
+  VCHK(v, launch_norm_rows(v->h, nrm, v->y, M, W, eps, s));
   VCHK(v, launch_rope_table(v->zero_len, v->rope, batch, prefix, Dh, v->cfg.rope_base, s));
+  BlockLaunch b{};
+  b.B = batch;
+  b.H = prefix;
+  b.W = W;
+  b.nH = nH;
+  b.Dh = Dh;
+  b.F = F;
+  b.n_cu = v->n_cu;
+  b.off_o = v->off_o;
+  b.off_gu = v->off_gu;
+  b.off_d = v->off_d;
+  b.h = v->h;
+  b.y = v->y;
+  b.q = v->q;
+  b.o = v->o;
+  b.z = v->z;
+  b.partial = v->partial;
+  b.s_o = v->s_o;
+  b.s_d = v->s_d;
+  b.opart = v->opart;
+  b.ks_bstride = tg.kp_bstride;
+  b.vst_ld = tg.vpt_ld;
+  b.kp_bstride = tg.kp_bstride;
+  b.vpt_bstride = tg.vpt_bstride;
+  b.vpt_dstride = tg.vpt_ld;
+  b.prefix_len = v->zero_len;  // the prefix tokens are the query rows and their own keys
+  b.P = 0;
+  b.rope = v->rope;
+  b.ones = v->ones;
+  b.zeros = v->zeros;
+  b.eps = eps;
   for (int l = 0; l < L; ++l) {
-    const char* lay = (const char*)v->w_layers + (size_t)l * lay_bytes;
-    void* kl = (char*)tg.kp + (size_t)l * tg.kp_lstride * 2;
-    void* vl = (char*)tg.vpt + (size_t)l * tg.vpt_lstride * 2;
-    GemmLaunch g{};
-    g.A = v->y;
-    g.W = lay;
-    g.M = M;
-    g.N = (nH + 2) * Dh;
-    g.K = W;
-    g.splitk = 1;
-    g.n_cu = v->n_cu;
-    g.epi = EPI_QKV;
-    g.ep.q = v->q;
-    g.ep.ks = kl;
-    g.ep.ks_bstride = tg.kp_bstride;
-    g.ep.vst = vl;
-    g.ep.vst_ld = tg.vpt_ld;
-    g.ep.rope = v->rope;
-    g.ep.n_heads = nH;
-    g.ep.head_dim = Dh;
-    g.ep.horizon = prefix;
-    VCHK(v, launch_gemm(JPI_BF16, g, s));
-    AttnLaunch a{};
-    a.q = v->q;
-    a.ks = kl;
-    a.ks_bstride = tg.kp_bstride;
-    a.vst = vl;
-    a.vst_ld = tg.vpt_ld;
-    a.kp = kl;
-    a.vpt = vl;
-    a.kp_bstride = tg.kp_bstride;
-    a.vpt_bstride = tg.vpt_bstride;
-    a.vpt_dstride = tg.vpt_ld;
-    a.prefix_len = v->zero_len;  // the prefix tokens are the query rows and their own keys
-    a.B = batch;
-    a.nH = nH;
-    a.H = prefix;
-    a.P = 0;
-    a.Dh = Dh;
-    a.opart = v->opart;
-    a.out = v->o;
-    a.out_f32 = 0;
-    a.n_cu = v->n_cu;
-    VCHK(v, launch_attention(JPI_BF16, a, s));
-    g = GemmLaunch{};
-    g.A = v->o;
-    g.W = lay + v->off_o * 2;
-    g.M = M;
-    g.N = W;
-    g.K = nH * Dh;
-    g.splitk = v->s_o;
-    g.n_cu = v->n_cu;
-    g.epi = EPI_STORE_F32;
-    g.ep.out_f32 = v->partial;
-    VCHK(v, launch_gemm(JPI_BF16, g, s));
-    RowLaunch r{};
-    r.part = v->partial;
-    r.S = v->s_o;
-    r.M = M;
-    r.W = W;
-    r.h = v->h;
-    r.gate = v->ones;
-    r.scale = nrm + ((size_t)2 * l + 1) * W;
-    r.shift = v->zeros;
-    r.y = v->y;
-    r.eps = eps;
-    VCHK(v, launch_resid_norm(JPI_BF16, r, false, s));
-    g = GemmLaunch{};
-    g.A = v->y;
-    g.W = lay + v->off_gu * 2;
-    g.M = M;
-    g.N = 2 * F;
-    g.K = W;
-    g.splitk = 1;
-    g.n_cu = v->n_cu;
-    g.epi = EPI_GEGLU;
-    g.ep.z = v->z;
-    g.ep.mlp_dim = F;
-    VCHK(v, launch_gemm(JPI_BF16, g, s));
-    g = GemmLaunch{};
-    g.A = v->z;
-    g.W = lay + v->off_d * 2;
-    g.M = M;
-    g.N = W;
-    g.K = F;
-    g.splitk = v->s_d;
-    g.n_cu = v->n_cu;
-    g.epi = EPI_STORE_F32;
-    g.ep.out_f32 = v->partial;
-    VCHK(v, launch_gemm(JPI_BF16, g, s));
-    r.S = v->s_d;
-    r.scale = nrm + (l + 1 < L ? (size_t)2 * (l + 1) : (size_t)2 * L) * W;  // next layer's norm, else the final one
-    VCHK(v, launch_resid_norm(JPI_BF16, r, false, s));
+    // K (rotated) and V^T go straight into the expert's buffers of layer l
+    b.w = (const char*)v->w_layers + (size_t)l * lay_bytes;
+    b.ks = (char*)tg.kp + (size_t)l * tg.kp_lstride * 2;
+    b.vst = (char*)tg.vpt + (size_t)l * tg.vpt_lstride * 2;
+    b.kp = b.ks;
+    b.vpt = b.vst;
+    b.mlp_norm = nrm + ((size_t)2 * l + 1) * W;
+    b.next_norm = nrm + (l + 1 < L ? (size_t)2 * (l + 1) : (size_t)2 * L) * W;  // next layer's norm, else the final one
+    VCHK(v, enqueue_block(b, s));
   }
   if (hidden_out) VCHK(v, hipMemcpyAsync(hidden_out, v->y, (size_t)M * W * 2, hipMemcpyDeviceToDevice, s));
   // bind: prefix_len = prefix for every rollout; the expert's own rows sit at positions prefix + i
-  hipLaunchKernelGGL(k_fill_i32, dim3((batch + 255) / 256), dim3(256), 0, s, tg.prefix_len, batch, prefix);
-  VCHK(v, hipGetLastError());
+  VCHK(v, launch_fill_i32(tg.prefix_len, batch, prefix, s));
   VCHK(v, launch_rope_table(tg.prefix_len, tg.rope_tab, batch, tg.H, Dh, tg.rope_base, s));
-  return ae_prefix_bound(ae, batch, prefix);
+  return ae_prefix_bound(ae, batch, prefix, tg.H);
 }
 
 const char* jpi_vlm_last_error(const jpi_vlm* v) { return v ? v->err.c_str() : "vlm is NULL"; }

@@ -28,11 +28,11 @@ class ActionExpert:
     """One libjpi context on one GPU."""
 
     def __init__(self, dims, dtype: str, max_batch: int, max_prefix: int, device: int = 0,
-                 rms_eps: float = 1e-6, rope_base: float = 1e4):
+                 rms_eps: float = 1e-6, rope_base: float = 1e4, max_corr: int = 0):
         self.dims, self.dtype, self.device = dims, dtype, device
         cfg = _j.jpi_config(dims.n_layers, dims.width, dims.n_heads, dims.n_kv_heads, dims.head_dim,
                             dims.mlp_dim, dims.action_dim, dims.horizon, max_batch, max_prefix, _dt(dtype),
-                            rms_eps, rope_base)
+                            rms_eps, rope_base, max_corr)
         st, ctx = _j.jpi_create(cfg, device)
         _j.check(st, None)
         self.ctx = ctx
@@ -65,8 +65,11 @@ class ActionExpert:
         self._chk(_j.jpi_bind_prefix(self.ctx, K, V, prefix_len, B, P, stream))
         self.batch = B
 
-    def bind_state(self, committed: torch.Tensor | None, n_fixed: int, stream=None):
-        self._chk(_j.jpi_bind_state(self.ctx, committed, n_fixed, None, 0, stream))
+    def bind_state(self, committed: torch.Tensor | None, n_fixed: int, corr: torch.Tensor | None = None,
+                   stream=None):
+        """committed: device [B][n_fixed][A] fp32; corr: device [B][n_corr][W] fp32 correction tokens."""
+        n_corr = 0 if corr is None else int(corr.shape[1])
+        self._chk(_j.jpi_bind_state(self.ctx, committed, n_fixed, corr, n_corr, stream))
 
     def denoise(self, noise: torch.Tensor, n_steps: int, out: torch.Tensor | None = None, stream=None):
         if out is None:

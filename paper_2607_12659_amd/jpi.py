@@ -22,7 +22,9 @@ EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create",
             "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
             "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
             "jpi_sched_run", "jpi_sched_sim_hooks", "jpi_vlm_create", "jpi_vlm_destroy", "jpi_vlm_set_weight",
-            "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error"]
+            "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error", "jpi_corr_create",
+            "jpi_corr_destroy", "jpi_corr_set_weight", "jpi_corr_finalize_weights", "jpi_corr_compress",
+            "jpi_corr_predict", "jpi_corr_last_error"]
 JPI_KERNEL_NONE, JPI_KERNEL_QKV, JPI_KERNEL_ATTENTION, JPI_KERNEL_OPROJ, JPI_KERNEL_GATEUP, JPI_KERNEL_DOWN, \
     JPI_KERNEL_PERSISTENT = range(-1, 6)
 
@@ -32,7 +34,7 @@ class jpi_config(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int), ("head_dim", ctypes.c_int), ("mlp_dim", ctypes.c_int),
                 ("action_dim", ctypes.c_int), ("horizon", ctypes.c_int), ("max_batch", ctypes.c_int),
                 ("max_prefix", ctypes.c_int), ("dtype", ctypes.c_int), ("rms_eps", ctypes.c_float),
-                ("rope_base", ctypes.c_float)]
+                ("rope_base", ctypes.c_float), ("max_corr", ctypes.c_int)]
 
 
 # include/jpi_vlm.h
@@ -40,6 +42,15 @@ class jpi_vlm_config(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int), ("width", ctypes.c_int), ("n_heads", ctypes.c_int),
                 ("n_kv_heads", ctypes.c_int), ("head_dim", ctypes.c_int), ("mlp_dim", ctypes.c_int),
                 ("max_batch", ctypes.c_int), ("max_prefix", ctypes.c_int), ("dtype", ctypes.c_int),
+                ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float)]
+
+
+# include/jpi_corr.h
+class jpi_corr_config(ctypes.Structure):
+    _fields_ = [("width", ctypes.c_int), ("n_heads", ctypes.c_int), ("n_kv_heads", ctypes.c_int),
+                ("head_dim", ctypes.c_int), ("mlp_dim", ctypes.c_int), ("action_dim", ctypes.c_int),
+                ("vlm_width", ctypes.c_int), ("n_query", ctypes.c_int), ("max_batch", ctypes.c_int),
+                ("max_actions", ctypes.c_int), ("max_vlm_tokens", ctypes.c_int), ("dtype", ctypes.c_int),
                 ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float)]
 
 
@@ -117,6 +128,13 @@ _sig = {
     "jpi_vlm_finalize_weights": (_i, [_vp, _vp]),
     "jpi_vlm_prefill": (_i, [_vp, _vp, _i, _i, _vp, _vp, _vp]),
     "jpi_vlm_last_error": (ctypes.c_char_p, [_vp]),
+    "jpi_corr_create": (_i, [ctypes.POINTER(jpi_corr_config), _i, ctypes.POINTER(_vp)]),
+    "jpi_corr_destroy": (_i, [_vp]),
+    "jpi_corr_set_weight": (_i, [_vp, ctypes.c_char_p, _vp, _i64, _i, _i, _vp]),
+    "jpi_corr_finalize_weights": (_i, [_vp, _vp]),
+    "jpi_corr_compress": (_i, [_vp, _vp, _i, _i, _vp, _vp]),
+    "jpi_corr_predict": (_i, [_vp, _vp, _vp, _i, _i, _vp, _vp, _vp]),
+    "jpi_corr_last_error": (ctypes.c_char_p, [_vp]),
 }
 for _name, (_res, _args) in _sig.items():
     _fn = getattr(_lib, _name)
@@ -266,6 +284,37 @@ def jpi_vlm_prefill(vlm, emb, batch: int, prefix: int, ae_ctx, hidden_out=None, 
 
 def jpi_vlm_last_error(vlm) -> str:
     return _lib.jpi_vlm_last_error(vlm).decode()
+
+
+def jpi_corr_create(cfg: jpi_corr_config, device: int = 0):
+    out = _vp()
+    st = _lib.jpi_corr_create(ctypes.byref(cfg), device, ctypes.byref(out))
+    return st, out
+
+
+def jpi_corr_destroy(m) -> int:
+    return _lib.jpi_corr_destroy(m)
+
+
+def jpi_corr_set_weight(m, name: str, data, n_elems: int, dtype: int, is_device: int, stream=None) -> int:
+    return _lib.jpi_corr_set_weight(m, name.encode(), addr(data), n_elems, dtype, is_device, stream_handle(stream))
+
+
+def jpi_corr_finalize_weights(m, stream=None) -> int:
+    return _lib.jpi_corr_finalize_weights(m, stream_handle(stream))
+
+
+def jpi_corr_compress(m, vlm_state, batch: int, n_tokens: int, state_out, stream=None) -> int:
+    return _lib.jpi_corr_compress(m, addr(vlm_state), batch, n_tokens, addr(state_out), stream_handle(stream))
+
+
+def jpi_corr_predict(m, state, actions, batch: int, n_actions: int, item_out, conf_out, stream=None) -> int:
+    return _lib.jpi_corr_predict(m, addr(state), addr(actions), batch, n_actions, addr(item_out), addr(conf_out),
+                                 stream_handle(stream))
+
+
+def jpi_corr_last_error(m) -> str:
+    return _lib.jpi_corr_last_error(m).decode()
 
 
 class JpiError(RuntimeError):

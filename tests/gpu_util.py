@@ -32,19 +32,21 @@ class Inputs:
         self.prefix_len = [wl.valid_lengths()[b] for b in self.rollouts]
 
 
-def make_expert(wl, weights, max_batch=None, max_prefix=None):
+def make_expert(wl, weights, max_batch=None, max_prefix=None, max_corr=0):
     from paper_2607_12659_amd.expert import ActionExpert
-    ae = ActionExpert(wl.dims, wl.dtype, max_batch or wl.batch, max_prefix if max_prefix is not None else wl.prefix)
+    ae = ActionExpert(wl.dims, wl.dtype, max_batch or wl.batch, max_prefix if max_prefix is not None else wl.prefix,
+                      max_corr=max_corr)
     ae.load_weights(weights)
     return ae
 
 
-def run(ae, K, V, noise, n_steps, prefix_len=None, committed=None, n_fixed=0):
-    """Bind and denoise; returns fp64 host actions."""
+def run(ae, K, V, noise, n_steps, prefix_len=None, committed=None, n_fixed=0, corr=None):
+    """Bind and denoise; returns fp64 host actions.  corr: host [B][n_corr][W] correction tokens."""
     torch = torch_cuda()
     from paper_2607_12659_amd.expert import to_device
     ae.bind_prefix(to_device(K), to_device(V), prefix_len)
-    ae.bind_state(None if committed is None else to_device(np.ascontiguousarray(committed, np.float32)), n_fixed)
+    ae.bind_state(None if committed is None else to_device(np.ascontiguousarray(committed, np.float32)), n_fixed,
+                  None if corr is None else to_device(np.ascontiguousarray(corr, np.float32)))
     out = ae.denoise(to_device(np.ascontiguousarray(noise, np.float32)), n_steps)
     ae.sync()
     torch.cuda.synchronize()
@@ -90,6 +92,44 @@ class Vlm:
 
     def close(self):
         self.jpi.jpi_vlm_destroy(self.ctx)
+
+
+class Corr:
+    """A jpi_corr module loaded with synthetic weights (bf16)."""
+
+    def __init__(self, d, weights, max_batch, max_actions, max_vlm_tokens):
+        torch = torch_cuda()
+        from paper_2607_12659_amd import jpi
+        self.jpi, self.torch, self.d = jpi, torch, d
+        cfg = jpi.jpi_corr_config(width=d.width, n_heads=d.n_heads, n_kv_heads=1, head_dim=d.head_dim,
+                                  mlp_dim=d.mlp_dim, action_dim=d.action_dim, vlm_width=d.vlm_width,
+                                  n_query=d.n_query, max_batch=max_batch, max_actions=max_actions,
+                                  max_vlm_tokens=max_vlm_tokens, dtype=jpi.JPI_BF16, rms_eps=1e-6, rope_base=1e4)
+        st, self.ctx = jpi.jpi_corr_create(cfg)
+        assert st == jpi.JPI_OK, st
+        for name, arr in weights.items():
+            arr = np.ascontiguousarray(arr)
+            dt = jpi.JPI_BF16 if arr.dtype == np.uint16 else jpi.JPI_F32
+            st = jpi.jpi_corr_set_weight(self.ctx, name, arr, arr.size, dt, 0)
+            assert st == jpi.JPI_OK, (name, jpi.jpi_corr_last_error(self.ctx))
+        assert jpi.jpi_corr_finalize_weights(self.ctx) == jpi.JPI_OK, jpi.jpi_corr_last_error(self.ctx)
+
+    def compress(self, vlm_state_dev, batch, n_tokens, out=None):
+        out = out if out is not None else self.torch.empty((batch, self.d.n_query, self.d.width), device="cuda")
+        st = self.jpi.jpi_corr_compress(self.ctx, vlm_state_dev, batch, n_tokens, out)
+        assert st == self.jpi.JPI_OK, self.jpi.jpi_corr_last_error(self.ctx)
+        return out
+
+    def predict(self, state_dev, actions_dev, batch, n_actions, item=None):
+        torch = self.torch
+        item = item if item is not None else torch.empty((batch, self.d.n_query, self.d.width), device="cuda")
+        conf = torch.empty((batch,), device="cuda")
+        st = self.jpi.jpi_corr_predict(self.ctx, state_dev, actions_dev, batch, n_actions, item, conf)
+        assert st == self.jpi.JPI_OK, self.jpi.jpi_corr_last_error(self.ctx)
+        return item, conf
+
+    def close(self):
+        self.jpi.jpi_corr_destroy(self.ctx)
 
 
 def device_view_i16(ptr, shape):
