@@ -256,6 +256,132 @@ def bench_prefill(args, vwl):
     print(json.dumps(result), flush=True)
 
 
+def corr_bytes(cd, wl):
+    """Algorithmic HBM bytes of one VLM-refresh call of the correction module
+    (compress + predict): every weight once, the VLM state, actions, item and
+    confidence."""
+    import numpy as np
+    import synth.correction as synth_corr
+    wbytes = sum(int(np.prod(s)) * (2 if mat else 4) for _, s, mat in synth_corr.corr_weight_specs(cd))
+    io = wl.batch * (wl.vlm_tokens * cd.vlm_width * 2 + wl.n_actions * cd.action_dim * 4
+                     + 2 * cd.n_query * cd.width * 4 + 4)
+    return wbytes + io
+
+
+def bench_corr(args, cwl):
+    """Future correction module (about 40M parameters): one step = the
+    VLM-refresh branch of Algorithm 1 (compress the VLM final-layer state,
+    then predict the correction item and confidence from the committed
+    actions).  Also timed: the skip branch alone (predict from the previous
+    item) and a whole skip iteration (predict, then the pi0.5 expert denoise
+    with the 4-token item and the committed rows)."""
+    import numpy as np
+    import torch
+
+    import synth
+    import synth.correction as synth_corr
+    from paper_2607_12659_amd import jpi
+    from paper_2607_12659_amd.expert import ActionExpert, to_device
+
+    cd = cwl.dims
+    print("bench: workload %s" % cwl.name, file=sys.stderr, flush=True)
+    w = synth_corr.make_corr_weights(cwl)
+    vs = synth_corr.make_vlm_state(cwl)
+    acts = synth_corr.make_actions(cwl)
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    cfg = jpi.jpi_corr_config(width=cd.width, n_heads=cd.n_heads, n_kv_heads=1, head_dim=cd.head_dim,
+                              mlp_dim=cd.mlp_dim, action_dim=cd.action_dim, vlm_width=cd.vlm_width,
+                              n_query=cd.n_query, max_batch=cwl.batch, max_actions=cwl.n_actions,
+                              max_vlm_tokens=cwl.vlm_tokens, dtype=jpi.JPI_BF16, rms_eps=1e-6, rope_base=1e4)
+    st, m = jpi.jpi_corr_create(cfg)
+    jpi.check(st)
+    for name, arr in w.items():
+        arr = np.ascontiguousarray(arr)
+        st = jpi.jpi_corr_set_weight(m, name, arr, arr.size, jpi.JPI_BF16 if arr.dtype == np.uint16 else jpi.JPI_F32, 0)
+        if st != jpi.JPI_OK:
+            raise RuntimeError(jpi.jpi_corr_last_error(m))
+    if jpi.jpi_corr_finalize_weights(m) != jpi.JPI_OK:
+        raise RuntimeError(jpi.jpi_corr_last_error(m))
+    vs_d = to_device(vs)
+    a_d = to_device(acts.astype(np.float32))
+    state = torch.empty((cwl.batch, cd.n_query, cd.width), device="cuda")
+    item = torch.empty_like(state)
+    conf = torch.empty((cwl.batch,), device="cuda")
+
+    def refresh():
+        jpi.check(jpi.jpi_corr_compress(m, vs_d, cwl.batch, cwl.vlm_tokens, state, stream))
+        jpi.check(jpi.jpi_corr_predict(m, state, a_d, cwl.batch, cwl.n_actions, item, conf, stream))
+
+    def skip():
+        jpi.check(jpi.jpi_corr_predict(m, item, a_d, cwl.batch, cwl.n_actions, item, conf, stream))
+
+    def timed(fn, steps, warmup):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    ms = timed(refresh, args.steps, args.warmup)
+    ms_skip = timed(skip, args.steps, args.warmup)
+    # a whole skip iteration: the item goes straight into the expert
+    ewl = synth.WORKLOADS["pi05-b1-committed10"]
+    ae = ActionExpert(ewl.dims, ewl.dtype, 1, ewl.prefix, max_corr=cd.n_query)
+    ae.load_weights(synth.make_weights(ewl))
+    K, V = synth.make_prefix(ewl)
+    ae.bind_prefix(to_device(K), to_device(V), stream=stream)
+    com = to_device(np.ascontiguousarray(synth.make_committed(ewl), np.float32))
+    noise = to_device(np.ascontiguousarray(synth.make_noise(ewl), np.float32))
+    out = torch.empty_like(noise)
+
+    def iteration():
+        skip()
+        ae.bind_state(com, ewl.n_fixed, item, stream=stream)
+        ae.denoise(noise, ewl.n_steps, out=out, stream=stream)
+
+    ms_iter = timed(iteration, max(5, args.steps // 5), 2)
+    ae.sync()
+    finite = bool(torch.isfinite(out).all().item()) and bool(torch.isfinite(conf).all().item())
+    ae.close()
+    jpi.jpi_corr_destroy(m)
+    byts = corr_bytes(cd, cwl)
+    gbs = byts / (ms * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu:
+        import oracle
+        calls, t0 = 0, time.time()
+        while True:
+            oracle.correction.forward(cd, w, acts[:1], vlm_state=vs[:1])
+            calls += 1
+            if time.time() - t0 >= 10.0:
+                break
+        dt = time.time() - t0
+        cpu = {"value": round(calls / dt, 3), "unit": "refresh calls/s", "cores": os.cpu_count(), "kind": "oracle",
+               "sample": "%d repeated fp64 oracle calls (compress + predict, rollout 0), %.1f s" % (calls, dt)}
+    result = {
+        "metric": "future correction module calls/sec (VLM-refresh branch: compress + predict, ~40M parameters)",
+        "value": round(cwl.batch / (ms * 1e-3), 1), "unit": "calls/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": cwl.name, "batch": cwl.batch, "committed_actions": cwl.n_actions,
+                   "vlm_tokens": cwl.vlm_tokens, "width": cd.width, "heads": cd.n_heads, "head_dim": cd.head_dim,
+                   "mlp_dim": cd.mlp_dim, "vlm_width": cd.vlm_width, "n_query": cd.n_query},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "bytes_per_launch": byts,
+                     "avg_launch_us": round(ms * 1e3, 1), "note": "whole call (about 40 launches), not one kernel"},
+        "skip_branch_ms": round(ms_skip, 4),
+        "skip_iteration_ms": round(ms_iter, 4),
+        "cpu_baseline": cpu, "outputs_finite": finite,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -280,12 +406,16 @@ def main():
     import torch
 
     import synth
+    import synth.correction as synth_corr
     import synth.vlm as synth_vlm
     from paper_2607_12659_amd import jpi
     from paper_2607_12659_amd.expert import ActionExpert, to_device
 
     if args.workload in synth_vlm.VLM_WORKLOADS:
         bench_prefill(args, synth_vlm.VLM_WORKLOADS[args.workload])
+        return
+    if args.workload in synth_corr.CORR_WORKLOADS:
+        bench_corr(args, synth_corr.CORR_WORKLOADS[args.workload])
         return
     wl = synth.WORKLOADS[args.workload]
     print("bench: workload %s, generating inputs" % wl.name, file=sys.stderr, flush=True)

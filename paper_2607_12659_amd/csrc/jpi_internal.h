@@ -114,7 +114,9 @@ hipError_t launch_flash(const AttnLaunch& a, int S, hipStream_t s);
 
 // Persistent single-launch denoise (jpi_persist.hip), M <= 64, bf16.
 struct PersistArgs {
-  int L, W, nH, Dh, F, A, H, B, M;
+  int L, W, nH, Dh, F, A, H, B, M;  // H: suffix rows per rollout (n_corr correction rows, then the action rows)
+  int n_corr;               // correction rows ahead of each rollout's action rows
+  const float* corr;        // [B][n_corr][W] correction tokens (rows restart from them every step)
   int C;                    // attention chunks (32 keys) per rollout
   int n_steps, n_fixed, s_o, s_d, R;
   float eps, dt;
@@ -131,7 +133,7 @@ struct PersistArgs {
   int64_t kp_lstride, kp_bstride, vpt_lstride, vpt_bstride, vpt_dstride;
   const int* prefix_len;    // [B]
   const float2* rope;       // [B][H][Dh/2]
-  float* x;                 // [M][A]
+  float* x;                 // [B][H - n_corr][A] action rows
   float* h;                 // [M][W]
   void* y;                  // fragment-ordered [64][W] bf16 (single-launch path)
   void* q;                  // fragment-ordered [B][nH][64][Dh]

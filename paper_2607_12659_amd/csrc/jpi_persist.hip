@@ -665,14 +665,18 @@ __device__ __forceinline__ void store_y(const PersistArgs& a, const float* hrow,
 // In-projection of the owner's row: h = x W_in^T + b_in (x in LDS, W_in
 // [W][A] in global memory; with A % 8 == 0 a thread loads its rows as
 // 16-byte pieces, all in flight), then the step's first adaRMSNorm -> y.
+// A correction row (crow != nullptr) starts from its token instead.
 __device__ __forceinline__ void inproj_row(const PersistArgs& a, const float* scale, const float* shift, float* hrow,
-                                           const float* bin, const float* xs, float* red) {
+                                           const float* bin, const float* xs, float* red, const float* crow) {
   const int W = a.W, A = a.A;
   const bf16* win = reinterpret_cast<const bf16*>(a.w_in);
   f32x4 sc[NGRP], sh[NGRP];
   load_mod(a, scale, shift, sc, sh);
   __syncthreads();  // xs
-  if ((A & 7) == 0) {
+  if (crow) {
+    for (int k4 = 4 * threadIdx.x; k4 < W; k4 += 4 * PT)
+      *reinterpret_cast<f32x4*>(hrow + k4) = *reinterpret_cast<const f32x4*>(crow + k4);
+  } else if ((A & 7) == 0) {
     constexpr int NJ = MAX_W / PT;  // rows per thread
     for (int j0 = 0; j0 < NJ; j0 += 4) {
       if (PT * j0 >= W) break;
@@ -793,7 +797,7 @@ __device__ __forceinline__ void phase_rows(const PersistArgs& a, const RowJob& r
   if (t < A) {
     float v = pp[t];
     for (int s = 1; s < tpa; ++s) v += pp[s * apad + t];
-    if (m % a.H >= a.n_fixed) xreg += a.dt * (v + bo);
+    if (m % a.H - a.n_corr >= a.n_fixed) xreg += a.dt * (v + bo);  // action rows past the committed ones
     xs[t] = xreg;
   }
 }
@@ -860,13 +864,17 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   const int t = threadIdx.x, m = blockIdx.x;
   const int L = a.L, W = a.W, A = a.A;
   const bool owner = m < a.M;
+  // owned row: rollout m / H, suffix row m % H; action index ia < 0 for a correction row
+  const int ia = m % a.H - a.n_corr;
+  const size_t xrow = (size_t)(m / a.H) * (a.H - a.n_corr) + ia;
+  const float* crow = ia < 0 ? a.corr + ((size_t)(m / a.H) * a.n_corr + (m % a.H)) * W : nullptr;
   float xreg = 0.f;
   if (t == 0) s_abort = 0u;
   if (owner) {
     for (int k4 = 4 * t; k4 < W; k4 += 4 * PT)
       *reinterpret_cast<f32x4*>(s_bin + k4) = *reinterpret_cast<const f32x4*>(a.b_in + k4);
-    if (t < A) {
-      xreg = a.x[(size_t)m * A + t];
+    if (t < A && ia >= 0) {
+      xreg = a.x[xrow * A + t];
       s_x[t] = xreg;
     }
   }
@@ -920,11 +928,11 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     }
     if (ki >= 0 && owner) {
       const float* ti = a.table + (size_t)ki * a.R;
-      inproj_row(a, ti, ti + W, s_hrow, s_bin, s_x, reinterpret_cast<float*>(smem));
+      inproj_row(a, ti, ti + W, s_hrow, s_bin, s_x, reinterpret_cast<float*>(smem), crow);
     }
     if (ph < last_phase) phase_done(a, (u32)(ph + 2));
   }
-  if (owner && t < A) a.x[(size_t)m * A + t] = xreg;
+  if (owner && t < A && ia >= 0) a.x[xrow * A + t] = xreg;
 }
 
 // dst = fragment-ordered copy of the row-major bf16 matrix src [R][K]

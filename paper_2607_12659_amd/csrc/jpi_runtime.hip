@@ -644,8 +644,8 @@ struct StepGemms {
 bool use_persist(jpi_ctx* c, int batch) {
   const char* e = getenv("JPI_PERSIST");
   if (e && e[0] == '0') return false;
-  if (c->n_corr > 0) return false;  // the single-launch kernel has action rows only
-  if (!persist_supported(c->dt, batch * c->H, c->W, c->nH, c->Dh, c->F, c->H, c->A, c->Pmax)) return false;
+  const int S = c->H + c->n_corr;  // suffix rows per rollout
+  if (!persist_supported(c->dt, batch * S, c->W, c->nH, c->Dh, c->F, S, c->A, c->Pmax)) return false;
   if (c->n_cu > persist_max_grid()) return false;
   if (c->persist_occ < 0) {
     int occ = 0;
@@ -776,10 +776,12 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     pa.Dh = Dh;
     pa.F = F;
     pa.A = c->A;
-    pa.H = H;
+    pa.H = S;
+    pa.n_corr = C;
+    pa.corr = c->corr;
     pa.B = batch;
     pa.M = M;
-    pa.C = persist_chunks(prefix, H);
+    pa.C = persist_chunks(prefix, S);
     pa.n_steps = n_steps;
     pa.n_fixed = c->n_fixed;
     pa.s_o = p.s_o;
@@ -814,7 +816,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     pa.ks = c->ks;
     pa.vst = c->vst;
     pa.opart = c->opart;
-    pa.ml = c->opart + (size_t)batch * nH * pa.C * H * Dh;
+    pa.ml = c->opart + (size_t)batch * nH * pa.C * S * Dh;
     pa.o = c->osw;
     pa.part = c->partial;
     pa.z = c->zsw;

@@ -53,6 +53,22 @@ def run(ae, K, V, noise, n_steps, prefix_len=None, committed=None, n_fixed=0, co
     return out.cpu().numpy().astype(np.float64)
 
 
+def run_env(ae, env, *args, **kw):
+    """run() with JPI_PERSIST set to env ("0" forces the multi-kernel path, None the default choice)."""
+    old = os.environ.get("JPI_PERSIST")
+    if env is None:
+        os.environ.pop("JPI_PERSIST", None)
+    else:
+        os.environ["JPI_PERSIST"] = env
+    try:
+        return run(ae, *args, **kw)
+    finally:
+        if old is None:
+            os.environ.pop("JPI_PERSIST", None)
+        else:
+            os.environ["JPI_PERSIST"] = old
+
+
 def load_golden(name):
     with open(os.path.join(GOLDEN, name + ".json")) as f:
         meta = json.load(f)

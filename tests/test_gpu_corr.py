@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import load_golden, make_expert, rel_l2_per_rollout, run, torch_cuda
+from gpu_util import load_golden, make_expert, rel_l2_per_rollout, run, run_env, torch_cuda
 from oracle import correction as oc
 from synth import correction as sc
 
@@ -84,8 +84,9 @@ def test_tiny_expert_rejects_too_many_correction_tokens():
 
 def test_pi05_committed10_with_correction_item():
     """The pi0.5 expert at full size with the 4-token correction item and the
-    10 committed rows of one scheduler iteration, against the stored oracle
-    output; the single-launch path (no correction rows) is unchanged after."""
+    10 committed rows of one scheduler iteration (54 suffix rows: the
+    single-launch kernel), against the stored oracle output and the
+    multi-kernel path; the call without the item is unchanged after."""
     torch_cuda()
     wl = synth.WORKLOADS["pi05-b1-committed10"]
     print("case pi05-b1-committed10-corr4", flush=True)
@@ -98,20 +99,52 @@ def test_pi05_committed10_with_correction_item():
     try:
         before = run(ae, K, V, noise, wl.n_steps, committed=com, n_fixed=10)
         got = run(ae, K, V, noise, wl.n_steps, committed=com, n_fixed=10, corr=corr)
+        multi = run_env(ae, "0", K, V, noise, wl.n_steps, committed=com, n_fixed=10, corr=corr)
         ref, meta = load_golden("pi05-b1-committed10-corr4")
         assert meta["n_corr"] == 4
-        rel = rel_l2_per_rollout(got, ref)
         plain, _ = load_golden("pi05-b1-committed10")
         effect = rel_l2_per_rollout(plain, ref)
-        print("rel-L2 %.3e max-abs %.3e; the item moves the actions by %.3e" % (rel, np.abs(got - ref).max(), effect),
-              flush=True)
-        assert rel <= BF16_TOL
-        assert effect > 10 * rel
-        assert np.array_equal(got[:, :10].astype(np.float32), com)
+        for label, out in (("single-launch", got), ("multi-kernel", multi)):
+            rel = rel_l2_per_rollout(out, ref)
+            print("%s: rel-L2 %.3e max-abs %.3e; the item moves the actions by %.3e"
+                  % (label, rel, np.abs(out - ref).max(), effect), flush=True)
+            assert rel <= BF16_TOL
+            assert effect > 10 * rel
+            assert np.array_equal(out[:, :10].astype(np.float32), com)
+        assert np.array_equal(got, run(ae, K, V, noise, wl.n_steps, committed=com, n_fixed=10, corr=corr))
         after = run(ae, K, V, noise, wl.n_steps, committed=com, n_fixed=10)
         assert np.array_equal(before, after)
     finally:
         ae.close()
+
+
+def test_persistent_tiny_bf16_correction_rows_batched():
+    """Two rollouts of 4 correction + horizon action rows in the single-launch
+    kernel (ragged prefixes, committed rows) against the oracle and the
+    multi-kernel path, and bitwise repeatable."""
+    torch_cuda()
+    wl = synth.WORKLOADS["tiny-fp32"].with_(dtype="bf16", batch=2, n_fixed=2, name="tiny-bf16-corr-b2")
+    lens = [wl.prefix, 17]
+    assert 2 * (wl.dims.horizon + 4) <= 64
+    print("case tiny bf16 b2 + 4 correction rows, single-launch, prefix_len %s" % lens, flush=True)
+    w, K, V, noise, corr = _inputs(wl, 4, lens)
+    com = synth.make_committed(wl)
+    ae = make_expert(wl, w, max_batch=2, max_prefix=wl.prefix, max_corr=4)
+    try:
+        kw = dict(prefix_len=lens, committed=com, n_fixed=2, corr=corr)
+        got = run_env(ae, None, K, V, noise, wl.n_steps, **kw)
+        multi = run_env(ae, "0", K, V, noise, wl.n_steps, **kw)
+        again = run_env(ae, None, K, V, noise, wl.n_steps, **kw)
+    finally:
+        ae.close()
+    ref = oracle.denoise(oracle.Expert(wl.dims, w), noise, K, V, lens, wl.n_steps, committed=com, n_fixed=2,
+                         corr=corr)
+    rel = rel_l2_per_rollout(got, ref)
+    print("single-launch rel-L2 %.3e, vs multi-kernel %.3e" % (rel, rel_l2_per_rollout(got, multi)), flush=True)
+    assert rel <= BF16_TOL
+    assert rel_l2_per_rollout(got, multi) <= 5e-3
+    assert np.array_equal(got, again)
+    assert np.array_equal(got[:, :2].astype(np.float32), com)
 
 
 # ---------------------------------------------------------------------------

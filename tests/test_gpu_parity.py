@@ -13,7 +13,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import Inputs, load_golden, make_expert, rel_l2_per_rollout, run, torch_cuda
+from gpu_util import Inputs, load_golden, make_expert, rel_l2_per_rollout, run, run_env, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -235,21 +235,6 @@ def test_pi05_fp32_shape_at_1e4():
 # ---------------------------------------------------------------------------
 # single-launch (persistent) path: batch * horizon <= 64 with bf16 weights
 # ---------------------------------------------------------------------------
-def _run_env(ae, env, *args, **kw):
-    old = os.environ.get("JPI_PERSIST")
-    if env is None:
-        os.environ.pop("JPI_PERSIST", None)
-    else:
-        os.environ["JPI_PERSIST"] = env
-    try:
-        return run(ae, *args, **kw)
-    finally:
-        if old is None:
-            os.environ.pop("JPI_PERSIST", None)
-        else:
-            os.environ["JPI_PERSIST"] = old
-
-
 def test_persistent_tiny_bf16_batched_ragged_committed():
     torch_cuda()
     wl = synth.WORKLOADS["tiny-fp32"].with_(dtype="bf16", batch=3, n_fixed=2, prefix_len=(64, 5, 41),
@@ -257,9 +242,9 @@ def test_persistent_tiny_bf16_batched_ragged_committed():
     inp = Inputs(wl)
     ae = make_expert(wl, inp.weights)
     try:
-        got = _run_env(ae, None, inp.K, inp.V, inp.noise, wl.n_steps, prefix_len=inp.prefix_len,
+        got = run_env(ae, None, inp.K, inp.V, inp.noise, wl.n_steps, prefix_len=inp.prefix_len,
                        committed=inp.committed, n_fixed=2)
-        multi = _run_env(ae, "0", inp.K, inp.V, inp.noise, wl.n_steps, prefix_len=inp.prefix_len,
+        multi = run_env(ae, "0", inp.K, inp.V, inp.noise, wl.n_steps, prefix_len=inp.prefix_len,
                          committed=inp.committed, n_fixed=2)
     finally:
         ae.close()
@@ -276,12 +261,12 @@ def test_persistent_matches_multikernel_pi05(pi05):
     wl = synth.WORKLOADS["pi05-b1"]
     K, V = synth.make_prefix(wl)
     noise = synth.make_noise(wl)
-    a = _run_env(ae, None, K, V, noise, 2)
-    b = _run_env(ae, "0", K, V, noise, 2)
+    a = run_env(ae, None, K, V, noise, 2)
+    b = run_env(ae, "0", K, V, noise, 2)
     print("pi05 2-step: persistent vs multi-kernel rel-L2 %.3e" % rel_l2_per_rollout(a, b))
     assert rel_l2_per_rollout(a, b) <= 5e-3
     # graph replay determinism of the single-launch kernel
-    assert np.array_equal(a, _run_env(ae, None, K, V, noise, 2))
+    assert np.array_equal(a, run_env(ae, None, K, V, noise, 2))
 
 
 def test_persistent_repeated_calls_bitwise(pi05):
