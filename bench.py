@@ -46,10 +46,10 @@ METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roof
 # sha256 of the kernel source they were measured on; the byte counts are the
 # counter readings times the copy calibration factor.
 MEASURED_TRAFFIC = {
-    # pi0.5 shape, batch 1: FETCH_SIZE 5274264.5 KiB x 1.99980 (a 256 MiB copy
-    # reads back 131085.17 KiB) + WRITE_SIZE 2007096.2 KiB x 1.00000 (the copy's
+    # pi0.5 shape, batch 1: FETCH_SIZE 5269989.5 KiB x 1.99980 (a 256 MiB copy
+    # reads back 131085.25 KiB) + WRITE_SIZE 2007096.2 KiB x 1.00000 (the copy's
     # 262144 KiB), mean over 29 dispatches
-    ("f40321efb8dc85dc30d3e2cd99221187d67baeddc6568681346d6a2593fd6a48", "pi05-b1"): 12855875392,
+    ("f471df150c702af926344b09f1d035fe028a52a76f76b106143f1b819aa69089", "pi05-b1"): 12847114162,
 }
 
 
