@@ -38,6 +38,10 @@ R8  Each action query sees prefix keys j < prefix_len and all H action keys;
     masked prefix slots are never read.
 R9  Committed rows (i < n_fixed) are ordinary tokens that share the global t
     and are never Euler-updated.
+R9b Variant (not the default): committed rows carry flow time t = 0 -- they
+    are clean actions -- while the other rows carry the step's t_k, so the
+    adaRMSNorm modulation (scale, shift, gate) is chosen per row.  The
+    correction tokens keep the step's t.
 R10 The correction item (T' tokens already in the expert's width, Section
     "Foresight-Aligned Asynchronous Correction") enters as T' extra suffix
     tokens placed ahead of the action tokens: correction token j sits at RoPE
@@ -211,12 +215,13 @@ def modulation(ex: Expert, name: str, cond):
     return tuple(m[i * ex.W:(i + 1) * ex.W] for i in range(m.shape[0] // ex.W))
 
 
-def velocity(ex: Expert, x, t: float, Kp, Vp, prefix_len, corr=None):
+def velocity(ex: Expert, x, t: float, Kp, Vp, prefix_len, corr=None, n_t0: int = 0):
     """v(x, t) for a batch of independent rollouts.
 
     x: [B][H][A]; Kp, Vp: [L][B][P][Dh] (any dtype, widened here);
     prefix_len: [B]; corr: [B][T'][W] correction tokens or None (reading
-    R10).  Returns v [B][H][A].
+    R10); n_t0: leading action rows that carry t = 0 instead of t (reading
+    R9b).  Returns v [B][H][A].
     """
     w = ex.w
     B, H, A = x.shape
@@ -224,13 +229,23 @@ def velocity(ex: Expert, x, t: float, Kp, Vp, prefix_len, corr=None):
     C = 0 if corr is None else np.asarray(corr).shape[1]
     S = C + H                                                                  # suffix tokens per rollout
     cond = time_conditioning(ex, t)
+    cond0 = time_conditioning(ex, 0.0) if n_t0 else cond
+    zero_t = np.zeros((B, S, 1), dtype=bool)
+    zero_t[:, C:C + n_t0] = True                                               # reading R9b
+    zero_t = zero_t.reshape(B * S, 1)
+
+    def mod(name):
+        """Per-row (scale, shift[, gate]): the t = 0 chunks on rows in zero_t."""
+        return tuple(np.where(zero_t, m0, mt) for m0, mt in zip(modulation(ex, name, cond0),
+                                                                 modulation(ex, name, cond)))
+
     act = x.reshape(B, H, A) @ w["action_in.w"].T + w["action_in.b"]           # [B][H][W]
     if C:
         act = np.concatenate([widen(corr).reshape(B, C, W), act], axis=1)      # reading R10
     h = act.reshape(B * S, W)
     for l in range(L):
         p = "layers.%d." % l
-        scale, shift, gate = modulation(ex, p + "attn_mod", cond)
+        scale, shift, gate = mod(p + "attn_mod")
         y = ada_rms_norm(h, scale, shift)
         q = (y @ w[p + "q.w"].T).reshape(B, S, nH, Dh)
         ks = (y @ w[p + "k.w"].T).reshape(B, S, Dh)
@@ -244,11 +259,11 @@ def velocity(ex: Expert, x, t: float, Kp, Vp, prefix_len, corr=None):
             ob = prefix_self_attention(qb, widen(Kp[l, b]), widen(Vp[l, b]), pl, kb, vs[b])
             o[b] = np.transpose(ob, (1, 0, 2)).reshape(S, nH * Dh)
         h = h + gate * (o.reshape(B * S, nH * Dh) @ w[p + "o.w"].T)
-        scale, shift, gate = modulation(ex, p + "mlp_mod", cond)
+        scale, shift, gate = mod(p + "mlp_mod")
         y = ada_rms_norm(h, scale, shift)
         z = gelu_tanh(y @ w[p + "gate.w"].T) * (y @ w[p + "up.w"].T)
         h = h + gate * (z @ w[p + "down.w"].T)
-    scale, shift = modulation(ex, "final_mod", cond)
+    scale, shift = (m.reshape(B, S, W)[:, C:, :].reshape(B * H, W) for m in mod("final_mod"))
     h = h.reshape(B, S, W)[:, C:, :].reshape(B * H, W)                          # action tokens only
     v = ada_rms_norm(h, scale, shift) @ w["action_out.w"].T + w["action_out.b"]
     return v.reshape(B, H, A)
@@ -279,14 +294,16 @@ def integrate(x1, n_fixed: int, n_steps: int, vel_fn):
 
 
 def denoise(ex: Expert, noise, Kp, Vp, prefix_len, n_steps: int, committed=None, n_fixed: int = 0,
-            corr=None):
+            corr=None, committed_t0: bool = False):
     """The whole hot path: action chunk from noise by N Euler steps.
 
     noise: [B][H][A]; committed: [B][n_fixed][A] or None; corr: [B][T'][W]
-    correction tokens or None (reading R10).  Returns fp64 [B][H][A].
+    correction tokens or None (reading R10); committed_t0: the committed rows
+    carry t = 0 (reading R9b).  Returns fp64 [B][H][A].
     """
     x = np.array(noise, dtype=np.float64)
     if n_fixed:
         x[:, :n_fixed, :] = np.asarray(committed, dtype=np.float64)
     return integrate(x, n_fixed, n_steps,
-                     lambda xx, t: velocity(ex, xx, t, Kp, Vp, prefix_len, corr))
+                     lambda xx, t: velocity(ex, xx, t, Kp, Vp, prefix_len, corr,
+                                            n_fixed if committed_t0 else 0))

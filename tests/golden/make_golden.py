@@ -39,9 +39,13 @@ CASES = {
     # the correction item of the future correction module (4 tokens) ahead of the
     # action tokens, with the committed rows of the same call
     "pi05-b1-committed10-corr4": ("pi05-b1-committed10", {"name": "pi05-b1-committed10-corr4"}, None),
+    # the variant in which the committed rows carry flow time t = 0
+    "pi05-b1-committed10-t0": ("pi05-b1-committed10", {"name": "pi05-b1-committed10-t0"}, None),
 }
 # cases whose expert call also gets correction tokens: name -> tokens per rollout
 CORR_TOKENS = {"pi05-b1-committed10-corr4": 4}
+# cases run with the committed rows at t = 0
+COMMITTED_T0 = {"pi05-b1-committed10-t0"}
 
 
 def source_hash(*paths):
@@ -70,7 +74,9 @@ def make(name):
     corr = synth_corr.make_item(wl.seed, wl.batch, n_corr, wl.dims.width, rl) if n_corr else None
     ex = oracle.Expert(wl.dims, w)
     t1 = time.time()
-    out = oracle.denoise(ex, noise, K, V, lens, wl.n_steps, committed=com, n_fixed=wl.n_fixed, corr=corr)
+    at_t0 = name in COMMITTED_T0
+    out = oracle.denoise(ex, noise, K, V, lens, wl.n_steps, committed=com, n_fixed=wl.n_fixed, corr=corr,
+                         committed_t0=at_t0)
     t2 = time.time()
     np.save(os.path.join(HERE, name + ".npy"), out, allow_pickle=False)
     meta = {"workload": wl.name, "base_workload": CASES[name][0], "overrides": {k: list(v) if isinstance(v, tuple) else v
@@ -81,7 +87,7 @@ def make(name):
             "synth_sha256": source_hash(os.path.join(ROOT, "synth", "synth.c"),
                                         os.path.join(ROOT, "synth", "__init__.py")),
             "oracle_seconds": round(t2 - t1, 2), "setup_seconds": round(t1 - t0, 2),
-            "n_corr": n_corr,
+            "n_corr": n_corr, "committed_t0": at_t0,
             "made_by": "tests/golden/make_golden.py (oracle + synth only)"}
     if n_corr:
         meta["item_sha256"] = source_hash(os.path.join(ROOT, "synth", "correction.py"))

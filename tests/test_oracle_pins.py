@@ -203,10 +203,11 @@ def _small(seed=99, P=6, B=2, dtype="f32"):
     return wl, w, K, V, synth.make_noise(wl)
 
 
-def _bruteforce_velocity(w, d, x, t, Kp, Vp, plen, corr=()):
+def _bruteforce_velocity(w, d, x, t, Kp, Vp, plen, corr=(), n_t0=0):
     """Scalar-loop velocity for one rollout, written from the same readings
     with explicit [out][in] indexing (a second, independent formulation).
-    ``corr`` holds correction tokens, which occupy the first suffix slots."""
+    ``corr`` holds correction tokens, which occupy the first suffix slots;
+    the first ``n_t0`` action tokens are conditioned on t = 0."""
     W, H, A, nH, Dh, F = d.width, d.horizon, d.action_dim, d.n_heads, d.head_dim, d.mlp_dim
     g = {k: np.asarray(synth.bf16_bits_to_f32(v) if v.dtype == np.uint16 else v, dtype=np.float64)
          for k, v in w.items()}
@@ -220,10 +221,14 @@ def _bruteforce_velocity(w, d, x, t, Kp, Vp, plen, corr=()):
 
     sig = lambda z: 1.0 / (1.0 + math.exp(-z))
     half = W // 2
-    emb = [math.cos(1000 * t * 10000 ** (-j / half)) for j in range(half)] + \
-          [math.sin(1000 * t * 10000 ** (-j / half)) for j in range(half)]
-    c = [z * sig(z) for z in lin("time_mlp.0.w", emb, "time_mlp.0.b")]
-    cond = [z * sig(z) for z in lin("time_mlp.1.w", c, "time_mlp.1.b")]
+
+    def conditioning(tt):
+        emb = [math.cos(1000 * tt * 10000 ** (-j / half)) for j in range(half)] + \
+              [math.sin(1000 * tt * 10000 ** (-j / half)) for j in range(half)]
+        c = [z * sig(z) for z in lin("time_mlp.0.w", emb, "time_mlp.0.b")]
+        return [z * sig(z) for z in lin("time_mlp.1.w", c, "time_mlp.1.b")]
+
+    conds = [conditioning(t), conditioning(0.0)]
 
     def norm(row, s, b):
         r = math.sqrt(sum(v * v for v in row) / len(row) + 1e-6)
@@ -241,11 +246,15 @@ def _bruteforce_velocity(w, d, x, t, Kp, Vp, plen, corr=()):
     C = len(corr)
     h = [list(map(float, corr[j])) for j in range(C)] + [lin("action_in.w", x[i], "action_in.b") for i in range(H)]
     H = C + d.horizon                       # every suffix token goes through the layers
+    which = [1 if C <= i < C + n_t0 else 0 for i in range(H)]   # conditioning of each token
+
+    def mods(name):
+        return [lin(name + ".w", cnd, name + ".b") for cnd in conds]
+
     for l in range(d.n_layers):
         p = "layers.%d." % l
-        m = lin(p + "attn_mod.w", cond, p + "attn_mod.b")
-        s, sh, gt = m[:W], m[W:2 * W], m[2 * W:]
-        y = [norm(h[i], s, sh) for i in range(H)]
+        mm2 = mods(p + "attn_mod")
+        y = [norm(h[i], mm2[which[i]][:W], mm2[which[i]][W:2 * W]) for i in range(H)]
         q = [lin(p + "q.w", y[i]) for i in range(H)]
         ks = [rot(lin(p + "k.w", y[i]), plen + i) for i in range(H)]
         vs = [lin(p + "v.w", y[i]) for i in range(H)]
@@ -263,18 +272,20 @@ def _bruteforce_velocity(w, d, x, t, Kp, Vp, plen, corr=()):
                     o[i][n * Dh + e] = sum(ex[j] * vals[j][e] for j in range(len(keys))) / tot
         for i in range(H):
             ao = lin(p + "o.w", o[i])
+            gt = mm2[which[i]][2 * W:]
             h[i] = [h[i][c_] + gt[c_] * ao[c_] for c_ in range(W)]
-        m = lin(p + "mlp_mod.w", cond, p + "mlp_mod.b")
-        s, sh, gt = m[:W], m[W:2 * W], m[2 * W:]
+        mm2 = mods(p + "mlp_mod")
         for i in range(H):
+            s, sh, gt = mm2[which[i]][:W], mm2[which[i]][W:2 * W], mm2[which[i]][2 * W:]
             yi = norm(h[i], s, sh)
             gg, uu = lin(p + "gate.w", yi), lin(p + "up.w", yi)
             z = [0.5 * gg[f] * (1 + math.tanh(math.sqrt(2 / math.pi) * (gg[f] + 0.044715 * gg[f] ** 3))) * uu[f]
                  for f in range(F)]
             dn = lin(p + "down.w", z)
             h[i] = [h[i][c_] + gt[c_] * dn[c_] for c_ in range(W)]
-    m = lin("final_mod.w", cond, "final_mod.b")
-    return np.array([lin("action_out.w", norm(h[i], m[:W], m[W:]), "action_out.b") for i in range(C, H)])
+    fm = mods("final_mod")
+    return np.array([lin("action_out.w", norm(h[i], fm[which[i]][:W], fm[which[i]][W:]), "action_out.b")
+                     for i in range(C, H)])
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -467,3 +478,38 @@ def test_bf16_rounding_is_rne():
     bits = synth.f32_to_bf16_bits(a)
     assert [int(b) for b in bits] == [0x3F80, 0x3F80, 0x3F82, 0xC020, 0x7F80]
     np.testing.assert_array_equal(synth.bf16_bits_to_f32(bits)[:4], [1.0, 1.0, 1.0 + 2 ** -6, -2.5])
+
+
+# ---------------------------------------------------------------------------
+# committed rows at t = 0 (reading R9b)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("with_corr", [False, True])
+def test_velocity_with_committed_rows_at_t0_matches_scalar_bruteforce(with_corr):
+    wl, w, K, V, noise = _small()
+    ex = oracle.Expert(SMALL, w)
+    corr = _corr(C=2) if with_corr else None
+    plens = [6, 3]
+    v = oracle.velocity(ex, noise, 0.6, K, V, plens, corr, n_t0=2)
+    for b in range(2):
+        ref = _bruteforce_velocity(w, SMALL, noise[b].astype(np.float64), 0.6, oracle.widen(K[:, b]),
+                                   oracle.widen(V[:, b]), plens[b], () if corr is None else corr[b], n_t0=2)
+        np.testing.assert_allclose(v[b], ref, rtol=1e-10, atol=1e-12)
+
+
+def test_committed_t0_matters_only_through_time():
+    wl, w, K, V, noise = _small()
+    com = np.random.default_rng(6).normal(size=(2, 2, 3))
+    ex = oracle.Expert(SMALL, w)
+    a = oracle.denoise(ex, noise, K, V, [6, 6], 3, committed=com, n_fixed=2, committed_t0=True)
+    b = oracle.denoise(ex, noise, K, V, [6, 6], 3, committed=com, n_fixed=2)
+    assert np.array_equal(a[:, :2], com)
+    assert np.abs(a - b).max() > 1e-3
+    # no committed rows: the variant is the default exactly
+    assert np.array_equal(oracle.denoise(ex, noise, K, V, [6, 6], 3, committed_t0=True),
+                          oracle.denoise(ex, noise, K, V, [6, 6], 3))
+    # conditioning that ignores t: both readings agree bit for bit
+    w["time_mlp.0.w"][:] = 0.0
+    ex = oracle.Expert(SMALL, w)
+    a = oracle.denoise(ex, noise, K, V, [6, 6], 3, committed=com, n_fixed=2, committed_t0=True)
+    b = oracle.denoise(ex, noise, K, V, [6, 6], 3, committed=com, n_fixed=2)
+    assert np.array_equal(a, b)
