@@ -167,6 +167,16 @@ jpi_status jpi_bind_prefix(jpi_ctx* ctx, const void* k, const void* v, const int
 jpi_status jpi_bind_state(jpi_ctx* ctx, const float* committed_dev, int n_fixed, const void* corr_tokens,
                           int n_corr, void* stream);
 
+/* Flow time of the committed rows (a variant; Algorithm 1 commits actions
+ * that are already final, while the paper does not say at which flow time
+ * the expert sees them).  enable = 0 (default): committed rows share the
+ * step's t_k with every other row.  enable != 0: committed rows carry t = 0
+ * (clean actions) at every step, so their adaRMSNorm scale, shift and gate
+ * come from the time conditioning at t = 0 while the other rows use t_k; the
+ * correction tokens keep t_k.  Takes effect at the next jpi_denoise.
+ * Errors: JPI_ERR_ARG (NULL ctx). */
+jpi_status jpi_set_committed_t0(jpi_ctx* ctx, int enable);
+
 /* Denoise one action chunk per rollout: x starts at noise (rows < n_fixed
  * take the committed values), then n_steps Euler steps of the velocity field
  * run, and x is written to actions_dev.  noise_dev, actions_dev: device

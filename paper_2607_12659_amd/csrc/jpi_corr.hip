@@ -10,7 +10,7 @@
 //   predict: action MLP (a row kernel for A -> W, then a GEMM), the action
 //     block with RoPE at 0..n-1, the feature concatenation [c_j ; s] gathered
 //     in bf16, the fusion GEMM, two blocks over the T' tokens, the correction
-//     head GEMM and one row kernel that adds its bias and computes the
+//     head GEMM, a row kernel that adds its bias and one that computes the
 //     confidence.
 // Linear layers with bias run as: residual rows preset to the bias, fp32
 // split-K GEMM slices, then the residual + norm row kernel with gate 1, which
@@ -66,25 +66,29 @@ __global__ __launch_bounds__(256) void k_fuse_in(const float* __restrict__ c, co
   }
 }
 
-// One workgroup per rollout: item = sum_z P[z] + b_c over its T' rows;
-// conf = sum_k w_conf[k] mean_j y[j][k] + b_conf
-__global__ __launch_bounds__(256) void k_heads(const float* __restrict__ part, int S, int M,
-                                               const float* __restrict__ bc, const bf16* __restrict__ y,
-                                               const bf16* __restrict__ wconf, const float* __restrict__ bconf,
-                                               float* __restrict__ item, float* __restrict__ conf, int T, int W) {
+// item[m] = sum_z P[z][m] + b_c, one workgroup per token row m, four columns per thread
+__global__ __launch_bounds__(256) void k_item(const float* __restrict__ part, int S, int M,
+                                              const float* __restrict__ bc, float* __restrict__ item, int W) {
+  const int m = blockIdx.x;
+  const size_t MW = (size_t)M * W;
+  for (int k = 4 * threadIdx.x; k < W; k += 1024) {
+    const size_t o = (size_t)m * W + k;
+    f32x4 v = *reinterpret_cast<const f32x4*>(bc + k);
+    for (int z = 0; z < S; ++z) v += *reinterpret_cast<const f32x4*>(part + z * MW + o);
+    *reinterpret_cast<f32x4*>(item + o) = v;
+  }
+}
+
+// conf[b] = sum_k w_conf[k] mean_j y[b T + j][k] + b_conf, one workgroup per rollout
+__global__ __launch_bounds__(256) void k_conf(const bf16* __restrict__ y, const bf16* __restrict__ wconf,
+                                              const float* __restrict__ bconf, float* __restrict__ conf, int T,
+                                              int W) {
   __shared__ float red[4];
   const int b = blockIdx.x;
-  const size_t MW = (size_t)M * W;
   float acc = 0.f;
   for (int k = threadIdx.x; k < W; k += 256) {
     float ym = 0.f;
-    for (int j = 0; j < T; ++j) {
-      const size_t o = ((size_t)b * T + j) * W + k;
-      float v = 0.f;
-      for (int z = 0; z < S; ++z) v += part[z * MW + o];
-      item[o] = v + bc[k];
-      ym += static_cast<float>(y[o]);
-    }
+    for (int j = 0; j < T; ++j) ym += static_cast<float>(y[((size_t)b * T + j) * W + k]);
     acc = fmaf(static_cast<float>(wconf[k]), ym / (float)T, acc);
   }
   acc = block_sum_256(acc, red);
@@ -525,8 +529,10 @@ jpi_status jpi_corr_predict(jpi_corr* m, const float* state, const float* action
   g.epi = EPI_STORE_F32;
   g.ep.out_f32 = m->partial;
   CCHK(m, launch_gemm(JPI_BF16, g, s));
-  hipLaunchKernelGGL(k_heads, dim3(batch), dim3(256), 0, s, m->partial, g.splitk, Mq, m->b_corr, (const bf16*)m->y,
-                     (const bf16*)m->w_conf, m->b_conf, item_out, conf_out, T, W);
+  hipLaunchKernelGGL(k_conf, dim3(batch), dim3(256), 0, s, (const bf16*)m->y, (const bf16*)m->w_conf, m->b_conf,
+                     conf_out, T, W);
+  CCHK(m, hipGetLastError());
+  hipLaunchKernelGGL(k_item, dim3(Mq), dim3(256), 0, s, m->partial, g.splitk, Mq, m->b_corr, item_out, W);
   CCHK(m, hipGetLastError());
   return JPI_OK;
 }

@@ -73,11 +73,15 @@ struct RowLaunch {
   int A, horizon, n_fixed;
   int n_lead;            // correction rows ahead of each rollout's action rows (rows m = b*(n_lead+horizon)+r)
   float dt;
+  int n_t0;              // leading action rows (committed) that take the t = 0 modulation
+  int64_t t0_delta;      // offset (floats) from the step's modulation row to the t = 0 row
 };
 // corr: [B][n_lead][W] correction tokens (rows r < n_lead of each rollout), may be NULL when n_lead == 0
+// n_t0 / t0_delta: the first n_t0 action rows read scale and shift at +t0_delta floats (the t = 0 table row)
 hipError_t launch_inproj_norm(jpi_dtype dt, const float* x, const void* w_in, const float* b_in, float* h,
                               const float* scale, const float* shift, void* y, int M, int W, int A, float eps,
-                              const float* corr, int n_lead, int horizon, hipStream_t s);
+                              const float* corr, int n_lead, int horizon, int n_t0, int64_t t0_delta,
+                              hipStream_t s);
 hipError_t launch_resid_norm(jpi_dtype dt, const RowLaunch& r, bool final_step, hipStream_t s);
 
 struct AttnLaunch {
@@ -119,6 +123,7 @@ struct PersistArgs {
   const float* corr;        // [B][n_corr][W] correction tokens (rows restart from them every step)
   int C;                    // attention chunks (32 keys) per rollout
   int n_steps, n_fixed, s_o, s_d, R;
+  int n_t0;                 // leading action rows (committed) modulated at t = 0: table row n_steps
   float eps, dt;
   const void* w_layers;     // packed layer weights (bf16)
   const void* w_frag;       // the same, each matrix fragment-ordered
@@ -127,7 +132,7 @@ struct PersistArgs {
   const float* b_in;
   const void* w_out;
   const float* b_out;
-  const float* table;       // [n_steps][R] modulation
+  const float* table;       // [n_steps + 1][R] modulation (row n_steps: t = 0)
   const void* kp;           // prefix K [L][Bmax][Pmax][Dh]
   const void* vpt;          // prefix V transposed [L][Bmax][Dh][Ppad]
   int64_t kp_lstride, kp_bstride, vpt_lstride, vpt_bstride, vpt_dstride;
@@ -217,7 +222,8 @@ hipError_t launch_fill_f32(float* p, int n, float v, hipStream_t s);
 hipError_t launch_identity_rope(float2* tab, int n, hipStream_t s);
 hipError_t launch_bcast_rows(const float* src, float* dst, int M, int period, int W, hipStream_t s);
 
-hipError_t launch_time_embed(const float* t, float* emb, int n, int W, hipStream_t s);
+// emb[k] for k < rows at t = 1 - k/n
+hipError_t launch_time_embed(float* emb, int rows, int n, int W, hipStream_t s);
 // out[m][n] = act(sum_k in[m][k] w[n][k] + b[n]), fp64 accumulation; act 0 = none, 1 = swish
 hipError_t launch_rowdot(jpi_dtype dt, const float* in, const void* w, const float* b, float* out, int M,
                          int N, int K, int act, hipStream_t s);

@@ -476,11 +476,16 @@ __global__ __launch_bounds__(256) void k_inproj_norm(const float* __restrict__ x
                                                      const float* __restrict__ b_in, float* __restrict__ h,
                                                      const float* __restrict__ scale, const float* __restrict__ shift,
                                                      T* __restrict__ y, int W, int A, float eps,
-                                                     const float* __restrict__ corr, int n_lead, int horizon) {
+                                                     const float* __restrict__ corr, int n_lead, int horizon,
+                                                     int n_t0, int64_t t0_delta) {
   __shared__ float hs[ROW_MAX_W];
   __shared__ float xs[256];
   __shared__ float red[4];
   const int m = blockIdx.x, S = n_lead + horizon, b = m / S, i = m % S;
+  if (i >= n_lead && i - n_lead < n_t0) {  // a committed row at t = 0: the t = 0 table row
+    scale += t0_delta;
+    shift += t0_delta;
+  }
   if (i < n_lead) {
     const float* cr = corr + ((size_t)b * n_lead + i) * W;
     for (int n = threadIdx.x; n < W; n += 256) {
@@ -520,6 +525,16 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
   if constexpr (FINAL) {
     if (m % (r.n_lead + r.horizon) < r.n_lead) return;
   }
+  // committed rows at t = 0 take the gate, scale and shift of the t = 0 table row
+  const float *gate = r.gate, *scale = r.scale, *shift = r.shift;
+  if (r.n_t0 > 0) {
+    const int ia = m % (r.n_lead + r.horizon) - r.n_lead;
+    if (ia >= 0 && ia < r.n_t0) {
+      gate += r.t0_delta;
+      scale += r.t0_delta;
+      shift += r.t0_delta;
+    }
+  }
   float* hr = r.h + (size_t)m * W;
   const float* pr = r.part + (size_t)m * W;
   // four columns per thread per pass; all split-K slices loaded before summing
@@ -531,7 +546,7 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
 #pragma unroll
       for (int z = 0; z < ROW_MAX_S; ++z) v[j][z] = (z < S && k < W) ? pr[z * MW + k] : 0.f;
       hv[j] = k < W ? hr[k] : 0.f;
-      gv[j] = k < W ? r.gate[k] : 0.f;
+      gv[j] = k < W ? gate[k] : 0.f;
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -551,7 +566,7 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
   const float rs = row_rstd(hs, W, r.eps, red);
   if constexpr (!FINAL) {
     T* yr = reinterpret_cast<T*>(r.y) + (size_t)m * W;
-    for (int k = threadIdx.x; k < W; k += 256) yr[k] = from_f32<T>(hs[k] * rs * (1.0f + r.scale[k]) + r.shift[k]);
+    for (int k = threadIdx.x; k < W; k += 256) yr[k] = from_f32<T>(hs[k] * rs * (1.0f + scale[k]) + shift[k]);
   } else {
     // v[a] = sum_k y[k] W_out[a][k] + b_out[a]; each thread owns columns k = t + 256 j
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -560,7 +575,7 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
 #pragma unroll
     for (int j = 0; j < ROW_MAX_W / 256; ++j) {
       const int k = threadIdx.x + 256 * j;
-      yk[j] = k < W ? hs[k] * rs * (1.0f + r.scale[k]) + r.shift[k] : 0.f;
+      yk[j] = k < W ? hs[k] * rs * (1.0f + scale[k]) + shift[k] : 0.f;
     }
     for (int a0 = 0; a0 < r.A; a0 += 8) {
       float p[8];
@@ -591,15 +606,16 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
 
 hipError_t launch_inproj_norm(jpi_dtype dt, const float* x, const void* w_in, const float* b_in, float* h,
                               const float* scale, const float* shift, void* y, int M, int W, int A, float eps,
-                              const float* corr, int n_lead, int horizon, hipStream_t s) {
+                              const float* corr, int n_lead, int horizon, int n_t0, int64_t t0_delta,
+                              hipStream_t s) {
   if (W > ROW_MAX_W || A > 256 || horizon < 1 || n_lead < 0 || (n_lead > 0 && !corr) || M % (n_lead + horizon))
     return hipErrorInvalidValue;
   if (dt == JPI_BF16)
     hipLaunchKernelGGL(k_inproj_norm<bf16>, dim3(M), dim3(256), 0, s, x, (const bf16*)w_in, b_in, h, scale, shift,
-                       (bf16*)y, W, A, eps, corr, n_lead, horizon);
+                       (bf16*)y, W, A, eps, corr, n_lead, horizon, n_t0, t0_delta);
   else
     hipLaunchKernelGGL(k_inproj_norm<float>, dim3(M), dim3(256), 0, s, x, (const float*)w_in, b_in, h, scale, shift,
-                       (float*)y, W, A, eps, corr, n_lead, horizon);
+                       (float*)y, W, A, eps, corr, n_lead, horizon, n_t0, t0_delta);
   return hipGetLastError();
 }
 
@@ -916,9 +932,10 @@ hipError_t launch_transpose(jpi_dtype dt, const void* src, void* dst, int rows, 
 // once per (weights, n_steps): timestep embedding, time MLP and the
 // modulation table.  fp64 arithmetic; results stored in fp32.
 // ===========================================================================
-__global__ void k_time_embed(float* emb, int n, int W) {
+// rows k = 0 .. rows-1 at t = 1 - k/n (row n, when present, is t = 0)
+__global__ void k_time_embed(float* emb, int rows, int n, int W) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= n * W) return;
+  if (idx >= rows * W) return;
   const int k = idx / W, j = idx - k * W, half = W / 2;
   const int jj = j < half ? j : j - half;
   const double t = 1.0 - (double)k / (double)n;
@@ -927,8 +944,8 @@ __global__ void k_time_embed(float* emb, int n, int W) {
   emb[idx] = (float)(j < half ? cos(arg) : sin(arg));
 }
 
-hipError_t launch_time_embed(const float* /*unused*/, float* emb, int n, int W, hipStream_t s) {
-  hipLaunchKernelGGL(k_time_embed, dim3((n * W + 255) / 256), dim3(256), 0, s, emb, n, W);
+hipError_t launch_time_embed(float* emb, int rows, int n, int W, hipStream_t s) {
+  hipLaunchKernelGGL(k_time_embed, dim3((rows * W + 255) / 256), dim3(256), 0, s, emb, rows, n, W);
   return hipGetLastError();
 }
 

@@ -868,6 +868,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   const int ia = m % a.H - a.n_corr;
   const size_t xrow = (size_t)(m / a.H) * (a.H - a.n_corr) + ia;
   const float* crow = ia < 0 ? a.corr + ((size_t)(m / a.H) * a.n_corr + (m % a.H)) * W : nullptr;
+  const bool at_t0 = ia >= 0 && ia < a.n_t0;  // a committed row modulated at t = 0 (table row n_steps)
   float xreg = 0.f;
   if (t == 0) s_abort = 0u;
   if (owner) {
@@ -887,7 +888,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     // in-projection + first norm of step ki (one call site for every step)
     int ki = ph < 0 ? 0 : -1;
     const int k = ph < 0 ? 0 : ph / (8 * L), l = ph < 0 ? 0 : (ph / 8) % L, p = ph < 0 ? -1 : ph % 8;
-    const float* tk = a.table + (size_t)k * a.R;
+    const float* tk = a.table + (size_t)(at_t0 ? a.n_steps : k) * a.R;
     const float* am = tk + (size_t)(2 * l) * 3 * W;      // attention modulation: scale | shift | gate
     const float* mm = tk + (size_t)(2 * l + 1) * 3 * W;  // MLP modulation
     const bool gemm = p == 0 || p == 3 || p == 5 || p == 6;
@@ -927,7 +928,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
       phase_gemm(a, job, l, wt, smem);
     }
     if (ki >= 0 && owner) {
-      const float* ti = a.table + (size_t)ki * a.R;
+      const float* ti = a.table + (size_t)(at_t0 ? a.n_steps : ki) * a.R;
       inproj_row(a, ti, ti + W, s_hrow, s_bin, s_x, reinterpret_cast<float*>(smem), crow);
     }
     if (ph < last_phase) phase_done(a, (u32)(ph + 2));

@@ -13,8 +13,9 @@
 //   MLP norm, 2L the final norm (scale | shift | gate, W rows each).
 //
 // Per denoise step k the modulation depends only on t_k = 1 - k/N, so the
-// table [N][(6L+2)W] of all (scale, shift, gate) is computed once per
-// (weights, N) and read by the step kernels.
+// table [N + 1][(6L+2)W] of all (scale, shift, gate) is computed once per
+// (weights, N) and read by the step kernels; row N is t = 0, the time of
+// committed rows when they are treated as clean actions.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -50,10 +51,11 @@ bool kind_is_matrix(int k) {
 
 struct GraphKey {
   int batch, prefix, n_steps, n_fixed, n_corr;
-  bool persist;  // the single-launch path and the multi-kernel path capture different graphs
+  bool committed_t0;  // committed rows modulated at t = 0
+  bool persist;       // the single-launch path and the multi-kernel path capture different graphs
   bool operator<(const GraphKey& o) const {
-    return std::tie(batch, prefix, n_steps, n_fixed, n_corr, persist) <
-           std::tie(o.batch, o.prefix, o.n_steps, o.n_fixed, o.n_corr, o.persist);
+    return std::tie(batch, prefix, n_steps, n_fixed, n_corr, committed_t0, persist) <
+           std::tie(o.batch, o.prefix, o.n_steps, o.n_fixed, o.n_corr, o.committed_t0, o.persist);
   }
 };
 
@@ -98,6 +100,7 @@ struct jpi_ctx {
   int n_fixed = 0;
   float* corr = nullptr;       // [Bmax][Cmax][W] correction tokens
   int n_corr = 0;
+  bool committed_t0 = false;   // committed rows take the t = 0 modulation
   // activations
   float *x = nullptr, *h = nullptr;
   void *y = nullptr, *q = nullptr, *ks = nullptr, *vst = nullptr, *o = nullptr, *z = nullptr;
@@ -612,18 +615,19 @@ jpi_status ensure_table(jpi_ctx* c, int n_steps, hipStream_t s, float** out) {
     return JPI_OK;
   }
   const size_t W = c->W;
+  const int rows = n_steps + 1;  // t_0 .. t_{N-1}, then t = 0
   float *tab = nullptr, *tmp = nullptr;
-  TRY(dmalloc(c, (void**)&tab, (size_t)n_steps * c->R * sizeof(float)));
-  jpi_status st = dmalloc(c, (void**)&tmp, (size_t)3 * n_steps * W * sizeof(float));
+  TRY(dmalloc(c, (void**)&tab, (size_t)rows * c->R * sizeof(float)));
+  jpi_status st = dmalloc(c, (void**)&tmp, (size_t)3 * rows * W * sizeof(float));
   if (st != JPI_OK) {
     (void)hipFree(tab);
     return st;
   }
-  float *emb = tmp, *c1 = tmp + n_steps * W, *cond = tmp + 2 * n_steps * W;
-  hipError_t e = launch_time_embed(nullptr, emb, n_steps, c->W, s);
-  if (e == hipSuccess) e = launch_rowdot(c->dt, emb, c->w_t0, c->b_t0, c1, n_steps, c->W, c->W, 1, s);
-  if (e == hipSuccess) e = launch_rowdot(c->dt, c1, c->w_t1, c->b_t1, cond, n_steps, c->W, c->W, 1, s);
-  if (e == hipSuccess) e = launch_rowdot(c->dt, cond, c->w_mod, c->b_mod, tab, n_steps, c->R, c->W, 0, s);
+  float *emb = tmp, *c1 = tmp + rows * W, *cond = tmp + 2 * rows * W;
+  hipError_t e = launch_time_embed(emb, rows, n_steps, c->W, s);
+  if (e == hipSuccess) e = launch_rowdot(c->dt, emb, c->w_t0, c->b_t0, c1, rows, c->W, c->W, 1, s);
+  if (e == hipSuccess) e = launch_rowdot(c->dt, c1, c->w_t1, c->b_t1, cond, rows, c->W, c->W, 1, s);
+  if (e == hipSuccess) e = launch_rowdot(c->dt, cond, c->w_mod, c->b_mod, tab, rows, c->R, c->W, 0, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   (void)hipFree(tmp);
   if (e != hipSuccess) {
@@ -784,6 +788,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     pa.C = persist_chunks(prefix, S);
     pa.n_steps = n_steps;
     pa.n_fixed = c->n_fixed;
+    pa.n_t0 = c->committed_t0 ? c->n_fixed : 0;
     pa.s_o = p.s_o;
     pa.s_d = p.s_d;
     pa.R = c->R;
@@ -826,10 +831,13 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     ENQ(launch_persist(pa, c->n_cu, s));
     return hipSuccess;
   }
+  const int n_t0 = c->committed_t0 ? c->n_fixed : 0;
   for (int k = 0; k < n_steps; ++k) {
     const float* tk = table + (size_t)k * c->R;
     const float* fm = tk + (size_t)(6 * L) * W;
-    ENQ(launch_inproj_norm(c->dt, c->x, c->w_in, c->b_in, c->h, tk, tk + W, c->y, M, W, c->A, eps, c->corr, C, H, s));
+    const int64_t t0_delta = (int64_t)(n_steps - k) * c->R;  // to the t = 0 row
+    ENQ(launch_inproj_norm(c->dt, c->x, c->w_in, c->b_in, c->h, tk, tk + W, c->y, M, W, c->A, eps, c->corr, C, H,
+                           n_t0, t0_delta, s));
     for (int l = 0; l < L; ++l) {
       const char* lay = (const char*)c->w_layers + (size_t)l * c->layer_elems * es;
       const float* am = tk + (size_t)(2 * l) * 3 * W;
@@ -903,6 +911,10 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       r.shift = mm + W;
       r.y = c->y;
       r.eps = eps;
+      r.horizon = H;
+      r.n_lead = C;
+      r.n_t0 = n_t0;
+      r.t0_delta = t0_delta;
       ENQ(launch_resid_norm(c->dt, r, false, s));
       // GateUp + GeGLU
       g = GemmLaunch{};
@@ -945,8 +957,6 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
         r.b_out = c->b_out;
         r.x = c->x;
         r.A = c->A;
-        r.horizon = H;
-        r.n_lead = C;
         r.n_fixed = c->n_fixed;
         r.dt = dt_step;
       }
@@ -986,7 +996,7 @@ jpi_status jpi_denoise(jpi_ctx* c, const float* noise_dev, int n_steps, float* a
   if (eager_mode() || c->timed_kind >= 0) {
     HIPCHK(c, enqueue_steps(c, table, n_steps, s));
   } else {
-    const GraphKey key{c->batch, c->prefix, n_steps, c->n_fixed, c->n_corr, use_persist(c, c->batch)};
+    const GraphKey key{c->batch, c->prefix, n_steps, c->n_fixed, c->n_corr, c->committed_t0, use_persist(c, c->batch)};
     auto it = c->graphs.find(key);
     if (it == c->graphs.end()) {
       hipGraph_t graph = nullptr;
@@ -1008,6 +1018,12 @@ jpi_status jpi_denoise(jpi_ctx* c, const float* noise_dev, int n_steps, float* a
   }
   HIPCHK(c, hipMemcpyAsync(actions_dev, c->x, (size_t)c->batch * c->H * c->A * sizeof(float),
                            hipMemcpyDeviceToDevice, s));
+  return JPI_OK;
+}
+
+jpi_status jpi_set_committed_t0(jpi_ctx* c, int enable) {
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_set_committed_t0: ctx is NULL");
+  c->committed_t0 = enable != 0;
   return JPI_OK;
 }
 

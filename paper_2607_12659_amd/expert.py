@@ -71,6 +71,10 @@ class ActionExpert:
         n_corr = 0 if corr is None else int(corr.shape[1])
         self._chk(_j.jpi_bind_state(self.ctx, committed, n_fixed, corr, n_corr, stream))
 
+    def set_committed_t0(self, enable: bool):
+        """Committed rows at flow time t = 0 (True) or at the step's t (False, the default)."""
+        self._chk(_j.jpi_set_committed_t0(self.ctx, int(bool(enable))))
+
     def denoise(self, noise: torch.Tensor, n_steps: int, out: torch.Tensor | None = None, stream=None):
         if out is None:
             out = torch.empty_like(noise)

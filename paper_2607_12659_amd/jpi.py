@@ -22,7 +22,7 @@ EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create",
             "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
             "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
             "jpi_sched_run", "jpi_sched_sim_hooks", "jpi_vlm_create", "jpi_vlm_destroy", "jpi_vlm_set_weight",
-            "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error", "jpi_corr_create",
+            "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error", "jpi_set_committed_t0", "jpi_corr_create",
             "jpi_corr_destroy", "jpi_corr_set_weight", "jpi_corr_finalize_weights", "jpi_corr_compress",
             "jpi_corr_predict", "jpi_corr_last_error"]
 JPI_KERNEL_NONE, JPI_KERNEL_QKV, JPI_KERNEL_ATTENTION, JPI_KERNEL_OPROJ, JPI_KERNEL_GATEUP, JPI_KERNEL_DOWN, \
@@ -128,6 +128,7 @@ _sig = {
     "jpi_vlm_finalize_weights": (_i, [_vp, _vp]),
     "jpi_vlm_prefill": (_i, [_vp, _vp, _i, _i, _vp, _vp, _vp]),
     "jpi_vlm_last_error": (ctypes.c_char_p, [_vp]),
+    "jpi_set_committed_t0": (_i, [_vp, _i]),
     "jpi_corr_create": (_i, [ctypes.POINTER(jpi_corr_config), _i, ctypes.POINTER(_vp)]),
     "jpi_corr_destroy": (_i, [_vp]),
     "jpi_corr_set_weight": (_i, [_vp, ctypes.c_char_p, _vp, _i64, _i, _i, _vp]),
@@ -284,6 +285,10 @@ def jpi_vlm_prefill(vlm, emb, batch: int, prefix: int, ae_ctx, hidden_out=None, 
 
 def jpi_vlm_last_error(vlm) -> str:
     return _lib.jpi_vlm_last_error(vlm).decode()
+
+
+def jpi_set_committed_t0(ctx, enable: int) -> int:
+    return _lib.jpi_set_committed_t0(ctx, enable)
 
 
 def jpi_corr_create(cfg: jpi_corr_config, device: int = 0):
