@@ -30,7 +30,8 @@ from .actionexpert import (RMS_EPS, gelu_tanh, integrate, prefix_self_attention,
 
 
 def _w(weights):
-    return {k: widen(v) for k, v in weights.items()}
+    """fp64 weights (arrays already in fp64 are taken as they are)."""
+    return {k: v if isinstance(v, np.ndarray) and v.dtype == np.float64 else widen(v) for k, v in weights.items()}
 
 
 def velocity(dims, weights: dict, x, t: float, Kp, Vp, prefix_len, state):
@@ -78,4 +79,5 @@ def denoise(dims, weights: dict, noise, Kp, Vp, prefix_len, n_steps: int, state,
     x = np.array(noise, dtype=np.float64)
     if n_fixed:
         x[:, :n_fixed, :] = np.asarray(committed, dtype=np.float64)
-    return integrate(x, n_fixed, n_steps, lambda xx, t: velocity(dims, weights, xx, t, Kp, Vp, prefix_len, state))
+    w = _w(weights)  # widened once for all steps
+    return integrate(x, n_fixed, n_steps, lambda xx, t: velocity(dims, w, xx, t, Kp, Vp, prefix_len, state))

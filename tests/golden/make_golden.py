@@ -24,6 +24,7 @@ sys.path.insert(0, ROOT)
 import oracle  # noqa: E402
 import synth  # noqa: E402
 from synth import correction as synth_corr  # noqa: E402
+from synth import pi0 as synth_pi0  # noqa: E402
 
 # name -> (workload key, overrides, rollouts evaluated)
 CASES = {
@@ -46,6 +47,9 @@ CASES = {
 CORR_TOKENS = {"pi05-b1-committed10-corr4": 4}
 # cases run with the committed rows at t = 0
 COMMITTED_T0 = {"pi05-b1-committed10-t0"}
+# cases of the pi0-style expert variant (its own oracle, weights and robot state)
+PI0 = {"pi0-b1": ("pi05-b1-committed10", {"name": "pi0-b1", "prefix_len": (815,)}, None)}
+CASES.update(PI0)
 
 
 def source_hash(*paths):
@@ -61,29 +65,40 @@ def workload(name):
     return synth.WORKLOADS[key].with_(**over), rollouts
 
 
+def oracle_files(name):
+    """Oracle sources a stored output depends on (their sha256 is recorded)."""
+    if name in PI0:
+        return [os.path.join(ROOT, "oracle", "actionexpert.py"), os.path.join(ROOT, "oracle", "pi0.py")]
+    return [os.path.join(ROOT, "oracle", "actionexpert.py")]
+
+
 def make(name):
     wl, rollouts = workload(name)
     rl = list(range(wl.batch)) if rollouts is None else rollouts
     t0 = time.time()
-    w = synth.make_weights(wl)
+    w = synth_pi0.make_pi0_weights(wl) if name in PI0 else synth.make_weights(wl)
     K, V = synth.make_prefix(wl, rl)
     noise = synth.make_noise(wl, rl)
     com = synth.make_committed(wl, rl) if wl.n_fixed else None
     lens = [wl.valid_lengths()[b] for b in rl]
     n_corr = CORR_TOKENS.get(name, 0)
     corr = synth_corr.make_item(wl.seed, wl.batch, n_corr, wl.dims.width, rl) if n_corr else None
-    ex = oracle.Expert(wl.dims, w)
-    t1 = time.time()
     at_t0 = name in COMMITTED_T0
-    out = oracle.denoise(ex, noise, K, V, lens, wl.n_steps, committed=com, n_fixed=wl.n_fixed, corr=corr,
-                         committed_t0=at_t0)
+    t1 = time.time()
+    if name in PI0:
+        out = oracle.pi0.denoise(wl.dims, w, noise, K, V, lens, wl.n_steps, synth_pi0.make_state(wl, rl),
+                                 committed=com, n_fixed=wl.n_fixed)
+    else:
+        ex = oracle.Expert(wl.dims, w)
+        out = oracle.denoise(ex, noise, K, V, lens, wl.n_steps, committed=com, n_fixed=wl.n_fixed, corr=corr,
+                             committed_t0=at_t0)
     t2 = time.time()
     np.save(os.path.join(HERE, name + ".npy"), out, allow_pickle=False)
     meta = {"workload": wl.name, "base_workload": CASES[name][0], "overrides": {k: list(v) if isinstance(v, tuple) else v
                                                                              for k, v in CASES[name][1].items()},
             "rollouts": rl, "seed": wl.seed, "n_steps": wl.n_steps, "n_fixed": wl.n_fixed, "dtype": wl.dtype,
             "prefix": wl.prefix, "prefix_len": lens,
-            "oracle_sha256": source_hash(os.path.join(ROOT, "oracle", "actionexpert.py")),
+            "oracle_sha256": source_hash(*oracle_files(name)),
             "synth_sha256": source_hash(os.path.join(ROOT, "synth", "synth.c"),
                                         os.path.join(ROOT, "synth", "__init__.py")),
             "oracle_seconds": round(t2 - t1, 2), "setup_seconds": round(t1 - t0, 2),
@@ -91,6 +106,9 @@ def make(name):
             "made_by": "tests/golden/make_golden.py (oracle + synth only)"}
     if n_corr:
         meta["item_sha256"] = source_hash(os.path.join(ROOT, "synth", "correction.py"))
+    if name in PI0:
+        meta["variant"] = "action_time"
+        meta["variant_synth_sha256"] = source_hash(os.path.join(ROOT, "synth", "pi0.py"))
     with open(os.path.join(HERE, name + ".json"), "w") as f:
         json.dump(meta, f, indent=1)
     print("%s: oracle %.1fs setup %.1fs" % (name, t2 - t1, t1 - t0), flush=True)

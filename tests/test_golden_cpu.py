@@ -33,10 +33,12 @@ def test_every_case_has_a_golden():
 
 @pytest.mark.parametrize("name,meta", _metas())
 def test_golden_made_by_current_sources(name, meta):
-    assert meta["oracle_sha256"] == make_golden.source_hash(os.path.join(ROOT, "oracle", "actionexpert.py")), \
+    assert meta["oracle_sha256"] == make_golden.source_hash(*make_golden.oracle_files(name)), \
         "oracle changed since %s was generated: rerun tests/golden/make_golden.py" % name
     assert meta["synth_sha256"] == make_golden.source_hash(os.path.join(ROOT, "synth", "synth.c"),
                                                            os.path.join(ROOT, "synth", "__init__.py"))
+    if meta.get("variant"):
+        assert meta["variant_synth_sha256"] == make_golden.source_hash(os.path.join(ROOT, "synth", "pi0.py"))
     if meta.get("n_corr"):
         assert meta["item_sha256"] == make_golden.source_hash(os.path.join(ROOT, "synth", "correction.py"))
     arr = np.load(os.path.join(HERE, "golden", name + ".npy"), allow_pickle=False)
