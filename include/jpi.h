@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define JPI_ABI_VERSION 2
+#define JPI_ABI_VERSION 3
 
 typedef enum {
   JPI_OK = 0,
@@ -64,6 +64,20 @@ typedef enum {
 } jpi_status;
 
 typedef enum { JPI_F32 = 0, JPI_BF16 = 1 } jpi_dtype;
+
+/* Expert variants of the π series (Appendix "Model Architecture of π series
+ * Models" lists one action expert for π0 and π0.5; the paper does not spell
+ * out how time and state enter, so both forms here are readings):
+ *   JPI_VARIANT_ADARMS: time conditions every norm (adaRMSNorm scale, shift
+ *     and gate from a time MLP), the default described above.
+ *   JPI_VARIANT_ACTION_TIME: π0 style -- plain RMSNorm (1 + w) and ungated
+ *     residuals; time enters through an action-time MLP on each action token,
+ *     h_i = W_o swish(W_i [W_a a_i + b_a ; e(t)] + b_i) + b_o; the robot state
+ *     is one suffix token W_s s + b_s ahead of the actions (RoPE position
+ *     prefix_len; actions at prefix_len + 1 + i) that attends to the prefix and
+ *     itself only, so its keys and values are computed once per call and
+ *     occupy prefix slot prefix_len of every layer. */
+typedef enum { JPI_VARIANT_ADARMS = 0, JPI_VARIANT_ACTION_TIME = 1 } jpi_variant;
 
 typedef struct {
   int n_layers;     /* L   (pi0.5 expert: 18, Table "pi_architecture") */
@@ -80,6 +94,8 @@ typedef struct {
   float rms_eps;    /* 1e-6 */
   float rope_base;  /* 1e4 */
   int max_corr;     /* correction tokens per rollout, upper bound (0: none; at most 64) */
+  int variant;      /* jpi_variant (0: JPI_VARIANT_ADARMS) */
+  int state_dim;    /* robot-state values per rollout (JPI_VARIANT_ACTION_TIME only; else 0) */
 } jpi_config;
 
 typedef struct jpi_ctx jpi_ctx;
@@ -115,6 +131,11 @@ jpi_status jpi_destroy(jpi_ctx* ctx);
  *   layers.{l}.gate.w [F][W]  .up.w [F][W]  .down.w [W][F]
  *   final_mod.w [2W][W]  final_mod.b [2W]           (scale | shift)
  *   action_out.w [A][W]  action_out.b [A]
+ * JPI_VARIANT_ACTION_TIME replaces the time MLP and every *_mod tensor by
+ *   action_time_mlp_in.w [W][2W] (columns: action part, then time part)
+ *   action_time_mlp_in.b [W]  action_time_mlp_out.w [W][W]  action_time_mlp_out.b [W]
+ *   state_proj.w [W][state_dim]  state_proj.b [W]
+ *   layers.{l}.attn_norm.w [W]  layers.{l}.mlp_norm.w [W]  final_norm.w [W]
  * Matrices must have dt == cfg.dtype, vectors dt == JPI_F32.  `data` is a
  * device pointer if is_device != 0, else a host pointer; the caller keeps
  * ownership.  The copy is complete when the call returns (the stream is
@@ -166,6 +187,14 @@ jpi_status jpi_bind_prefix(jpi_ctx* ctx, const void* k, const void* v, const int
  * (NULL ctx or data, counts out of range), JPI_ERR_STATE (no prefix bound). */
 jpi_status jpi_bind_state(jpi_ctx* ctx, const float* committed_dev, int n_fixed, const void* corr_tokens,
                           int n_corr, void* stream);
+
+/* Robot state for JPI_VARIANT_ACTION_TIME: state_dev, device fp32
+ * [batch][state_dim], copied stream-ordered; required before jpi_denoise.
+ * Must follow jpi_bind_prefix (batch).  With this variant every prefix_len
+ * must stay below max_prefix (the state token takes slot prefix_len), and
+ * correction tokens are not supported.  Errors: JPI_ERR_ARG (NULL),
+ * JPI_ERR_STATE (no prefix bound), JPI_ERR_UNSUPPORTED (other variant). */
+jpi_status jpi_bind_robot_state(jpi_ctx* ctx, const float* state_dev, void* stream);
 
 /* Flow time of the committed rows (a variant; Algorithm 1 commits actions
  * that are already final, while the paper does not say at which flow time

@@ -15,17 +15,18 @@ namespace jpi {
 
 namespace {
 
-// y[m] = bf16(h[m] / rms(h[m]) * (1 + w)), one workgroup per row
+// y[m] = T(h[m] / rms(h[m]) * (1 + w)), one workgroup per row
+template <typename T>
 __global__ __launch_bounds__(256) void k_norm_rows(const float* __restrict__ h, const float* __restrict__ w,
-                                                   bf16* __restrict__ y, int W, float eps) {
+                                                   T* __restrict__ y, int W, float eps) {
   __shared__ float red[4];
   const float* hr = h + (size_t)blockIdx.x * W;
   float ss = 0.f;
   for (int i = threadIdx.x; i < W; i += 256) ss += hr[i] * hr[i];
   ss = block_sum_256(ss, red);
   const float r = 1.0f / sqrtf(ss / (float)W + eps);
-  bf16* yr = y + (size_t)blockIdx.x * W;
-  for (int i = threadIdx.x; i < W; i += 256) yr[i] = static_cast<bf16>(hr[i] * r * (1.0f + w[i]));
+  T* yr = y + (size_t)blockIdx.x * W;
+  for (int i = threadIdx.x; i < W; i += 256) yr[i] = from_f32<T>(hr[i] * r * (1.0f + w[i]));
 }
 
 __global__ void k_fill_i32(int* p, int n, int v) {
@@ -61,9 +62,11 @@ __global__ void k_scatter(const char* __restrict__ src, char* __restrict__ dst, 
 
 }  // namespace
 
-hipError_t launch_norm_rows(const float* h, const float* w, void* y, int M, int W, float eps, hipStream_t s) {
+hipError_t launch_norm_rows(const float* h, const float* w, void* y, int M, int W, float eps, hipStream_t s,
+                            bool f32) {
   if (M < 1) return hipSuccess;
-  hipLaunchKernelGGL(k_norm_rows, dim3(M), dim3(256), 0, s, h, w, (bf16*)y, W, eps);
+  if (f32) hipLaunchKernelGGL(k_norm_rows<float>, dim3(M), dim3(256), 0, s, h, w, (float*)y, W, eps);
+  else hipLaunchKernelGGL(k_norm_rows<bf16>, dim3(M), dim3(256), 0, s, h, w, (bf16*)y, W, eps);
   return hipGetLastError();
 }
 
@@ -133,6 +136,7 @@ hipError_t upload_rows(void* dst, const std::vector<int>& map, int row_bytes, co
 
 hipError_t enqueue_block(const BlockLaunch& b, hipStream_t s) {
   const int M = b.B * b.H, W = b.W, nH = b.nH, Dh = b.Dh, F = b.F;
+  const jpi_dtype dt = b.f32 ? JPI_F32 : JPI_BF16;
   hipError_t e;
   GemmLaunch g{};
   g.A = b.y;
@@ -152,7 +156,7 @@ hipError_t enqueue_block(const BlockLaunch& b, hipStream_t s) {
   g.ep.n_heads = nH;
   g.ep.head_dim = Dh;
   g.ep.horizon = b.H;
-  if ((e = launch_gemm(JPI_BF16, g, s)) != hipSuccess) return e;
+  if ((e = launch_gemm(dt, g, s)) != hipSuccess) return e;
   AttnLaunch a{};
   a.q = b.q;
   a.ks = b.ks;
@@ -171,13 +175,18 @@ hipError_t enqueue_block(const BlockLaunch& b, hipStream_t s) {
   a.P = b.P;
   a.Dh = Dh;
   a.opart = b.opart;
+  if (b.f32) {  // the fp32 attention's chunk maxima and sums follow its partial rows
+    const int nch = attn_n_chunks(dt, b.P, b.H);
+    a.mpart = b.opart + (size_t)b.B * nH * nch * b.H * Dh;
+    a.lpart = a.mpart + (size_t)b.B * nH * nch * b.H;
+  }
   a.out = b.o;
   a.out_f32 = 0;
   a.n_cu = b.n_cu;
-  if ((e = launch_attention(JPI_BF16, a, s)) != hipSuccess) return e;
+  if ((e = launch_attention(dt, a, s)) != hipSuccess) return e;
   g = GemmLaunch{};
   g.A = b.o;
-  g.W = b.w + b.off_o * 2;
+  g.W = b.w + b.off_o * (b.f32 ? 4 : 2);
   g.M = M;
   g.N = W;
   g.K = nH * Dh;
@@ -185,7 +194,7 @@ hipError_t enqueue_block(const BlockLaunch& b, hipStream_t s) {
   g.n_cu = b.n_cu;
   g.epi = EPI_STORE_F32;
   g.ep.out_f32 = b.partial;
-  if ((e = launch_gemm(JPI_BF16, g, s)) != hipSuccess) return e;
+  if ((e = launch_gemm(dt, g, s)) != hipSuccess) return e;
   RowLaunch r{};
   r.part = b.partial;
   r.S = b.s_o;
@@ -197,10 +206,10 @@ hipError_t enqueue_block(const BlockLaunch& b, hipStream_t s) {
   r.shift = b.zeros;
   r.y = b.y;
   r.eps = b.eps;
-  if ((e = launch_resid_norm(JPI_BF16, r, false, s)) != hipSuccess) return e;
+  if ((e = launch_resid_norm(dt, r, false, s)) != hipSuccess) return e;
   g = GemmLaunch{};
   g.A = b.y;
-  g.W = b.w + b.off_gu * 2;
+  g.W = b.w + b.off_gu * (b.f32 ? 4 : 2);
   g.M = M;
   g.N = 2 * F;
   g.K = W;
@@ -209,10 +218,10 @@ hipError_t enqueue_block(const BlockLaunch& b, hipStream_t s) {
   g.epi = EPI_GEGLU;
   g.ep.z = b.z;
   g.ep.mlp_dim = F;
-  if ((e = launch_gemm(JPI_BF16, g, s)) != hipSuccess) return e;
+  if ((e = launch_gemm(dt, g, s)) != hipSuccess) return e;
   g = GemmLaunch{};
   g.A = b.z;
-  g.W = b.w + b.off_d * 2;
+  g.W = b.w + b.off_d * (b.f32 ? 4 : 2);
   g.M = M;
   g.N = W;
   g.K = F;
@@ -220,10 +229,10 @@ hipError_t enqueue_block(const BlockLaunch& b, hipStream_t s) {
   g.n_cu = b.n_cu;
   g.epi = EPI_STORE_F32;
   g.ep.out_f32 = b.partial;
-  if ((e = launch_gemm(JPI_BF16, g, s)) != hipSuccess) return e;
+  if ((e = launch_gemm(dt, g, s)) != hipSuccess) return e;
   r.S = b.s_d;
   r.scale = b.next_norm;
-  return launch_resid_norm(JPI_BF16, r, false, s);
+  return launch_resid_norm(dt, r, false, s);
 }
 
 }  // namespace jpi

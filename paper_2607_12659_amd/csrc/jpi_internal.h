@@ -214,15 +214,32 @@ struct BlockLaunch {
   const float2* rope;            // [B][H][Dh/2] (an identity table for no rotation)
   const float *mlp_norm, *next_norm, *ones, *zeros;
   float eps;
+  bool f32;                      // fp32 weights and activations (default bf16)
 };
 hipError_t enqueue_block(const BlockLaunch& b, hipStream_t s);
-hipError_t launch_norm_rows(const float* h, const float* w, void* y, int M, int W, float eps, hipStream_t s);
+// y[m] = rms(h[m]) (1 + w) in bf16 (or fp32 with f32)
+hipError_t launch_norm_rows(const float* h, const float* w, void* y, int M, int W, float eps, hipStream_t s,
+                            bool f32 = false);
 hipError_t launch_fill_i32(int* p, int n, int v, hipStream_t s);
 hipError_t launch_fill_f32(float* p, int n, float v, hipStream_t s);
 hipError_t launch_identity_rope(float2* tab, int n, hipStream_t s);
 hipError_t launch_bcast_rows(const float* src, float* dst, int M, int period, int W, hipStream_t s);
 
 // emb[k] for k < rows at t = 1 - k/n
+// ---- action-time expert variant (jpi_variant.hip)
+hipError_t launch_const_table(float* tab, const float* norms, int rows, int L, int W, hipStream_t s);
+hipError_t launch_plus_one(const int* src, int* dst, int n, hipStream_t s);
+// u[m] = W_a x[m] + b_a in the context dtype
+hipError_t launch_action_embed(jpi_dtype dt, const float* x, const void* w, const float* b, void* u, int M, int W,
+                               int A, hipStream_t s);
+// z[m] = swish(sum of S split-K slices + c) in the context dtype
+hipError_t launch_swish_slices(jpi_dtype dt, const float* part, int S, int M, const float* c, void* z, int W,
+                               hipStream_t s);
+// key row b and value column 0 of rollout b into slot prefix_len[b] of one layer's K and V^T
+hipError_t launch_put_state_kv(jpi_dtype dt, const void* ks, const void* vst, int vst_ld, void* kp, int64_t kp_bstride,
+                               void* vpt, int64_t vpt_bstride, int vpt_dstride, const int* prefix_len, int B, int Dh,
+                               hipStream_t s);
+
 hipError_t launch_time_embed(float* emb, int rows, int n, int W, hipStream_t s);
 // out[m][n] = act(sum_k in[m][k] w[n][k] + b[n]), fp64 accumulation; act 0 = none, 1 = swish
 hipError_t launch_rowdot(jpi_dtype dt, const float* in, const void* w, const float* b, float* out, int M,

@@ -34,19 +34,32 @@ namespace {
 
 enum TensorKind {
   T_IN_W, T_IN_B, T_TIME0_W, T_TIME0_B, T_TIME1_W, T_TIME1_B, T_ATTN_MOD_W, T_ATTN_MOD_B, T_Q, T_K, T_V, T_O,
-  T_MLP_MOD_W, T_MLP_MOD_B, T_GATE, T_UP, T_DOWN, T_FINAL_MOD_W, T_FINAL_MOD_B, T_OUT_W, T_OUT_B, T_NKINDS
+  T_MLP_MOD_W, T_MLP_MOD_B, T_GATE, T_UP, T_DOWN, T_FINAL_MOD_W, T_FINAL_MOD_B, T_OUT_W, T_OUT_B,
+  // action-time variant
+  T_ATM_IN_W, T_ATM_IN_B, T_ATM_OUT_W, T_ATM_OUT_B, T_STATE_W, T_STATE_B, T_FINAL_NORM, T_ATTN_NORM, T_MLP_NORM,
+  T_NKINDS
 };
 
 const char* kind_suffix[T_NKINDS] = {"action_in.w", "action_in.b", "time_mlp.0.w", "time_mlp.0.b", "time_mlp.1.w",
                                      "time_mlp.1.b", "attn_mod.w", "attn_mod.b", "q.w", "k.w", "v.w", "o.w",
                                      "mlp_mod.w", "mlp_mod.b", "gate.w", "up.w", "down.w", "final_mod.w",
-                                     "final_mod.b", "action_out.w", "action_out.b"};
+                                     "final_mod.b", "action_out.w", "action_out.b", "action_time_mlp_in.w",
+                                     "action_time_mlp_in.b", "action_time_mlp_out.w", "action_time_mlp_out.b",
+                                     "state_proj.w", "state_proj.b", "final_norm.w", "attn_norm.w", "mlp_norm.w"};
 
-bool kind_is_layer(int k) { return k >= T_ATTN_MOD_W && k <= T_DOWN; }
+bool kind_is_layer(int k) { return (k >= T_ATTN_MOD_W && k <= T_DOWN) || k == T_ATTN_NORM || k == T_MLP_NORM; }
 bool kind_is_matrix(int k) {
   return k == T_IN_W || k == T_TIME0_W || k == T_TIME1_W || k == T_ATTN_MOD_W || k == T_Q || k == T_K || k == T_V ||
          k == T_O || k == T_MLP_MOD_W || k == T_GATE || k == T_UP || k == T_DOWN || k == T_FINAL_MOD_W ||
-         k == T_OUT_W;
+         k == T_OUT_W || k == T_ATM_IN_W || k == T_ATM_OUT_W || k == T_STATE_W;
+}
+// tensors each variant takes
+bool kind_in_variant(int k, int variant) {
+  const bool adarms = k == T_TIME0_W || k == T_TIME0_B || k == T_TIME1_W || k == T_TIME1_B || k == T_ATTN_MOD_W ||
+                      k == T_ATTN_MOD_B || k == T_MLP_MOD_W || k == T_MLP_MOD_B || k == T_FINAL_MOD_W ||
+                      k == T_FINAL_MOD_B;
+  const bool action_time = k >= T_ATM_IN_W && k <= T_MLP_NORM;
+  return variant == JPI_VARIANT_ACTION_TIME ? !adarms : !action_time;
 }
 
 struct GraphKey {
@@ -101,6 +114,17 @@ struct jpi_ctx {
   float* corr = nullptr;       // [Bmax][Cmax][W] correction tokens
   int n_corr = 0;
   bool committed_t0 = false;   // committed rows take the t = 0 modulation
+  // action-time variant: weights, robot state and the state token's pass
+  void *w_atm_a = nullptr, *w_atm_t = nullptr, *w_atm_out = nullptr, *w_state = nullptr;  // [W][W] x3, [W][state_dim]
+  float *b_atm_in = nullptr, *b_atm_out = nullptr, *b_state = nullptr;
+  float* norms = nullptr;      // [2L+1][W]: attention and MLP norm of each layer, then the final norm
+  float *ones = nullptr, *zeros = nullptr;
+  float* state = nullptr;      // [Bmax][state_dim]
+  bool state_bound = false;
+  int* d_plen1 = nullptr;      // prefix_len + 1: the action rows also see the state slot
+  float2* rope_s = nullptr;    // [Bmax][Dh/2] the state token's rotation (position prefix_len)
+  float* hs = nullptr;         // [Bmax][W] state token residual
+  void *ys = nullptr, *ks_s = nullptr, *vst_s = nullptr, *u2 = nullptr;
   // activations
   float *x = nullptr, *h = nullptr;
   void *y = nullptr, *q = nullptr, *ks = nullptr, *vst = nullptr, *o = nullptr, *z = nullptr;
@@ -195,6 +219,10 @@ int64_t expected_elems(const jpi_ctx* c, int k) {
     case T_FINAL_MOD_B: return 2 * W;
     case T_OUT_W: return A * W;
     case T_OUT_B: return A;
+    case T_ATM_IN_W: return W * 2 * W;
+    case T_ATM_OUT_W: return W * W;
+    case T_ATM_IN_B: case T_ATM_OUT_B: case T_STATE_B: case T_FINAL_NORM: case T_ATTN_NORM: case T_MLP_NORM: return W;
+    case T_STATE_W: return W * c->cfg.state_dim;
   }
   return -1;
 }
@@ -209,8 +237,8 @@ bool parse_name(const jpi_ctx* c, const char* name, int* kind, int* layer) {
     char* end = nullptr;
     long l = strtol(p, &end, 10);
     if (!end || *end != '.' || l < 0 || l >= c->L) return false;
-    for (int k = T_ATTN_MOD_W; k <= T_DOWN; ++k)
-      if (strcmp(end + 1, kind_suffix[k]) == 0) {
+    for (int k = 0; k < T_NKINDS; ++k)
+      if (kind_is_layer(k) && kind_in_variant(k, c->cfg.variant) && strcmp(end + 1, kind_suffix[k]) == 0) {
         *kind = k;
         *layer = (int)l;
         return true;
@@ -218,7 +246,7 @@ bool parse_name(const jpi_ctx* c, const char* name, int* kind, int* layer) {
     return false;
   }
   for (int k = 0; k < T_NKINDS; ++k)
-    if (!kind_is_layer(k) && strcmp(name, kind_suffix[k]) == 0) {
+    if (!kind_is_layer(k) && kind_in_variant(k, c->cfg.variant) && strcmp(name, kind_suffix[k]) == 0) {
       *kind = k;
       return true;
     }
@@ -267,7 +295,9 @@ jpi_status jpi_destroy(jpi_ctx* c) {
   drop_graphs(c);
   drop_tables(c);
   drop_events(c);
-  void* bufs[] = {c->w_layers, c->w_in, c->w_t0, c->w_t1, c->w_mod, c->w_out, c->b_in, c->b_t0, c->b_t1, c->b_mod,
+  void* bufs[] = {c->w_atm_a, c->w_atm_t, c->w_atm_out, c->w_state, c->b_atm_in, c->b_atm_out, c->b_state, c->norms,
+                  c->ones, c->zeros, c->state, c->d_plen1, c->rope_s, c->hs, c->ys, c->ks_s, c->vst_s, c->u2,
+                  c->w_layers, c->w_in, c->w_t0, c->w_t1, c->w_mod, c->w_out, c->b_in, c->b_t0, c->b_t1, c->b_mod,
                   c->b_out, c->kp, c->vp, c->vpt, c->d_prefix_len, c->rope_tab, c->committed, c->corr, c->x, c->h, c->y, c->q, c->ks,
                   c->vst, c->o, c->z, c->partial, c->opart, c->pflags, c->perr, c->w_frag, c->ysw, c->osw,
                   c->zsw, c->qsw};
@@ -288,6 +318,13 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
       g.action_dim < 1 || g.horizon < 1 || g.max_batch < 1 || g.max_prefix < 0)
     return fail(nullptr, JPI_ERR_ARG, "jpi_create: every dimension must be positive");
   if (g.max_corr < 0 || g.max_corr > 64) return fail(nullptr, JPI_ERR_ARG, "jpi_create: max_corr outside [0, 64]");
+  if (g.variant != JPI_VARIANT_ADARMS && g.variant != JPI_VARIANT_ACTION_TIME)
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: unknown variant");
+  if (g.variant == JPI_VARIANT_ACTION_TIME ? (g.state_dim < 1 || g.state_dim > 4096 || g.max_corr != 0 ||
+                                              g.max_prefix < 1)
+                                           : g.state_dim != 0)
+    return fail(nullptr, JPI_ERR_ARG, "jpi_create: the action-time variant needs 1 <= state_dim <= 4096, max_corr 0 "
+                                      "and max_prefix >= 1; the default variant state_dim 0");
   const int seq_max = g.horizon + g.max_corr;  // suffix rows per rollout
   if (g.n_kv_heads != 1 || g.n_heads % g.n_kv_heads != 0)
     return fail(nullptr, JPI_ERR_ARG, "jpi_create: this version implements exactly one shared KV head");
@@ -387,6 +424,30 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   ALLOC(c->z, M * F * es);
   ALLOC(c->pflags, (size_t)persist_flag_words() * sizeof(unsigned));
   ALLOC(c->perr, 256);
+  if (g.variant == JPI_VARIANT_ACTION_TIME) {
+    const size_t B = c->Bmax, SD = g.state_dim;
+    ALLOC(c->w_atm_a, W * W * es);
+    ALLOC(c->w_atm_t, W * W * es);
+    ALLOC(c->w_atm_out, W * W * es);
+    ALLOC(c->w_state, W * SD * es);
+    ALLOC(c->b_atm_in, W * 4);
+    ALLOC(c->b_atm_out, W * 4);
+    ALLOC(c->b_state, W * 4);
+    ALLOC(c->norms, (2 * (size_t)c->L + 1) * W * 4);
+    ALLOC(c->ones, W * 4);
+    ALLOC(c->zeros, W * 4);
+    ALLOC(c->state, B * SD * 4);
+    ALLOC(c->d_plen1, B * 4);
+    ALLOC(c->rope_s, B * (Dh / 2) * sizeof(float2));
+    ALLOC(c->hs, B * W * 4);
+    ALLOC(c->ys, B * W * es);
+    ALLOC(c->ks_s, B * Dh * es);
+    ALLOC(c->vst_s, B * Dh * 8 * es);
+    ALLOC(c->u2, M * W * es);
+    if (launch_fill_f32(c->ones, (int)W, 1.0f, 0) != hipSuccess || launch_fill_f32(c->zeros, (int)W, 0.0f, 0) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess)
+      return cleanup_fail(fail(c, JPI_ERR_HIP, "fill"));
+  }
 #undef ALLOC
   if (hipMemset(c->perr, 0, 256) != hipSuccess) return cleanup_fail(fail(c, JPI_ERR_HIP, "hipMemset"));
   if (hipHostMalloc((void**)&c->h_prefix_len, c->Bmax * sizeof(int)) != hipSuccess) {
@@ -446,6 +507,15 @@ jpi_status jpi_set_weight(jpi_ctx* c, const char* name, const void* data, int64_
     case T_FINAL_MOD_B: identity((char*)(c->b_mod + (size_t)(6 * c->L) * W), 1, 2 * c->W); break;
     case T_OUT_W: identity((char*)c->w_out, c->A, c->W); break;
     case T_OUT_B: identity((char*)c->b_out, 1, c->A); break;
+    case T_ATM_IN_B: identity((char*)c->b_atm_in, 1, c->W); break;
+    case T_ATM_OUT_W: identity((char*)c->w_atm_out, c->W, c->W); break;
+    case T_ATM_OUT_B: identity((char*)c->b_atm_out, 1, c->W); break;
+    case T_STATE_W: identity((char*)c->w_state, c->W, c->cfg.state_dim); break;
+    case T_STATE_B: identity((char*)c->b_state, 1, c->W); break;
+    case T_FINAL_NORM: identity((char*)(c->norms + (size_t)2 * c->L * W), 1, c->W); break;
+    case T_ATTN_NORM: identity((char*)(c->norms + (size_t)2 * layer * W), 1, c->W); break;
+    case T_MLP_NORM: identity((char*)(c->norms + (size_t)(2 * layer + 1) * W), 1, c->W); break;
+    case T_ATM_IN_W: break;  // split below
     case T_O: identity(lay + c->off_o * c->esz, c->W, (int)(nH * Dh)); break;
     case T_DOWN: identity(lay + c->off_d * c->esz, c->W, c->F); break;
     case T_Q:
@@ -469,7 +539,12 @@ jpi_status jpi_set_weight(jpi_ctx* c, const char* name, const void* data, int64_
       break;
     }
   }
-  if (map.empty()) {
+  if (kind == T_ATM_IN_W) {
+    // [W][2W]: the action columns and the time columns go to two [W][W] matrices
+    const hipMemcpyKind ck = is_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    HIPCHK(c, hipMemcpy2DAsync(c->w_atm_a, W * es, data, 2 * W * es, W * es, W, ck, s));
+    HIPCHK(c, hipMemcpy2DAsync(c->w_atm_t, W * es, (const char*)data + W * es, 2 * W * es, W * es, W, ck, s));
+  } else if (map.empty()) {
     HIPCHK(c, hipMemcpyAsync(base, data, bytes, is_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, s));
   } else {
     void* src = const_cast<void*>(data);
@@ -506,6 +581,7 @@ jpi_status jpi_finalize_weights(jpi_ctx* c, void* stream) {
   (void)stream;
   if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_finalize_weights: ctx is NULL");
   for (int k = 0; k < T_NKINDS; ++k) {
+    if (!kind_in_variant(k, c->cfg.variant)) continue;
     if (kind_is_layer(k)) {
       for (int l = 0; l < c->L; ++l)
         if (!c->have[have_index(c, k, l)])
@@ -546,6 +622,11 @@ jpi_status jpi_bind_prefix(jpi_ctx* c, const void* k, const void* v, const int32
                                            std::to_string(prefix_len_host[b]) + " outside [0, prefix]");
       lens[b] = prefix_len_host[b];
     }
+  if (c->cfg.variant == JPI_VARIANT_ACTION_TIME)
+    for (int b = 0; b < batch; ++b)
+      if (lens[b] >= c->Pmax)
+        return fail(c, JPI_ERR_SHAPE, "jpi_bind_prefix: the action-time variant keeps prefix slot prefix_len free "
+                                      "for the state token, so every prefix_len must be below max_prefix");
   HIPCHK(c, hipSetDevice(c->device));
   hipStream_t s = (hipStream_t)stream;
   HIPCHK(c, hipStreamSynchronize(s));  // staging buffer and resident KV are free to overwrite
@@ -572,7 +653,10 @@ jpi_status jpi_bind_prefix(jpi_ctx* c, const void* k, const void* v, const int32
   }
   memcpy(c->h_prefix_len, lens.data(), batch * sizeof(int));
   HIPCHK(c, hipMemcpyAsync(c->d_prefix_len, c->h_prefix_len, batch * sizeof(int), hipMemcpyHostToDevice, s));
-  if (c->batch != batch) c->n_fixed = c->n_corr = 0;  // state rows were bound for another batch
+  if (c->batch != batch) {  // state rows were bound for another batch
+    c->n_fixed = c->n_corr = 0;
+    c->state_bound = false;
+  }
   HIPCHK(c, launch_rope_table(c->d_prefix_len, c->rope_tab, batch, c->H + c->n_corr, c->Dh, c->cfg.rope_base, s));
   c->rope_rows = c->H + c->n_corr;
   c->batch = batch;
@@ -591,6 +675,8 @@ jpi_status jpi_bind_state(jpi_ctx* c, const float* committed_dev, int n_fixed, c
   if (n_corr < 0 || n_corr > c->Cmax)
     return fail(c, JPI_ERR_ARG, "jpi_bind_state: n_corr must be in [0, max_corr=" + std::to_string(c->Cmax) + "]");
   if (n_corr > 0 && !corr_tokens) return fail(c, JPI_ERR_ARG, "jpi_bind_state: corr_tokens is NULL");
+  if (n_corr > 0 && c->cfg.variant != JPI_VARIANT_ADARMS)
+    return fail(c, JPI_ERR_UNSUPPORTED, "jpi_bind_state: correction tokens need the adaRMS variant");
   HIPCHK(c, hipSetDevice(c->device));
   hipStream_t s = (hipStream_t)stream;
   if (n_fixed > 0)
@@ -617,7 +703,7 @@ jpi_status ensure_table(jpi_ctx* c, int n_steps, hipStream_t s, float** out) {
   const size_t W = c->W;
   const int rows = n_steps + 1;  // t_0 .. t_{N-1}, then t = 0
   float *tab = nullptr, *tmp = nullptr;
-  TRY(dmalloc(c, (void**)&tab, (size_t)rows * c->R * sizeof(float)));
+  TRY(dmalloc(c, (void**)&tab, (size_t)rows * (c->R + W) * sizeof(float)));  // + [rows][W] for the variant
   jpi_status st = dmalloc(c, (void**)&tmp, (size_t)3 * rows * W * sizeof(float));
   if (st != JPI_OK) {
     (void)hipFree(tab);
@@ -625,9 +711,17 @@ jpi_status ensure_table(jpi_ctx* c, int n_steps, hipStream_t s, float** out) {
   }
   float *emb = tmp, *c1 = tmp + rows * W, *cond = tmp + 2 * rows * W;
   hipError_t e = launch_time_embed(emb, rows, n_steps, c->W, s);
-  if (e == hipSuccess) e = launch_rowdot(c->dt, emb, c->w_t0, c->b_t0, c1, rows, c->W, c->W, 1, s);
-  if (e == hipSuccess) e = launch_rowdot(c->dt, c1, c->w_t1, c->b_t1, cond, rows, c->W, c->W, 1, s);
-  if (e == hipSuccess) e = launch_rowdot(c->dt, cond, c->w_mod, c->b_mod, tab, rows, c->R, c->W, 0, s);
+  if (c->cfg.variant == JPI_VARIANT_ACTION_TIME) {
+    // plain RMSNorm layers: every row (scale, shift, gate) = (w, 0, 1); then, after the
+    // table, the time half of the action-time MLP's first layer at each t: W_t e(t) + b_i
+    if (e == hipSuccess) e = launch_const_table(tab, c->norms, rows, c->L, c->W, s);
+    if (e == hipSuccess)
+      e = launch_rowdot(c->dt, emb, c->w_atm_t, c->b_atm_in, tab + (size_t)rows * c->R, rows, c->W, c->W, 0, s);
+  } else {
+    if (e == hipSuccess) e = launch_rowdot(c->dt, emb, c->w_t0, c->b_t0, c1, rows, c->W, c->W, 1, s);
+    if (e == hipSuccess) e = launch_rowdot(c->dt, c1, c->w_t1, c->b_t1, cond, rows, c->W, c->W, 1, s);
+    if (e == hipSuccess) e = launch_rowdot(c->dt, cond, c->w_mod, c->b_mod, tab, rows, c->R, c->W, 0, s);
+  }
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   (void)hipFree(tmp);
   if (e != hipSuccess) {
@@ -643,11 +737,15 @@ struct StepGemms {
   int M;
   int s_o, s_d;  // split-K of the O and Down projections (QKV and GateUp are not split)
   bool persist;  // single-launch path
+  // action-time variant: split-K of the action-time MLP's two GEMMs, and of the
+  // state token's O and Down projections (M = batch rows)
+  int s_a = 1, s_so = 1, s_sd = 1;
 };
 
 bool use_persist(jpi_ctx* c, int batch) {
   const char* e = getenv("JPI_PERSIST");
   if (e && e[0] == '0') return false;
+  if (c->cfg.variant != JPI_VARIANT_ADARMS) return false;  // the single-launch kernel runs the adaRMS expert
   const int S = c->H + c->n_corr;  // suffix rows per rollout
   if (!persist_supported(c->dt, batch * S, c->W, c->nH, c->Dh, c->F, S, c->A, c->Pmax)) return false;
   if (c->n_cu > persist_max_grid()) return false;
@@ -673,12 +771,18 @@ StepGemms plan_gemms(jpi_ctx* c, int batch) {
     p.s_o = gemm_pick_splitk(c->dt, p.M, c->W, c->nH * c->Dh, c->n_cu);
     p.s_d = gemm_pick_splitk(c->dt, p.M, c->W, c->F, c->n_cu);
   }
+  if (c->cfg.variant == JPI_VARIANT_ACTION_TIME) {
+    p.s_a = gemm_pick_splitk(c->dt, p.M, c->W, c->W, c->n_cu);
+    p.s_so = gemm_pick_splitk(c->dt, batch, c->W, c->nH * c->Dh, c->n_cu);
+    p.s_sd = gemm_pick_splitk(c->dt, batch, c->W, c->F, c->n_cu);
+  }
   return p;
 }
 
 jpi_status ensure_scratch(jpi_ctx* c, int batch, int prefix) {
   const StepGemms p = plan_gemms(c, batch);
-  const size_t need = (size_t)std::max(p.s_o, p.s_d) * p.M * c->W;
+  const size_t need = std::max((size_t)std::max(std::max(p.s_o, p.s_d), p.s_a) * p.M * c->W,
+                               (size_t)std::max(p.s_so, p.s_sd) * batch * c->W);
   bool changed = false;
   if (need > c->partial_cap) {
     if (c->partial) (void)hipFree(c->partial);
@@ -747,7 +851,12 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
   const StepGemms p = plan_gemms(c, batch);
   const int M = p.M, W = c->W, Dh = c->Dh, nH = c->nH, F = c->F, L = c->L;
   const size_t es = c->esz;
-  const int nch = attn_n_chunks(c->dt, prefix, S);
+  // action-time variant: the state token sits in prefix slot prefix_len, so the
+  // action rows see prefix_len + 1 keys there and start at position prefix_len + 1
+  const bool at = c->cfg.variant == JPI_VARIANT_ACTION_TIME;
+  const int* plen_act = at ? c->d_plen1 : c->d_prefix_len;
+  const int P_act = at ? prefix + 1 : prefix;
+  const int nch = attn_n_chunks(c->dt, P_act, S);
   const float eps = c->cfg.rms_eps;
   const float dt_step = -1.0f / (float)n_steps;
   hipError_t e;
@@ -831,13 +940,103 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     ENQ(launch_persist(pa, c->n_cu, s));
     return hipSuccess;
   }
-  const int n_t0 = c->committed_t0 ? c->n_fixed : 0;
+  const int n_t0 = c->committed_t0 && !at ? c->n_fixed : 0;
+  if (at) {
+    // the state token: W_s s + b_s, then every layer over it alone (it sees the prefix
+    // and itself); each layer's key and value go into prefix slot prefix_len
+    ENQ(launch_plus_one(c->d_prefix_len, c->d_plen1, batch, s));
+    ENQ(launch_rope_table(c->d_plen1, c->rope_tab, batch, H, Dh, c->cfg.rope_base, s));
+    ENQ(launch_rope_table(c->d_prefix_len, c->rope_s, batch, 1, Dh, c->cfg.rope_base, s));
+    ENQ(launch_rowdot(c->dt, c->state, c->w_state, c->b_state, c->hs, batch, W, c->cfg.state_dim, 0, s));
+    ENQ(launch_norm_rows(c->hs, c->norms, c->ys, batch, W, eps, s, c->dt == JPI_F32));
+    BlockLaunch b{};
+    b.B = batch;
+    b.H = 1;
+    b.W = W;
+    b.nH = nH;
+    b.Dh = Dh;
+    b.F = F;
+    b.n_cu = c->n_cu;
+    b.off_o = c->off_o;
+    b.off_gu = c->off_gu;
+    b.off_d = c->off_d;
+    b.h = c->hs;
+    b.y = c->ys;
+    b.q = c->q;
+    b.o = c->o;
+    b.z = c->z;
+    b.partial = c->partial;
+    b.s_o = p.s_so;
+    b.s_d = p.s_sd;
+    b.opart = c->opart;
+    b.ks = c->ks_s;
+    b.ks_bstride = 0;
+    b.vst = c->vst_s;
+    b.vst_ld = 8;
+    b.kp_bstride = (int64_t)c->Pmax * Dh;
+    b.vpt_bstride = (int64_t)c->Ppad * Dh;
+    b.vpt_dstride = c->Ppad;
+    b.prefix_len = c->d_prefix_len;
+    b.P = prefix;
+    b.rope = c->rope_s;
+    b.ones = c->ones;
+    b.zeros = c->zeros;
+    b.eps = eps;
+    b.f32 = c->dt == JPI_F32;
+    for (int l = 0; l < L; ++l) {
+      b.w = (const char*)c->w_layers + (size_t)l * c->layer_elems * es;
+      char* kl = (char*)c->kp + (size_t)l * c->Bmax * c->Pmax * Dh * es;
+      char* vl = (char*)c->vpt + (size_t)l * c->Bmax * c->Ppad * Dh * es;
+      b.kp = kl;
+      b.vpt = vl;
+      b.mlp_norm = c->norms + (size_t)(2 * l + 1) * W;
+      b.next_norm = c->norms + (size_t)(l + 1 < L ? 2 * (l + 1) : 2 * L) * W;
+      ENQ(enqueue_block(b, s));
+      ENQ(launch_put_state_kv(c->dt, c->ks_s, c->vst_s, 8, kl, b.kp_bstride, vl, b.vpt_bstride, b.vpt_dstride,
+                              c->d_prefix_len, batch, Dh, s));
+    }
+  }
+  const float* ctab = table + (size_t)(n_steps + 1) * c->R;  // action-time variant: W_t e(t_k) + b_i rows
   for (int k = 0; k < n_steps; ++k) {
     const float* tk = table + (size_t)k * c->R;
     const float* fm = tk + (size_t)(6 * L) * W;
     const int64_t t0_delta = (int64_t)(n_steps - k) * c->R;  // to the t = 0 row
-    ENQ(launch_inproj_norm(c->dt, c->x, c->w_in, c->b_in, c->h, tk, tk + W, c->y, M, W, c->A, eps, c->corr, C, H,
-                           n_t0, t0_delta, s));
+    if (at) {
+      // h = W_o swish(W_i [W_a x + b_a ; e(t_k)] + b_i) + b_o, then the first norm
+      ENQ(launch_action_embed(c->dt, c->x, c->w_in, c->b_in, c->y, M, W, c->A, s));
+      GemmLaunch g{};
+      g.M = M;
+      g.A = c->y;
+      g.W = c->w_atm_a;
+      g.N = W;
+      g.K = W;
+      g.splitk = p.s_a;
+      g.epi = EPI_STORE_F32;
+      g.ep.out_f32 = c->partial;
+      g.n_cu = c->n_cu;
+      ENQ(launch_gemm(c->dt, g, s));
+      ENQ(launch_swish_slices(c->dt, c->partial, p.s_a, M, ctab + (size_t)k * W, c->u2, W, s));
+      g.A = c->u2;
+      g.W = c->w_atm_out;
+      ENQ(launch_gemm(c->dt, g, s));
+      ENQ(launch_bcast_rows(c->b_atm_out, c->h, M, 1, W, s));
+      RowLaunch r{};
+      r.part = c->partial;
+      r.S = p.s_a;
+      r.M = M;
+      r.W = W;
+      r.h = c->h;
+      r.gate = tk + 2 * W;  // ones in the plain-norm table
+      r.scale = tk;
+      r.shift = tk + W;
+      r.y = c->y;
+      r.eps = eps;
+      r.horizon = H;
+      ENQ(launch_resid_norm(c->dt, r, false, s));
+    } else {
+      ENQ(launch_inproj_norm(c->dt, c->x, c->w_in, c->b_in, c->h, tk, tk + W, c->y, M, W, c->A, eps, c->corr, C, H,
+                             n_t0, t0_delta, s));
+    }
     for (int l = 0; l < L; ++l) {
       const char* lay = (const char*)c->w_layers + (size_t)l * c->layer_elems * es;
       const float* am = tk + (size_t)(2 * l) * 3 * W;
@@ -873,11 +1072,11 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
       a.kp_bstride = (int64_t)c->Pmax * Dh;
       a.vpt_bstride = (int64_t)c->Ppad * Dh;
       a.vpt_dstride = c->Ppad;
-      a.prefix_len = c->d_prefix_len;
+      a.prefix_len = plen_act;
       a.B = batch;
       a.nH = nH;
       a.H = S;
-      a.P = prefix;
+      a.P = P_act;
       a.Dh = Dh;
       a.opart = c->opart;
       a.mpart = c->opart + (size_t)batch * nH * nch * S * Dh;
@@ -982,11 +1181,14 @@ jpi_status jpi_denoise(jpi_ctx* c, const float* noise_dev, int n_steps, float* a
   if (n_steps < 1) return fail(c, JPI_ERR_ARG, "jpi_denoise: n_steps must be >= 1");
   if (!c->finalized) return fail(c, JPI_ERR_STATE, "jpi_denoise: weights are not finalized");
   if (!c->prefix_bound) return fail(c, JPI_ERR_STATE, "jpi_denoise: no prefix bound");
+  if (c->cfg.variant == JPI_VARIANT_ACTION_TIME && !c->state_bound)
+    return fail(c, JPI_ERR_STATE, "jpi_denoise: the action-time variant needs jpi_bind_robot_state");
   HIPCHK(c, hipSetDevice(c->device));
   hipStream_t s = (hipStream_t)stream;
   float* table = nullptr;
   TRY(ensure_table(c, n_steps, s, &table));
-  TRY(ensure_scratch(c, c->batch, c->prefix));
+  // the action-time variant's action rows also see the state token's prefix slot
+  TRY(ensure_scratch(c, c->batch, c->prefix + (c->cfg.variant == JPI_VARIANT_ACTION_TIME ? 1 : 0)));
   if (use_persist(c, c->batch)) TRY(ensure_frag(c, s));
   HIPCHK(c, launch_init_x(noise_dev, c->committed, c->x, c->batch, c->H, c->A, c->n_fixed, s));
   if (c->rope_rows != c->H + c->n_corr) {  // the suffix length changed since the table was built
@@ -1018,6 +1220,19 @@ jpi_status jpi_denoise(jpi_ctx* c, const float* noise_dev, int n_steps, float* a
   }
   HIPCHK(c, hipMemcpyAsync(actions_dev, c->x, (size_t)c->batch * c->H * c->A * sizeof(float),
                            hipMemcpyDeviceToDevice, s));
+  return JPI_OK;
+}
+
+jpi_status jpi_bind_robot_state(jpi_ctx* c, const float* state_dev, void* stream) {
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_bind_robot_state: ctx is NULL");
+  if (c->cfg.variant != JPI_VARIANT_ACTION_TIME)
+    return fail(c, JPI_ERR_UNSUPPORTED, "jpi_bind_robot_state: only the action-time variant takes a robot state");
+  if (!state_dev) return fail(c, JPI_ERR_ARG, "jpi_bind_robot_state: state is NULL");
+  if (!c->prefix_bound) return fail(c, JPI_ERR_STATE, "jpi_bind_robot_state: bind the prefix first (it sets the batch)");
+  HIPCHK(c, hipSetDevice(c->device));
+  HIPCHK(c, hipMemcpyAsync(c->state, state_dev, (size_t)c->batch * c->cfg.state_dim * sizeof(float),
+                           hipMemcpyDeviceToDevice, (hipStream_t)stream));
+  c->state_bound = true;
   return JPI_OK;
 }
 
@@ -1199,6 +1414,10 @@ jpi_status jpi::ae_prefix_target(jpi_ctx* c, int L, int Dh, jpi_dtype dt, int ba
     *why = "batch or prefix exceeds the action expert's max_batch / max_prefix";
     return JPI_ERR_SHAPE;
   }
+  if (c->cfg.variant == JPI_VARIANT_ACTION_TIME && prefix >= c->Pmax) {
+    *why = "the action-time variant keeps prefix slot prefix_len free for the state token (prefix < max_prefix)";
+    return JPI_ERR_SHAPE;
+  }
   t->kp = c->kp;
   t->vpt = c->vpt;
   t->kp_bstride = (int64_t)c->Pmax * Dh;
@@ -1214,7 +1433,10 @@ jpi_status jpi::ae_prefix_target(jpi_ctx* c, int L, int Dh, jpi_dtype dt, int ba
 }
 
 jpi_status jpi::ae_prefix_bound(jpi_ctx* c, int batch, int prefix, int rope_rows) {
-  if (c->batch != batch) c->n_fixed = c->n_corr = 0;  // state rows were bound for another batch
+  if (c->batch != batch) {  // state rows were bound for another batch
+    c->n_fixed = c->n_corr = 0;
+    c->state_bound = false;
+  }
   c->rope_rows = rope_rows;  // jpi_denoise rebuilds the table if the suffix length differs
   c->batch = batch;
   c->prefix = prefix;

@@ -28,11 +28,13 @@ class ActionExpert:
     """One libjpi context on one GPU."""
 
     def __init__(self, dims, dtype: str, max_batch: int, max_prefix: int, device: int = 0,
-                 rms_eps: float = 1e-6, rope_base: float = 1e4, max_corr: int = 0):
+                 rms_eps: float = 1e-6, rope_base: float = 1e4, max_corr: int = 0, variant: int = 0,
+                 state_dim: int = 0):
+        """variant: jpi.JPI_VARIANT_ADARMS (0) or JPI_VARIANT_ACTION_TIME (1, with state_dim)."""
         self.dims, self.dtype, self.device = dims, dtype, device
         cfg = _j.jpi_config(dims.n_layers, dims.width, dims.n_heads, dims.n_kv_heads, dims.head_dim,
                             dims.mlp_dim, dims.action_dim, dims.horizon, max_batch, max_prefix, _dt(dtype),
-                            rms_eps, rope_base, max_corr)
+                            rms_eps, rope_base, max_corr, variant, state_dim)
         st, ctx = _j.jpi_create(cfg, device)
         _j.check(st, None)
         self.ctx = ctx
@@ -70,6 +72,10 @@ class ActionExpert:
         """committed: device [B][n_fixed][A] fp32; corr: device [B][n_corr][W] fp32 correction tokens."""
         n_corr = 0 if corr is None else int(corr.shape[1])
         self._chk(_j.jpi_bind_state(self.ctx, committed, n_fixed, corr, n_corr, stream))
+
+    def bind_robot_state(self, state: torch.Tensor, stream=None):
+        """state: device [B][state_dim] fp32 (action-time variant)."""
+        self._chk(_j.jpi_bind_robot_state(self.ctx, state, stream))
 
     def set_committed_t0(self, enable: bool):
         """Committed rows at flow time t = 0 (True) or at the step's t (False, the default)."""

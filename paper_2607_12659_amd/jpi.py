@@ -17,12 +17,13 @@ LIB_PATH = os.path.join(_HERE, "libjpi.so")
 
 JPI_OK, JPI_ERR_ARG, JPI_ERR_SHAPE, JPI_ERR_DTYPE, JPI_ERR_STATE, JPI_ERR_OOM, JPI_ERR_HIP, JPI_ERR_UNSUPPORTED = range(8)
 JPI_F32, JPI_BF16 = 0, 1
+JPI_VARIANT_ADARMS, JPI_VARIANT_ACTION_TIME = 0, 1
 
 EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create", "jpi_destroy", "jpi_set_weight",
             "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
             "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
             "jpi_sched_run", "jpi_sched_sim_hooks", "jpi_vlm_create", "jpi_vlm_destroy", "jpi_vlm_set_weight",
-            "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error", "jpi_set_committed_t0", "jpi_corr_create",
+            "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error", "jpi_set_committed_t0", "jpi_bind_robot_state", "jpi_corr_create",
             "jpi_corr_destroy", "jpi_corr_set_weight", "jpi_corr_finalize_weights", "jpi_corr_compress",
             "jpi_corr_predict", "jpi_corr_last_error"]
 JPI_KERNEL_NONE, JPI_KERNEL_QKV, JPI_KERNEL_ATTENTION, JPI_KERNEL_OPROJ, JPI_KERNEL_GATEUP, JPI_KERNEL_DOWN, \
@@ -34,7 +35,8 @@ class jpi_config(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int), ("head_dim", ctypes.c_int), ("mlp_dim", ctypes.c_int),
                 ("action_dim", ctypes.c_int), ("horizon", ctypes.c_int), ("max_batch", ctypes.c_int),
                 ("max_prefix", ctypes.c_int), ("dtype", ctypes.c_int), ("rms_eps", ctypes.c_float),
-                ("rope_base", ctypes.c_float), ("max_corr", ctypes.c_int)]
+                ("rope_base", ctypes.c_float), ("max_corr", ctypes.c_int), ("variant", ctypes.c_int),
+                ("state_dim", ctypes.c_int)]
 
 
 # include/jpi_vlm.h
@@ -129,6 +131,7 @@ _sig = {
     "jpi_vlm_prefill": (_i, [_vp, _vp, _i, _i, _vp, _vp, _vp]),
     "jpi_vlm_last_error": (ctypes.c_char_p, [_vp]),
     "jpi_set_committed_t0": (_i, [_vp, _i]),
+    "jpi_bind_robot_state": (_i, [_vp, _vp, _vp]),
     "jpi_corr_create": (_i, [ctypes.POINTER(jpi_corr_config), _i, ctypes.POINTER(_vp)]),
     "jpi_corr_destroy": (_i, [_vp]),
     "jpi_corr_set_weight": (_i, [_vp, ctypes.c_char_p, _vp, _i64, _i, _i, _vp]),
@@ -289,6 +292,10 @@ def jpi_vlm_last_error(vlm) -> str:
 
 def jpi_set_committed_t0(ctx, enable: int) -> int:
     return _lib.jpi_set_committed_t0(ctx, enable)
+
+
+def jpi_bind_robot_state(ctx, state_dev, stream=None) -> int:
+    return _lib.jpi_bind_robot_state(ctx, addr(state_dev), stream_handle(stream))
 
 
 def jpi_corr_create(cfg: jpi_corr_config, device: int = 0):

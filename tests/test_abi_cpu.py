@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     j = _lib()
-    assert j.jpi_abi_version() == 2
+    assert j.jpi_abi_version() == 3
     for st in range(8):
         assert j.jpi_status_str(st)
     assert j.jpi_status_str(99) == "unknown status"

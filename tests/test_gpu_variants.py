@@ -88,3 +88,109 @@ def test_pi05_committed10_at_t0():
         assert rel <= BF16_TOL
         assert np.array_equal(out[:, :10].astype(np.float32), com)
     assert np.array_equal(got, again)
+
+
+# ---------------------------------------------------------------------------
+# the action-time (pi0-style) expert
+# ---------------------------------------------------------------------------
+from oracle import pi0 as opi0  # noqa: E402
+from synth import pi0 as spi0  # noqa: E402
+
+
+def _pi0_expert(wl, w, max_batch, max_prefix, state_dim=spi0.STATE_DIM):
+    from paper_2607_12659_amd import jpi
+    from paper_2607_12659_amd.expert import ActionExpert
+    ae = ActionExpert(wl.dims, wl.dtype, max_batch, max_prefix, variant=jpi.JPI_VARIANT_ACTION_TIME,
+                      state_dim=state_dim)
+    ae.load_weights(w)
+    return ae
+
+
+def _pi0_run(ae, K, V, noise, n_steps, lens, state, committed=None, n_fixed=0):
+    from paper_2607_12659_amd.expert import to_device
+    torch = torch_cuda()
+    ae.bind_prefix(to_device(K), to_device(V), lens)
+    ae.bind_state(None if committed is None else to_device(np.ascontiguousarray(committed, np.float32)), n_fixed)
+    ae.bind_robot_state(to_device(np.ascontiguousarray(state, np.float32)))
+    out = ae.denoise(to_device(np.ascontiguousarray(noise, np.float32)), n_steps)
+    ae.sync()
+    torch.cuda.synchronize()
+    return out.cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tiny_action_time_variant(dtype):
+    torch_cuda()
+    wl = synth.WORKLOADS["tiny-fp32"].with_(dtype=dtype, batch=2, n_fixed=2, prefix_len=(64, 9),
+                                            name="tiny-pi0-%s" % dtype)
+    print("case tiny action-time variant %s, prefix_len %s" % (dtype, wl.prefix_len), flush=True)
+    w = spi0.make_pi0_weights(wl, std=0.1)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    com = synth.make_committed(wl)
+    st = spi0.make_state(wl)
+    lens = list(wl.prefix_len)
+    ae = _pi0_expert(wl, w, 2, wl.prefix + 1)
+    try:
+        got = _pi0_run(ae, K, V, noise, wl.n_steps, lens, st, com, 2)
+        again = _pi0_run(ae, K, V, noise, wl.n_steps, lens, st, com, 2)
+        moved = _pi0_run(ae, K, V, noise, wl.n_steps, lens, st * 3.0, com, 2)
+    finally:
+        ae.close()
+    ref = opi0.denoise(wl.dims, w, noise, K, V, lens, wl.n_steps, st, committed=com, n_fixed=2)
+    ref3 = opi0.denoise(wl.dims, w, noise, K, V, lens, wl.n_steps, st * 3.0, committed=com, n_fixed=2)
+    err, rel = np.abs(got - ref).max(), rel_l2_per_rollout(got, ref)
+    effect = np.abs(ref3 - ref).max()
+    print("max-abs %.3e rel-L2 %.3e; tripling the state moves the actions by %.3e (GPU: %.3e)"
+          % (err, rel, effect, np.abs(moved - got).max()), flush=True)
+    if dtype == "f32":
+        assert err <= F32_TOL
+        assert np.abs(moved - ref3).max() <= F32_TOL
+    else:
+        assert rel <= BF16_TOL and rel_l2_per_rollout(moved, ref3) <= BF16_TOL
+    assert effect > 20 * max(err, 1e-6)
+    assert np.array_equal(got, again)
+    assert np.array_equal(got[:, :2].astype(np.float32), com.astype(np.float32))
+
+
+def test_action_time_variant_rejects_a_full_prefix_and_needs_the_state():
+    torch = torch_cuda()
+    from paper_2607_12659_amd import jpi
+    from paper_2607_12659_amd.expert import to_device
+    wl = synth.WORKLOADS["tiny-fp32"]
+    w = spi0.make_pi0_weights(wl)
+    K, V = synth.make_prefix(wl)
+    ae = _pi0_expert(wl, w, 1, wl.prefix)
+    try:
+        # every prefix slot taken: no room for the state token
+        assert jpi.jpi_bind_prefix(ae.ctx, to_device(K), to_device(V), None, 1, wl.prefix, None) == jpi.JPI_ERR_SHAPE
+        assert jpi.jpi_bind_prefix(ae.ctx, to_device(K), to_device(V), [wl.prefix - 1], 1, wl.prefix, None) == jpi.JPI_OK
+        noise = to_device(synth.make_noise(wl).astype(np.float32))
+        assert jpi.jpi_denoise(ae.ctx, noise, 2, noise, None) == jpi.JPI_ERR_STATE   # no robot state yet
+        assert jpi.jpi_set_weight(ae.ctx, "time_mlp.0.w", np.zeros(wl.dims.width ** 2, np.float32),
+                                  wl.dims.width ** 2, jpi.JPI_F32, 0, None) == jpi.JPI_ERR_ARG
+        torch.cuda.synchronize()
+    finally:
+        ae.close()
+
+
+def test_pi0_shape_action_time_variant():
+    """The pi0-style expert at the pi0.5 shape (18 layers, width 1024, 8 x 256,
+    816-token prefix slots with 815 valid, 10 committed rows) against the
+    stored oracle output."""
+    torch_cuda()
+    ref, meta = load_golden("pi0-b1")
+    assert meta["variant"] == "action_time"
+    wl = synth.WORKLOADS["pi05-b1-committed10"].with_(name="pi0-b1", prefix_len=(815,))
+    print("case pi0-b1", flush=True)
+    w = spi0.make_pi0_weights(wl)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    ae = _pi0_expert(wl, w, 1, 816)
+    try:
+        got = _pi0_run(ae, K, V, noise, wl.n_steps, [815], spi0.make_state(wl), synth.make_committed(wl), 10)
+    finally:
+        ae.close()
+    rel = rel_l2_per_rollout(got, ref)
+    print("rel-L2 %.3e max-abs %.3e" % (rel, np.abs(got - ref).max()), flush=True)
+    assert rel <= BF16_TOL
