@@ -46,10 +46,10 @@ METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roof
 # sha256 of the kernel source they were measured on; the byte counts are the
 # counter readings times the copy calibration factor.
 MEASURED_TRAFFIC = {
-    # pi0.5 shape, batch 1: FETCH_SIZE 5269989.5 KiB x 1.99980 (a 256 MiB copy
-    # reads back 131085.25 KiB) + WRITE_SIZE 2007096.2 KiB x 1.00000 (the copy's
+    # pi0.5 shape, batch 1: FETCH_SIZE 5271318.5 KiB x 1.99980 (a 256 MiB copy
+    # reads back 131085.17 KiB) + WRITE_SIZE 2007096.2 KiB x 1.00000 (the copy's
     # 262144 KiB), mean over 29 dispatches
-    ("f471df150c702af926344b09f1d035fe028a52a76f76b106143f1b819aa69089", "pi05-b1"): 12847114162,
+    ("7ef5595361ede87fdd8c4c82b42bbc4d76dc671ba2f8b002d6400112cc848a76", "pi05-b1"): 12849842414,
 }
 
 
@@ -382,6 +382,94 @@ def bench_corr(args, cwl):
     print(json.dumps(result), flush=True)
 
 
+def pi0_bytes(d, wl):
+    """Algorithmic HBM bytes of one call of the action-time (pi0-style) expert:
+    per Euler step every layer matrix and the action-time MLP once plus each
+    rollout's valid prefix KV (and the state slot); once per call the state
+    token's pass over every layer matrix and the prefix KV."""
+    import numpy as np
+    import synth.pi0 as synth_pi0
+    es = 2 if wl.dtype == "bf16" else 4
+    layer = sum(int(np.prod(s)) * es for n, s, mat in synth_pi0.pi0_weight_specs(d) if mat and n.startswith("layers."))
+    mlp = sum(int(np.prod(s)) * es for n, s, mat in synth_pi0.pi0_weight_specs(d)
+              if mat and n.startswith("action_time_mlp"))
+    kv = sum(wl.valid_lengths()) * d.n_layers * d.head_dim * 2 * es
+    return wl.n_steps * (layer + mlp + kv + wl.batch * d.n_layers * d.head_dim * 2 * es) + layer + kv
+
+
+def bench_pi0(args, wl):
+    """The action-time (pi0-style) expert: one step = one jpi_denoise call
+    (the state token's pass, then N Euler steps) at the pi0.5 shape."""
+    import numpy as np
+    import torch
+
+    import synth
+    import synth.pi0 as synth_pi0
+    from paper_2607_12659_amd import jpi
+    from paper_2607_12659_amd.expert import ActionExpert, to_device
+
+    d = wl.dims
+    print("bench: workload %s" % wl.name, file=sys.stderr, flush=True)
+    w = synth_pi0.make_pi0_weights(wl)
+    K, V = synth.make_prefix(wl)
+    noise = synth.make_noise(wl)
+    st = synth_pi0.make_state(wl)
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    ae = ActionExpert(d, wl.dtype, wl.batch, wl.prefix + 1, variant=jpi.JPI_VARIANT_ACTION_TIME,
+                      state_dim=synth_pi0.STATE_DIM)
+    ae.load_weights(w)
+    ae.bind_prefix(to_device(K), to_device(V), wl.valid_lengths(), stream=stream)
+    ae.bind_state(None, 0, stream=stream)
+    ae.bind_robot_state(to_device(st.astype(np.float32)), stream=stream)
+    nd = to_device(noise.astype(np.float32))
+    out = torch.empty_like(nd)
+    for _ in range(args.warmup):
+        ae.denoise(nd, wl.n_steps, out=out, stream=stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        ae.denoise(nd, wl.n_steps, out=out, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ae.sync()
+    ms = e0.elapsed_time(e1) / args.steps
+    finite = bool(torch.isfinite(out).all().item())
+    ae.close()
+    byts = pi0_bytes(d, wl)
+    gbs = byts / (ms * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu:
+        import oracle
+        calls, t0 = 0, time.time()
+        while True:
+            oracle.pi0.denoise(d, w, noise[:1], K[:, :1], V[:, :1], wl.valid_lengths()[:1], wl.n_steps, st[:1])
+            calls += 1
+            if time.time() - t0 >= 10.0:
+                break
+        dt = time.time() - t0
+        cpu = {"value": round(calls / dt, 4), "unit": "chunks/s", "cores": os.cpu_count(), "kind": "oracle",
+               "sample": "%d repeated %d-step fp64 oracle denoise calls of rollout 0 (%.1f s)" % (calls, wl.n_steps, dt)}
+    result = {
+        "metric": "action chunks/sec (10-step flow denoise, action-time pi0-style expert, pi0.5 shape, B=1)",
+        "value": round(wl.batch / (ms * 1e-3), 3), "unit": "chunks/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "prefix_tokens": wl.valid_lengths(), "horizon": d.horizon,
+                   "layers": d.n_layers, "width": d.width, "n_steps": wl.n_steps, "variant": "action_time",
+                   "state_dim": synth_pi0.STATE_DIM},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "bytes_per_launch": byts,
+                     "avg_launch_us": round(ms * 1e3, 1), "note": "whole call on the multi-kernel graph"},
+        "cpu_baseline": cpu, "outputs_finite": finite,
+    }
+    print(json.dumps(result), flush=True)
+
+
+PI0_WORKLOADS = ("pi0-b1",)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -416,6 +504,10 @@ def main():
         return
     if args.workload in synth_corr.CORR_WORKLOADS:
         bench_corr(args, synth_corr.CORR_WORKLOADS[args.workload])
+        return
+    if args.workload in PI0_WORKLOADS:
+        # the pi0.5 shape with one prefix slot left for the robot-state token
+        bench_pi0(args, synth.WORKLOADS["pi05-b1"].with_(name="pi0-b1", prefix_len=(815,)))
         return
     wl = synth.WORKLOADS[args.workload]
     print("bench: workload %s, generating inputs" % wl.name, file=sys.stderr, flush=True)
