@@ -273,3 +273,68 @@ def test_correction_item_into_the_expert():
     finally:
         ae.close()
         m.close()
+
+
+def test_tiny_bf16_batch8_correction_rows_multikernel():
+    """Eight rollouts of 4 correction + 10 action rows (112 rows: the
+    multi-kernel path with several query tiles per rollout group), ragged
+    prefixes including an empty one, committed rows, against the oracle."""
+    torch_cuda()
+    wl = synth.WORKLOADS["tiny-fp32"].with_(dtype="bf16", batch=8, n_fixed=1, name="tiny-bf16-corr-b8")
+    lens = [64, 0, 17, 64, 1, 33, 63, 8]
+    print("case tiny bf16 b8 + 4 correction rows, prefix_len %s" % lens, flush=True)
+    w, K, V, noise, corr = _inputs(wl, 4, lens)
+    com = synth.make_committed(wl)
+    ae = make_expert(wl, w, max_batch=8, max_prefix=wl.prefix, max_corr=4)
+    try:
+        got = run(ae, K, V, noise, wl.n_steps, prefix_len=lens, committed=com, n_fixed=1, corr=corr)
+    finally:
+        ae.close()
+    ref = oracle.denoise(oracle.Expert(wl.dims, w), noise, K, V, lens, wl.n_steps, committed=com, n_fixed=1,
+                         corr=corr)
+    rel = rel_l2_per_rollout(got, ref)
+    print("rel-L2 %.3e max-abs %.3e" % (rel, np.abs(got - ref).max()), flush=True)
+    assert rel <= BF16_TOL
+    assert np.array_equal(got[:, :1].astype(np.float32), com)
+
+
+def test_vlm_prefill_with_correction_tokens_bound():
+    """The VLM prefill's in-place hand-off builds the expert's RoPE table for
+    the suffix rows it sees; binding correction tokens before or after the
+    prefill must give the same actions as the oracle on the prefill's KV."""
+    torch = torch_cuda()
+    from paper_2607_12659_amd.expert import to_device
+    from gpu_util import Vlm
+    import synth.vlm as sv
+    vwl = sv.VLM_WORKLOADS["vlm-tiny"]
+    awl = synth.WORKLOADS["tiny-fp32"].with_(dtype="bf16", name="tiny-bf16-vlm-corr")
+    assert awl.dims.n_layers == vwl.dims.n_layers and awl.dims.head_dim == vwl.dims.head_dim
+    print("case vlm-tiny prefill -> tiny bf16 expert with 3 correction tokens", flush=True)
+    vw = sv.make_vlm_weights(vwl)
+    emb = sv.make_embeddings(vwl)
+    aw = synth.make_weights(awl)
+    noise = synth.make_noise(awl)
+    corr = sc.make_item(awl.seed, 1, 3, awl.dims.width)
+    vlm = Vlm(vwl.dims, vw, 1, vwl.prefix)
+    ae = make_expert(awl, aw, max_batch=1, max_prefix=vwl.prefix, max_corr=3)
+    try:
+        e_d = to_device(emb.astype(np.float32))
+        c_d = to_device(corr.astype(np.float32))
+        n_d = to_device(noise.astype(np.float32))
+        vlm.prefill(e_d, 1, vwl.prefix, ae)          # tokens bound after the prefill
+        ae.bind_state(None, 0, c_d)
+        a = ae.denoise(n_d, awl.n_steps).cpu().numpy().astype(np.float64)
+        vlm.prefill(e_d, 1, vwl.prefix, ae)          # tokens already bound during the prefill
+        b = ae.denoise(n_d, awl.n_steps).cpu().numpy().astype(np.float64)
+        ae.sync()
+        torch.cuda.synchronize()
+    finally:
+        ae.close()
+        vlm.close()
+    Kr, Vr, _ = oracle.vlm_prefill(vwl.dims, vw, emb[0])
+    ref = oracle.denoise(oracle.Expert(awl.dims, aw), noise, Kr[:, None], Vr[:, None], [vwl.prefix], awl.n_steps,
+                         corr=corr)
+    print("after-prefill binding rel-L2 %.3e, during-prefill binding %.3e"
+          % (rel_l2_per_rollout(a, ref), rel_l2_per_rollout(b, ref)), flush=True)
+    assert rel_l2_per_rollout(a, ref) <= BF16_TOL and rel_l2_per_rollout(b, ref) <= BF16_TOL
+    assert np.array_equal(a, b)
