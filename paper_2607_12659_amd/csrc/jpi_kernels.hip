@@ -514,6 +514,22 @@ __global__ __launch_bounds__(256) void k_inproj_norm(const float* __restrict__ x
 constexpr int ROW_MAX_S = 16;
 constexpr int ROW_MAX_A = 64;
 
+// four consecutive elements as floats (8- or 16-byte aligned)
+__device__ __forceinline__ void load4(const float* p, float (&w)[4]) {
+  const f32x4 v = *reinterpret_cast<const f32x4*>(p);
+  w[0] = v[0];
+  w[1] = v[1];
+  w[2] = v[2];
+  w[3] = v[3];
+}
+__device__ __forceinline__ void load4(const bf16* p, float (&w)[4]) {
+  const uint2 v = *reinterpret_cast<const uint2*>(p);
+  w[0] = __uint_as_float(v.x << 16);
+  w[1] = __uint_as_float(v.x & 0xffff0000u);
+  w[2] = __uint_as_float(v.y << 16);
+  w[3] = __uint_as_float(v.y & 0xffff0000u);
+}
+
 template <typename T, bool FINAL>
 __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
   __shared__ float hs[ROW_MAX_W];
@@ -568,14 +584,18 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
     T* yr = reinterpret_cast<T*>(r.y) + (size_t)m * W;
     for (int k = threadIdx.x; k < W; k += 256) yr[k] = from_f32<T>(hs[k] * rs * (1.0f + scale[k]) + shift[k]);
   } else {
-    // v[a] = sum_k y[k] W_out[a][k] + b_out[a]; each thread owns columns k = t + 256 j
+    // v[a] = sum_k y[k] W_out[a][k] + b_out[a]; thread t owns columns 4t + 1024 j .. + 3,
+    // so each row of W_out is read with one 4-element load per thread, all independent
+    constexpr int NJ = ROW_MAX_W / 1024;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const T* wo = reinterpret_cast<const T*>(r.w_out);
-    float yk[ROW_MAX_W / 256];
+    float yk[NJ][4];
 #pragma unroll
-    for (int j = 0; j < ROW_MAX_W / 256; ++j) {
-      const int k = threadIdx.x + 256 * j;
-      yk[j] = k < W ? hs[k] * rs * (1.0f + scale[k]) + shift[k] : 0.f;
+    for (int j = 0; j < NJ; ++j) {
+      const int k = 4 * threadIdx.x + 1024 * j;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        yk[j][e] = k < W ? hs[k + e] * rs * (1.0f + scale[k + e]) + shift[k + e] : 0.f;
     }
     for (int a0 = 0; a0 < r.A; a0 += 8) {
       float p[8];
@@ -583,9 +603,14 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
       for (int u = 0; u < 8; ++u) {
         p[u] = 0.f;
 #pragma unroll
-        for (int j = 0; j < ROW_MAX_W / 256; ++j) {
-          const int k = threadIdx.x + 256 * j;
-          if (a0 + u < r.A && k < W) p[u] = fmaf(yk[j], static_cast<float>(wo[(size_t)(a0 + u) * W + k]), p[u]);
+        for (int j = 0; j < NJ; ++j) {
+          const int k = 4 * threadIdx.x + 1024 * j;
+          if (a0 + u < r.A && k < W) {
+            float w4[4];
+            load4(wo + (size_t)(a0 + u) * W + k, w4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) p[u] = fmaf(yk[j][e], w4[e], p[u]);
+          }
         }
       }
 #pragma unroll
