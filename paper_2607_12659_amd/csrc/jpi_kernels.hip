@@ -629,6 +629,59 @@ __global__ __launch_bounds__(256) void k_resid_norm(RowLaunch r) {
   }
 }
 
+// Non-final residual + norm, one workgroup per row: thread t owns columns
+// 4t + 1024 j .. + 3; the slices, the residual and the gate, scale and shift
+// are all loaded before the row reduction, and the row stays in registers.
+template <typename T>
+__global__ __launch_bounds__(256) void k_resid_norm_row(RowLaunch r) {
+  constexpr int NJ = ROW_MAX_W / 1024;
+  __shared__ float red[4];
+  const int m = blockIdx.x, W = r.W, S = r.S;
+  const size_t MW = (size_t)r.M * W;
+  const float *gate = r.gate, *scale = r.scale, *shift = r.shift;
+  if (r.n_t0 > 0) {  // committed rows at t = 0: the t = 0 table row
+    const int ia = m % (r.n_lead + r.horizon) - r.n_lead;
+    if (ia >= 0 && ia < r.n_t0) {
+      gate += r.t0_delta;
+      scale += r.t0_delta;
+      shift += r.t0_delta;
+    }
+  }
+  float* hr = r.h + (size_t)m * W;
+  const float* pr = r.part + (size_t)m * W;
+  f32x4 hv[NJ], sc[NJ], sh[NJ];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int k = 4 * threadIdx.x + 1024 * j;
+    if (k >= W) break;
+    f32x4 v[ROW_MAX_S];
+#pragma unroll
+    for (int z = 0; z < ROW_MAX_S; ++z)
+      v[z] = z < S ? *reinterpret_cast<const f32x4*>(pr + z * MW + k) : f32x4{0.f, 0.f, 0.f, 0.f};
+    const f32x4 h = *reinterpret_cast<const f32x4*>(hr + k), g4 = *reinterpret_cast<const f32x4*>(gate + k);
+    sc[j] = *reinterpret_cast<const f32x4*>(scale + k);
+    sh[j] = *reinterpret_cast<const f32x4*>(shift + k);
+    f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int z = 0; z < ROW_MAX_S; ++z)
+      if (z < S) sum += v[z];
+    const f32x4 h2 = h + g4 * sum;
+    *reinterpret_cast<f32x4*>(hr + k) = h2;
+    hv[j] = h2;
+    ss += h2[0] * h2[0] + h2[1] * h2[1] + h2[2] * h2[2] + h2[3] * h2[3];
+  }
+  const float rs = 1.0f / sqrtf(block_sum_256(ss, red) / (float)W + r.eps);
+  T* yr = reinterpret_cast<T*>(r.y) + (size_t)m * W;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int k = 4 * threadIdx.x + 1024 * j;
+    if (k >= W) break;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) yr[k + e] = from_f32<T>(hv[j][e] * rs * (1.0f + sc[j][e]) + sh[j][e]);
+  }
+}
+
 // Non-final residual + norm with one wave per row (four rows per workgroup):
 // the row's sum of squares is a wave reduction, so no workgroup barrier.
 // Same per-element arithmetic as k_resid_norm (slices summed in order).
@@ -696,16 +749,17 @@ hipError_t launch_resid_norm(jpi_dtype dt, const RowLaunch& r, bool final_step, 
     return hipErrorInvalidValue;
   // a wave per row pays off only with many rows (batch 64: 23 -> 12 us); with
   // fewer rows a workgroup per row keeps more loads in flight
-  const bool wave_rows = !final_step && r.M >= 2048 && r.W % 4 == 0;
+  if (!final_step && r.W % 4 != 0) return hipErrorInvalidValue;
+  const bool wave_rows = !final_step && r.M >= 2048;
   const dim3 wave_grid((r.M + 3) / 4);
   if (dt == JPI_BF16) {
     if (final_step) hipLaunchKernelGGL((k_resid_norm<bf16, true>), dim3(r.M), dim3(256), 0, s, r);
     else if (wave_rows) hipLaunchKernelGGL(k_resid_norm_wave<bf16>, wave_grid, dim3(256), 0, s, r);
-    else hipLaunchKernelGGL((k_resid_norm<bf16, false>), dim3(r.M), dim3(256), 0, s, r);
+    else hipLaunchKernelGGL(k_resid_norm_row<bf16>, dim3(r.M), dim3(256), 0, s, r);
   } else {
     if (final_step) hipLaunchKernelGGL((k_resid_norm<float, true>), dim3(r.M), dim3(256), 0, s, r);
     else if (wave_rows) hipLaunchKernelGGL(k_resid_norm_wave<float>, wave_grid, dim3(256), 0, s, r);
-    else hipLaunchKernelGGL((k_resid_norm<float, false>), dim3(r.M), dim3(256), 0, s, r);
+    else hipLaunchKernelGGL(k_resid_norm_row<float>, dim3(r.M), dim3(256), 0, s, r);
   }
   return hipGetLastError();
 }
