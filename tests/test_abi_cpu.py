@@ -77,6 +77,16 @@ def test_null_arguments():
     assert j.jpi_bind_state(None, None, 0) == j.JPI_ERR_ARG
     assert j.jpi_denoise(None, 1, 1, 1) == j.JPI_ERR_ARG
     assert j.jpi_sync(None) == j.JPI_ERR_ARG
+    assert j.jpi_set_committed_t0(None, 1) == j.JPI_ERR_ARG
+    assert j.jpi_bind_robot_state(None, 1) == j.JPI_ERR_ARG
+    assert j.jpi_corr_destroy(None) == j.JPI_OK
+    assert j.jpi_corr_set_weight(None, "fuse.w", 1, 1, j.JPI_BF16, 0) == j.JPI_ERR_ARG
+    assert j.jpi_corr_finalize_weights(None) == j.JPI_ERR_ARG
+    assert j.jpi_corr_compress(None, 1, 1, 1, 1) == j.JPI_ERR_ARG
+    assert j.jpi_corr_predict(None, 1, 1, 1, 1, 1, 1) == j.JPI_ERR_ARG
+    assert j.jpi_corr_last_error(None)
+    assert j.jpi_vlm_destroy(None) == j.JPI_OK
+    assert j.jpi_vlm_prefill(None, 1, 1, 1, None) == j.JPI_ERR_ARG
     assert j.jpi_debug_gemm(None, 1, 1, 4, 4, 64, j.JPI_BF16) == j.JPI_ERR_ARG
     assert j.jpi_debug_gemm(1, 1, 1, 4, 4, 65, j.JPI_BF16) == j.JPI_ERR_ARG      # K not a multiple of 64
     assert j.jpi_debug_gemm(1, 1, 1, 0, 4, 64, j.JPI_BF16) == j.JPI_ERR_ARG
@@ -84,6 +94,28 @@ def test_null_arguments():
     import numpy as np
     assert j.jpi_debug_attention(1, 1, 1, 1, 1, np.array([5]), 1, 1, 4, 4, 64, j.JPI_F32, 1) == j.JPI_ERR_ARG
     assert j.jpi_debug_attention(1, 1, 1, 1, 1, np.array([2]), 1, 1, 4, 4, 48, j.JPI_F32, 1) == j.JPI_ERR_ARG
+
+
+@pytest.mark.parametrize("bad", [dict(max_corr=-1), dict(max_corr=65), dict(variant=2), dict(state_dim=3),
+                                 dict(variant=1), dict(variant=1, state_dim=8, max_corr=2),
+                                 dict(variant=1, state_dim=8, max_prefix=0)])
+def test_create_rejects_bad_variant_or_correction_config(bad):
+    j = _lib()
+    st, ctx = j.jpi_create(_cfg(**bad), 0)
+    assert st == j.JPI_ERR_ARG and not ctx
+
+
+def test_corr_create_rejects_bad_config_before_touching_the_device():
+    j = _lib()
+    good = dict(width=256, n_heads=4, n_kv_heads=1, head_dim=64, mlp_dim=512, action_dim=7, vlm_width=256,
+                n_query=4, max_batch=1, max_actions=5, max_vlm_tokens=40, dtype=j.JPI_BF16, rms_eps=1e-6,
+                rope_base=1e4)
+    for bad in (dict(width=100), dict(n_kv_heads=2), dict(head_dim=48), dict(vlm_width=200), dict(n_query=0),
+                dict(max_actions=0), dict(action_dim=300), dict(rms_eps=0.0)):
+        st, m = j.jpi_corr_create(j.jpi_corr_config(**{**good, **bad}))
+        assert st == j.JPI_ERR_ARG and not m, bad
+    st, m = j.jpi_corr_create(j.jpi_corr_config(**{**good, "dtype": j.JPI_F32}))
+    assert st == j.JPI_ERR_UNSUPPORTED and not m
 
 
 def test_build_entry_compiles_everything():
