@@ -121,6 +121,8 @@ struct PersistArgs {
   int L, W, nH, Dh, F, A, H, B, M;  // H: suffix rows per rollout (n_corr correction rows, then the action rows)
   int n_corr;               // correction rows ahead of each rollout's action rows
   const float* corr;        // [B][n_corr][W] correction tokens (rows restart from them every step)
+  const float* h_in;        // [M][W] or null: every row starts from it instead of the in-projection
+                            // (the action-time expert's MLP output; then n_steps is 1)
   int C;                    // attention chunks (32 keys) per rollout
   int n_steps, n_fixed, s_o, s_d, R;
   int n_t0;                 // leading action rows (committed) modulated at t = 0: table row n_steps

@@ -665,7 +665,8 @@ __device__ __forceinline__ void store_y(const PersistArgs& a, const float* hrow,
 // In-projection of the owner's row: h = x W_in^T + b_in (x in LDS, W_in
 // [W][A] in global memory; with A % 8 == 0 a thread loads its rows as
 // 16-byte pieces, all in flight), then the step's first adaRMSNorm -> y.
-// A correction row (crow != nullptr) starts from its token instead.
+// A correction row, or every row when the caller hands the rows over
+// (crow != nullptr), starts from that row instead.
 __device__ __forceinline__ void inproj_row(const PersistArgs& a, const float* scale, const float* shift, float* hrow,
                                            const float* bin, const float* xs, float* red, const float* crow) {
   const int W = a.W, A = a.A;
@@ -867,7 +868,9 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   // owned row: rollout m / H, suffix row m % H; action index ia < 0 for a correction row
   const int ia = m % a.H - a.n_corr;
   const size_t xrow = (size_t)(m / a.H) * (a.H - a.n_corr) + ia;
-  const float* crow = ia < 0 ? a.corr + ((size_t)(m / a.H) * a.n_corr + (m % a.H)) * W : nullptr;
+  const float* crow = a.h_in ? a.h_in + (size_t)m * W
+                   : ia < 0   ? a.corr + ((size_t)(m / a.H) * a.n_corr + (m % a.H)) * W
+                              : nullptr;
   const bool at_t0 = ia >= 0 && ia < a.n_t0;  // a committed row modulated at t = 0 (table row n_steps)
   float xreg = 0.f;
   if (t == 0) s_abort = 0u;

@@ -745,7 +745,6 @@ struct StepGemms {
 bool use_persist(jpi_ctx* c, int batch) {
   const char* e = getenv("JPI_PERSIST");
   if (e && e[0] == '0') return false;
-  if (c->cfg.variant != JPI_VARIANT_ADARMS) return false;  // the single-launch kernel runs the adaRMS expert
   const int S = c->H + c->n_corr;  // suffix rows per rollout
   if (!persist_supported(c->dt, batch * S, c->W, c->nH, c->Dh, c->F, S, c->A, c->Pmax)) return false;
   if (c->n_cu > persist_max_grid()) return false;
@@ -881,66 +880,6 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     *stop = c->ev[c->ev_used + 1];
     c->ev_used += 2;
   };
-  if (p.persist) {
-    PersistArgs pa{};
-    pa.L = L;
-    pa.W = W;
-    pa.nH = nH;
-    pa.Dh = Dh;
-    pa.F = F;
-    pa.A = c->A;
-    pa.H = S;
-    pa.n_corr = C;
-    pa.corr = c->corr;
-    pa.B = batch;
-    pa.M = M;
-    pa.C = persist_chunks(prefix, S);
-    pa.n_steps = n_steps;
-    pa.n_fixed = c->n_fixed;
-    pa.n_t0 = c->committed_t0 ? c->n_fixed : 0;
-    pa.s_o = p.s_o;
-    pa.s_d = p.s_d;
-    pa.R = c->R;
-    pa.eps = eps;
-    pa.dt = dt_step;
-    pa.w_layers = c->w_layers;
-    pa.w_frag = c->w_frag;
-    pa.layer_elems = (int64_t)c->layer_elems;
-    pa.off_o = (int64_t)c->off_o;
-    pa.off_gu = (int64_t)c->off_gu;
-    pa.off_d = (int64_t)c->off_d;
-    pa.w_in = c->w_in;
-    pa.b_in = c->b_in;
-    pa.w_out = c->w_out;
-    pa.b_out = c->b_out;
-    pa.table = table;
-    pa.kp = c->kp;
-    pa.vpt = c->vpt;
-    pa.kp_lstride = (int64_t)c->Bmax * c->Pmax * Dh;
-    pa.kp_bstride = (int64_t)c->Pmax * Dh;
-    pa.vpt_lstride = (int64_t)c->Bmax * c->Ppad * Dh;
-    pa.vpt_bstride = (int64_t)c->Ppad * Dh;
-    pa.vpt_dstride = c->Ppad;
-    pa.prefix_len = c->d_prefix_len;
-    pa.rope = c->rope_tab;
-    pa.x = c->x;
-    pa.h = c->h;
-    pa.y = c->ysw;
-    pa.q = c->qsw;
-    pa.ks = c->ks;
-    pa.vst = c->vst;
-    pa.opart = c->opart;
-    pa.ml = c->opart + (size_t)batch * nH * pa.C * S * Dh;
-    pa.o = c->osw;
-    pa.part = c->partial;
-    pa.z = c->zsw;
-    pa.flags = c->pflags;
-    pa.err = c->perr;
-    timing(JPI_KERNEL_PERSISTENT, &pa.ev_start, &pa.ev_stop);
-    ENQ(launch_persist(pa, c->n_cu, s));
-    return hipSuccess;
-  }
-  const int n_t0 = c->committed_t0 && !at ? c->n_fixed : 0;
   if (at) {
     // the state token: W_s s + b_s, then every layer over it alone (it sees the prefix
     // and itself); each layer's key and value go into prefix slot prefix_len
@@ -996,43 +935,129 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
                               c->d_prefix_len, batch, Dh, s));
     }
   }
-  const float* ctab = table + (size_t)(n_steps + 1) * c->R;  // action-time variant: W_t e(t_k) + b_i rows
+  // action-time variant, step k: h = W_o swish(W_i [W_a x + b_a ; e(t_k)] + b_i) + b_o (and its first norm)
+  const float* ctab = table + (size_t)(n_steps + 1) * c->R;  // W_t e(t_k) + b_i rows after the table
+#define ENQ_L(x)                    \
+  do {                              \
+    hipError_t e_ = (x);            \
+    if (e_ != hipSuccess) return e_; \
+  } while (0)
+  auto action_time_inproj = [&](int k) -> hipError_t {
+    const float* tk = table + (size_t)k * c->R;
+    // h = W_o swish(W_i [W_a x + b_a ; e(t_k)] + b_i) + b_o, then the first norm
+    ENQ_L(launch_action_embed(c->dt, c->x, c->w_in, c->b_in, c->y, M, W, c->A, s));
+    GemmLaunch g{};
+    g.M = M;
+    g.A = c->y;
+    g.W = c->w_atm_a;
+    g.N = W;
+    g.K = W;
+    g.splitk = p.s_a;
+    g.epi = EPI_STORE_F32;
+    g.ep.out_f32 = c->partial;
+    g.n_cu = c->n_cu;
+    ENQ_L(launch_gemm(c->dt, g, s));
+    ENQ_L(launch_swish_slices(c->dt, c->partial, p.s_a, M, ctab + (size_t)k * W, c->u2, W, s));
+    g.A = c->u2;
+    g.W = c->w_atm_out;
+    ENQ_L(launch_gemm(c->dt, g, s));
+    ENQ_L(launch_bcast_rows(c->b_atm_out, c->h, M, 1, W, s));
+    RowLaunch r{};
+    r.part = c->partial;
+    r.S = p.s_a;
+    r.M = M;
+    r.W = W;
+    r.h = c->h;
+    r.gate = tk + 2 * W;  // ones in the plain-norm table
+    r.scale = tk;
+    r.shift = tk + W;
+    r.y = c->y;
+    r.eps = eps;
+    r.horizon = H;
+    ENQ_L(launch_resid_norm(c->dt, r, false, s));
+    return hipSuccess;
+  };
+#undef ENQ_L
+  const int n_t0 = c->committed_t0 && !at ? c->n_fixed : 0;
+  if (p.persist) {
+    PersistArgs pa{};
+    pa.L = L;
+    pa.W = W;
+    pa.nH = nH;
+    pa.Dh = Dh;
+    pa.F = F;
+    pa.A = c->A;
+    pa.H = S;
+    pa.n_corr = C;
+    pa.corr = c->corr;
+    pa.B = batch;
+    pa.M = M;
+    pa.C = persist_chunks(P_act, S);
+    pa.n_steps = n_steps;
+    pa.n_fixed = c->n_fixed;
+    pa.n_t0 = c->committed_t0 ? c->n_fixed : 0;
+    pa.s_o = p.s_o;
+    pa.s_d = p.s_d;
+    pa.R = c->R;
+    pa.eps = eps;
+    pa.dt = dt_step;
+    pa.w_layers = c->w_layers;
+    pa.w_frag = c->w_frag;
+    pa.layer_elems = (int64_t)c->layer_elems;
+    pa.off_o = (int64_t)c->off_o;
+    pa.off_gu = (int64_t)c->off_gu;
+    pa.off_d = (int64_t)c->off_d;
+    pa.w_in = c->w_in;
+    pa.b_in = c->b_in;
+    pa.w_out = c->w_out;
+    pa.b_out = c->b_out;
+    pa.table = table;
+    pa.kp = c->kp;
+    pa.vpt = c->vpt;
+    pa.kp_lstride = (int64_t)c->Bmax * c->Pmax * Dh;
+    pa.kp_bstride = (int64_t)c->Pmax * Dh;
+    pa.vpt_lstride = (int64_t)c->Bmax * c->Ppad * Dh;
+    pa.vpt_bstride = (int64_t)c->Ppad * Dh;
+    pa.vpt_dstride = c->Ppad;
+    pa.prefix_len = plen_act;
+    pa.rope = c->rope_tab;
+    pa.x = c->x;
+    pa.h = c->h;
+    pa.y = c->ysw;
+    pa.q = c->qsw;
+    pa.ks = c->ks;
+    pa.vst = c->vst;
+    pa.opart = c->opart;
+    pa.ml = c->opart + (size_t)batch * nH * pa.C * S * Dh;
+    pa.o = c->osw;
+    pa.part = c->partial;
+    pa.z = c->zsw;
+    pa.flags = c->pflags;
+    pa.err = c->perr;
+    if (!at) {
+      timing(JPI_KERNEL_PERSISTENT, &pa.ev_start, &pa.ev_stop);
+      ENQ(launch_persist(pa, c->n_cu, s));
+      return hipSuccess;
+    }
+    // action-time variant: per step the action-time MLP (multi-kernel), then one
+    // single-launch step that starts its rows from that h
+    pa.n_steps = 1;
+    pa.n_t0 = 0;
+    pa.h_in = c->h;
+    for (int k = 0; k < n_steps; ++k) {
+      ENQ(action_time_inproj(k));
+      pa.table = table + (size_t)k * c->R;
+      timing(JPI_KERNEL_PERSISTENT, &pa.ev_start, &pa.ev_stop);
+      ENQ(launch_persist(pa, c->n_cu, s));
+    }
+    return hipSuccess;
+  }
   for (int k = 0; k < n_steps; ++k) {
     const float* tk = table + (size_t)k * c->R;
     const float* fm = tk + (size_t)(6 * L) * W;
     const int64_t t0_delta = (int64_t)(n_steps - k) * c->R;  // to the t = 0 row
     if (at) {
-      // h = W_o swish(W_i [W_a x + b_a ; e(t_k)] + b_i) + b_o, then the first norm
-      ENQ(launch_action_embed(c->dt, c->x, c->w_in, c->b_in, c->y, M, W, c->A, s));
-      GemmLaunch g{};
-      g.M = M;
-      g.A = c->y;
-      g.W = c->w_atm_a;
-      g.N = W;
-      g.K = W;
-      g.splitk = p.s_a;
-      g.epi = EPI_STORE_F32;
-      g.ep.out_f32 = c->partial;
-      g.n_cu = c->n_cu;
-      ENQ(launch_gemm(c->dt, g, s));
-      ENQ(launch_swish_slices(c->dt, c->partial, p.s_a, M, ctab + (size_t)k * W, c->u2, W, s));
-      g.A = c->u2;
-      g.W = c->w_atm_out;
-      ENQ(launch_gemm(c->dt, g, s));
-      ENQ(launch_bcast_rows(c->b_atm_out, c->h, M, 1, W, s));
-      RowLaunch r{};
-      r.part = c->partial;
-      r.S = p.s_a;
-      r.M = M;
-      r.W = W;
-      r.h = c->h;
-      r.gate = tk + 2 * W;  // ones in the plain-norm table
-      r.scale = tk;
-      r.shift = tk + W;
-      r.y = c->y;
-      r.eps = eps;
-      r.horizon = H;
-      ENQ(launch_resid_norm(c->dt, r, false, s));
+      ENQ(action_time_inproj(k));
     } else {
       ENQ(launch_inproj_norm(c->dt, c->x, c->w_in, c->b_in, c->h, tk, tk + W, c->y, M, W, c->A, eps, c->corr, C, H,
                              n_t0, t0_delta, s));

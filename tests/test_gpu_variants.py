@@ -106,9 +106,23 @@ def _pi0_expert(wl, w, max_batch, max_prefix, state_dim=spi0.STATE_DIM):
     return ae
 
 
-def _pi0_run(ae, K, V, noise, n_steps, lens, state, committed=None, n_fixed=0):
+def _pi0_run(ae, K, V, noise, n_steps, lens, state, committed=None, n_fixed=0, persist=None):
+    """persist: None (default path choice) or "0" (force the multi-kernel path)."""
+    import os
     from paper_2607_12659_amd.expert import to_device
     torch = torch_cuda()
+    old = os.environ.pop("JPI_PERSIST", None)
+    if persist is not None:
+        os.environ["JPI_PERSIST"] = persist
+    try:
+        return _pi0_run_now(ae, K, V, noise, n_steps, lens, state, committed, n_fixed, to_device, torch)
+    finally:
+        os.environ.pop("JPI_PERSIST", None)
+        if old is not None:
+            os.environ["JPI_PERSIST"] = old
+
+
+def _pi0_run_now(ae, K, V, noise, n_steps, lens, state, committed, n_fixed, to_device, torch):
     ae.bind_prefix(to_device(K), to_device(V), lens)
     ae.bind_state(None if committed is None else to_device(np.ascontiguousarray(committed, np.float32)), n_fixed)
     ae.bind_robot_state(to_device(np.ascontiguousarray(state, np.float32)))
@@ -135,6 +149,7 @@ def test_tiny_action_time_variant(dtype):
         got = _pi0_run(ae, K, V, noise, wl.n_steps, lens, st, com, 2)
         again = _pi0_run(ae, K, V, noise, wl.n_steps, lens, st, com, 2)
         moved = _pi0_run(ae, K, V, noise, wl.n_steps, lens, st * 3.0, com, 2)
+        multi = _pi0_run(ae, K, V, noise, wl.n_steps, lens, st, com, 2, persist="0")
     finally:
         ae.close()
     ref = opi0.denoise(wl.dims, w, noise, K, V, lens, wl.n_steps, st, committed=com, n_fixed=2)
@@ -147,7 +162,14 @@ def test_tiny_action_time_variant(dtype):
         assert err <= F32_TOL
         assert np.abs(moved - ref3).max() <= F32_TOL
     else:
+        # bf16 with 2 x 10 rows runs the single-launch kernel once per step
         assert rel <= BF16_TOL and rel_l2_per_rollout(moved, ref3) <= BF16_TOL
+        # with these N(0, 0.1) weights each path is ~6e-3 from the oracle in bf16, so the
+        # two paths are held to the same bar against each other as against the oracle
+        print("single-launch steps vs multi-kernel rel-L2 %.3e; multi-kernel vs oracle %.3e"
+              % (rel_l2_per_rollout(got, multi), rel_l2_per_rollout(multi, ref)), flush=True)
+        assert rel_l2_per_rollout(multi, ref) <= BF16_TOL
+        assert rel_l2_per_rollout(got, multi) <= BF16_TOL
     assert effect > 20 * max(err, 1e-6)
     assert np.array_equal(got, again)
     assert np.array_equal(got[:, :2].astype(np.float32), com.astype(np.float32))
@@ -189,8 +211,11 @@ def test_pi0_shape_action_time_variant():
     ae = _pi0_expert(wl, w, 1, 816)
     try:
         got = _pi0_run(ae, K, V, noise, wl.n_steps, [815], spi0.make_state(wl), synth.make_committed(wl), 10)
+        multi = _pi0_run(ae, K, V, noise, wl.n_steps, [815], spi0.make_state(wl), synth.make_committed(wl), 10,
+                         persist="0")
     finally:
         ae.close()
-    rel = rel_l2_per_rollout(got, ref)
-    print("rel-L2 %.3e max-abs %.3e" % (rel, np.abs(got - ref).max()), flush=True)
-    assert rel <= BF16_TOL
+    for label, out in (("single-launch steps", got), ("multi-kernel", multi)):
+        rel = rel_l2_per_rollout(out, ref)
+        print("%s: rel-L2 %.3e max-abs %.3e" % (label, rel, np.abs(out - ref).max()), flush=True)
+        assert rel <= BF16_TOL
