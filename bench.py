@@ -46,10 +46,10 @@ METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roof
 # sha256 of the kernel source they were measured on; the byte counts are the
 # counter readings times the copy calibration factor.
 MEASURED_TRAFFIC = {
-    # pi0.5 shape, batch 1: FETCH_SIZE 5271318.5 KiB x 1.99980 (a 256 MiB copy
-    # reads back 131085.17 KiB) + WRITE_SIZE 2007096.2 KiB x 1.00000 (the copy's
+    # pi0.5 shape, batch 1: FETCH_SIZE 5273474.7 KiB x 1.99980 (a 256 MiB copy
+    # reads back 131085.25 KiB) + WRITE_SIZE 2007096.2 KiB x 1.00000 (the copy's
     # 262144 KiB), mean over 29 dispatches
-    ("7ef5595361ede87fdd8c4c82b42bbc4d76dc671ba2f8b002d6400112cc848a76", "pi05-b1"): 12849842414,
+    ("70973a2829f4b44eee75fd287bd4eb4f633e3127513cff878ccc46b78bb6663e", "pi05-b1"): 12854250995,
 }
 
 
