@@ -622,6 +622,8 @@ def main():
     ap.add_argument("--timed-kernel", default="auto",
                     choices=["auto", "persistent", "qkv", "attention", "oproj", "gateup", "down"])
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--committed-t0", action="store_true",
+                    help="committed rows at flow time t = 0 (the variant; the default workloads share t)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     args = ap.parse_args()
     if args.calibrate_copy:
@@ -669,6 +671,8 @@ def main():
     Kd, Vd = to_device(K), to_device(V)
     ae.bind_prefix(Kd, Vd, wl.valid_lengths(), stream=stream)
     ae.bind_state(None if committed is None else to_device(committed), wl.n_fixed, stream=stream)
+    if args.committed_t0:
+        ae.set_committed_t0(True)
     noise_d = to_device(noise)
     out = torch.empty_like(noise_d)
     torch.cuda.synchronize()
@@ -760,7 +764,7 @@ def main():
                    "action_dim": wl.dims.action_dim, "euler_steps": wl.n_steps, "layers": wl.dims.n_layers,
                    "width": wl.dims.width, "heads": wl.dims.n_heads, "kv_heads": wl.dims.n_kv_heads,
                    "head_dim": wl.dims.head_dim, "mlp_dim": wl.dims.mlp_dim, "n_fixed": wl.n_fixed,
-                   "seed": wl.seed},
+                   "committed_t0": bool(args.committed_t0), "seed": wl.seed},
         "per_euler_step_us": round(ms_per_call / wl.n_steps * 1e3, 2),
         "first_call_ms": round(first_ms, 2),
         "roofline": {"bound": "hbm", "kernel": ("k_persist (whole denoise call)" if kname == "persistent"
