@@ -137,14 +137,19 @@ def algorithmic_counts(wl):
     }
 
 
+def blas_threads():
+    """Threads numpy's BLAS uses on this host (what the fp64 oracle runs on)."""
+    try:
+        from threadpoolctl import threadpool_info
+        return max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        return os.cpu_count()
+
+
 def cpu_baseline(wl, weights, K, V, noise):
     import numpy as np
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count()
+    threads = blas_threads()
     ex = oracle.Expert(wl.dims, weights)
     lens = wl.valid_lengths()[:1]
     # Bounded sample: repeat the denoise of rollout 0 until at least 10 s of host time
@@ -235,7 +240,7 @@ def bench_prefill(args, vwl):
         t0 = time.time()
         oracle.vlm_prefill(vd1, w1, emb[0])
         dt = time.time() - t0
-        cpu = {"value": vwl.prefix / (dt * vd.n_layers), "unit": "tokens/s", "cores": os.cpu_count(),
+        cpu = {"value": vwl.prefix / (dt * vd.n_layers), "unit": "tokens/s", "cores": blas_threads(),
                "kind": "oracle", "sample": "one of the %d layers of the fp64 oracle prefill over %d tokens "
                "(%.1f s), scaled to the whole stack" % (vd.n_layers, vwl.prefix, dt)}
     result = {
@@ -362,7 +367,7 @@ def bench_corr(args, cwl):
             if time.time() - t0 >= 10.0:
                 break
         dt = time.time() - t0
-        cpu = {"value": round(calls / dt, 3), "unit": "refresh calls/s", "cores": os.cpu_count(), "kind": "oracle",
+        cpu = {"value": round(calls / dt, 3), "unit": "refresh calls/s", "cores": blas_threads(), "kind": "oracle",
                "sample": "%d repeated fp64 oracle calls (compress + predict, rollout 0), %.1f s" % (calls, dt)}
     result = {
         "metric": "future correction module calls/sec (VLM-refresh branch: compress + predict, ~40M parameters)",
@@ -449,7 +454,7 @@ def bench_pi0(args, wl):
             if time.time() - t0 >= 10.0:
                 break
         dt = time.time() - t0
-        cpu = {"value": round(calls / dt, 4), "unit": "chunks/s", "cores": os.cpu_count(), "kind": "oracle",
+        cpu = {"value": round(calls / dt, 4), "unit": "chunks/s", "cores": blas_threads(), "kind": "oracle",
                "sample": "%d repeated %d-step fp64 oracle denoise calls of rollout 0 (%.1f s)" % (calls, wl.n_steps, dt)}
     result = {
         "metric": "action chunks/sec (10-step flow denoise, action-time pi0-style expert, pi0.5 shape, B=1)",
