@@ -112,7 +112,9 @@ const char* jpi_last_error(const jpi_ctx* ctx);
 /* Create a context on HIP device `device`.  The config is validated on the
  * host before any HIP call: dims must be positive, n_kv_heads == 1,
  * n_heads % n_kv_heads == 0, head_dim a multiple of 32, width a multiple of
- * 64, mlp_dim a multiple of 64 (JPI_ERR_ARG otherwise).  All resident buffers
+ * 64, mlp_dim a multiple of 64, max_corr in [0, 64], variant known, state_dim
+ * in [1, 4096] for the action-time variant (which also needs max_corr 0 and
+ * max_prefix >= 1) and 0 otherwise (JPI_ERR_ARG otherwise).  All resident buffers
  * (max_batch x max_prefix prefix KV, activations, partial sums, weights) are
  * allocated here and owned by the context (Section "System Design":
  * GPU-resident intermediate buffers).  On failure *out is NULL. */
@@ -182,8 +184,8 @@ jpi_status jpi_bind_prefix(jpi_ctx* ctx, const void* k, const void* v, const int
  *     from the given values at every step and are never Euler-updated.
  * Both are copied stream-ordered into context buffers.  Must follow
  * jpi_bind_prefix, which sets the batch (binding a prefix with a different
- * batch clears both).  With n_corr > 0 the multi-kernel path runs (the
- * single-launch kernel covers the action rows alone).  Errors: JPI_ERR_ARG
+ * batch clears both).  Correction rows run on both paths (the single-launch
+ * kernel while batch * (n_corr + horizon) <= 64).  Errors: JPI_ERR_ARG
  * (NULL ctx or data, counts out of range), JPI_ERR_STATE (no prefix bound). */
 jpi_status jpi_bind_state(jpi_ctx* ctx, const float* committed_dev, int n_fixed, const void* corr_tokens,
                           int n_corr, void* stream);
@@ -202,7 +204,9 @@ jpi_status jpi_bind_robot_state(jpi_ctx* ctx, const float* state_dev, void* stre
  * step's t_k with every other row.  enable != 0: committed rows carry t = 0
  * (clean actions) at every step, so their adaRMSNorm scale, shift and gate
  * come from the time conditioning at t = 0 while the other rows use t_k; the
- * correction tokens keep t_k.  Takes effect at the next jpi_denoise.
+ * correction tokens keep t_k.  Takes effect at the next jpi_denoise.  The
+ * action-time variant ignores it (its time enters through the action-time
+ * MLP, at the step's t for every action row).
  * Errors: JPI_ERR_ARG (NULL ctx). */
 jpi_status jpi_set_committed_t0(jpi_ctx* ctx, int enable);
 
