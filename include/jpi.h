@@ -84,7 +84,7 @@ typedef struct {
   int width;        /* W   (1024) */
   int n_heads;      /* query heads (8) */
   int n_kv_heads;   /* KV heads; this version requires 1 */
-  int head_dim;     /* Dh  (256); multiple of 32 */
+  int head_dim;     /* Dh  (256); 64, 128 or 256 */
   int mlp_dim;      /* F   GeGLU hidden width (4096) */
   int action_dim;   /* A   (32) */
   int horizon;      /* H   action tokens per chunk (50) */
@@ -111,7 +111,7 @@ const char* jpi_last_error(const jpi_ctx* ctx);
 
 /* Create a context on HIP device `device`.  The config is validated on the
  * host before any HIP call: dims must be positive, n_kv_heads == 1,
- * n_heads % n_kv_heads == 0, head_dim a multiple of 32, width a multiple of
+ * n_heads % n_kv_heads == 0, head_dim 64, 128 or 256, width a multiple of
  * 64, mlp_dim a multiple of 64, max_corr in [0, 64], variant known, state_dim
  * in [1, 4096] for the action-time variant (which also needs max_corr 0 and
  * max_prefix >= 1) and 0 otherwise (JPI_ERR_ARG otherwise).  All resident buffers
