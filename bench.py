@@ -525,8 +525,7 @@ def bench_loop(args):
     jpi.check(jpi.jpi_corr_finalize_weights(corr))
     emb = to_device(np.ascontiguousarray(synth_vlm.make_embeddings(vwl), np.float32))
     hidden = torch.empty((1, vwl.prefix, vd.width), dtype=torch.int16, device="cuda")
-    fresh = torch.empty((1, cd.n_query, cd.width), device="cuda")     # compression of the latest VLM state
-    item = torch.empty_like(fresh)                                     # the hidden-state buffer B_h
+    item = torch.empty((1, cd.n_query, cd.width), device="cuda")      # the hidden-state buffer B_h
     conf_d = torch.empty((1,), device="cuda")
     noise = to_device(np.ascontiguousarray(synth.make_noise(ewl), np.float32))
     chunk = torch.empty_like(noise)                                    # the action buffer B_a
@@ -547,7 +546,7 @@ def bench_loop(args):
 
     def vlm_fn():
         jpi.check(jpi.jpi_vlm_prefill(vlm, emb, 1, vwl.prefix, ae.ctx, hidden, stream))
-        jpi.check(jpi.jpi_corr_compress(corr, hidden, 1, vwl.prefix, fresh, stream))
+        jpi.check(jpi.jpi_corr_compress(corr, hidden, 1, vwl.prefix, item, stream))  # B_h <- compressed h_t
 
     def vlm_hook(user, t, ms):
         ms[0] = timed("vlm", vlm_fn)
@@ -555,8 +554,8 @@ def bench_loop(args):
 
     def corr_hook(user, t, n, from_vlm, c, ms):
         n = max(1, min(n, ewl.dims.horizon))
-        src = fresh if from_vlm else item
-        ms[0] = timed("corr", lambda: jpi.check(jpi.jpi_corr_predict(corr, src, chunk, 1, n, item, conf_d, stream)))
+        # B_h holds the fresh compression after a refresh, else the previous item
+        ms[0] = timed("corr", lambda: jpi.check(jpi.jpi_corr_predict(corr, item, chunk, 1, n, item, conf_d, stream)))
         c[0] = forced[calls["corr"] % len(forced)]
         calls["corr"] += 1
         return 0
