@@ -136,10 +136,10 @@ class Corr:
         assert st == self.jpi.JPI_OK, self.jpi.jpi_corr_last_error(self.ctx)
         return out
 
-    def predict(self, state_dev, actions_dev, batch, n_actions, item=None):
+    def predict(self, state_dev, actions_dev, batch, n_actions, item=None, conf=None):
         torch = self.torch
         item = item if item is not None else torch.empty((batch, self.d.n_query, self.d.width), device="cuda")
-        conf = torch.empty((batch,), device="cuda")
+        conf = conf if conf is not None else torch.empty((batch,), device="cuda")
         st = self.jpi.jpi_corr_predict(self.ctx, state_dev, actions_dev, batch, n_actions, item, conf)
         assert st == self.jpi.JPI_OK, self.jpi.jpi_corr_last_error(self.ctx)
         return item, conf
