@@ -137,6 +137,44 @@ def algorithmic_counts(wl):
     }
 
 
+def host_cpu():
+    """The host's CPU model and the core counts the oracle could use."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        usable = os.cpu_count()
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable_cores": usable}
+
+
+def check_output(got, ref, dtype):
+    """The timed output of rollout 0 against the oracle's, at the contract bars:
+    fp32 max-abs <= 1e-4; bf16 relative L2 <= 2e-2 and every element within
+    2e-2 of the largest reference magnitude."""
+    import numpy as np
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    err = np.abs(got - ref)
+    rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+    elem = float(err.max() / np.abs(ref).max())
+    if dtype == "f32":
+        ok = bool(np.isfinite(got).all() and err.max() <= 1e-4)
+        bar = "max-abs <= 1e-4"
+    else:
+        ok = bool(np.isfinite(got).all() and rel <= 2e-2 and elem <= 2e-2)
+        bar = "relative L2 <= 2e-2 and max|err| <= 2e-2 max|ref|"
+    return {"checked": "rollout 0 of the last timed call vs the fp64 oracle on the same inputs",
+            "rel_l2": rel, "elem_rel": elem, "max_abs": float(err.max()), "bar": bar, "ok": ok}
+
+
 def blas_threads():
     """Threads numpy's BLAS uses on this host (what the fp64 oracle runs on)."""
     try:
@@ -146,24 +184,32 @@ def blas_threads():
         return os.cpu_count()
 
 
-def cpu_baseline(wl, weights, K, V, noise):
-    import numpy as np
+def cpu_baseline(wl, weights, K, V, noise, committed=None, committed_t0=False):
+    """Times the oracle on rollout 0 (a bounded sample) and returns
+    (baseline entry, the oracle's actions for rollout 0)."""
     import oracle
     threads = blas_threads()
+    host = host_cpu()
     ex = oracle.Expert(wl.dims, weights)
     lens = wl.valid_lengths()[:1]
+    com = None if committed is None else committed[:1]
     # Bounded sample: repeat the denoise of rollout 0 until at least 10 s of host time
     # has passed (and at most 16 calls), then report calls per second.
-    calls, t0 = 0, time.perf_counter()
+    calls, t0, ref = 0, time.perf_counter(), None
     while True:
-        oracle.denoise(ex, noise[:1], K[:, :1], V[:, :1], lens, wl.n_steps)
+        out = oracle.denoise(ex, noise[:1], K[:, :1], V[:, :1], lens, wl.n_steps, committed=com,
+                             n_fixed=wl.n_fixed, committed_t0=committed_t0)
+        ref = out if ref is None else ref
         calls += 1
         dt = time.perf_counter() - t0
         if dt >= 10.0 or calls >= 16:
             break
-    return {"value": round(calls / dt, 4), "unit": "chunks/s", "cores": int(threads), "kind": "oracle",
-            "sample": "%d repeated %d-step denoise calls on rollout 0 of %s (fp64 numpy, BLAS threads=%d), "
-                      "%.1f s in total" % (calls, wl.n_steps, wl.name, threads, dt)}
+    entry = {"value": round(calls / dt, 4), "unit": "chunks/s", "cores": int(threads), "kind": "oracle",
+             "blas_threads": int(threads), "nproc": host["nproc"], "usable_cores": host["usable_cores"],
+             "cpu_model": host["cpu_model"],
+             "sample": "%d repeated %d-step denoise calls on rollout 0 of %s (fp64 numpy, BLAS threads=%d), "
+                       "%.1f s in total" % (calls, wl.n_steps, wl.name, threads, dt)}
+    return entry, ref[0]
 
 
 def prefill_flops(vd, batch, prefix):
@@ -528,7 +574,13 @@ def bench_loop(args):
     item = torch.empty((1, cd.n_query, cd.width), device="cuda")      # the hidden-state buffer B_h
     conf_d = torch.empty((1,), device="cuda")
     noise = to_device(np.ascontiguousarray(synth.make_noise(ewl), np.float32))
-    chunk = torch.empty_like(noise)                                    # the action buffer B_a
+    chunk = torch.empty_like(noise)                                    # the expert's latest chunk
+    # the action buffer B_a as an absolute timeline: the chunk that starts at
+    # action index s occupies rows s .. s + H - 1 (Algorithm 1 reads the
+    # committed actions a_t .. a_{t+n-1} from it); sized for every iteration
+    H_a = ewl.dims.horizon
+    timeline = torch.zeros(((args.steps + max(1, args.warmup) + 4) * 2 * H_a + 64, ewl.dims.action_dim),
+                           device="cuda")
     forced = [1.0] * 6 + [-1.0]
     times = {"vlm": [], "corr": [], "act": []}
     calls = {"corr": 0}
@@ -552,10 +604,12 @@ def bench_loop(args):
         ms[0] = timed("vlm", vlm_fn)
         return 0
 
-    def corr_hook(user, t, n, from_vlm, c, ms):
-        n = max(1, min(n, ewl.dims.horizon))
+    def corr_hook(user, t, n, from_vlm, start, c, ms):
+        n = max(1, min(n, H_a))
+        committed = timeline[t:t + n]   # a_t .. a_{t+n-1}, contiguous rows
         # B_h holds the fresh compression after a refresh, else the previous item
-        ms[0] = timed("corr", lambda: jpi.check(jpi.jpi_corr_predict(corr, item, chunk, 1, n, item, conf_d, stream)))
+        ms[0] = timed("corr", lambda: jpi.check(jpi.jpi_corr_predict(corr, item, committed, 1, n, item, conf_d,
+                                                                     stream)))
         c[0] = forced[calls["corr"] % len(forced)]
         calls["corr"] += 1
         return 0
@@ -565,8 +619,10 @@ def bench_loop(args):
         ae.bind_state(None, 0, item if with_item else None, stream=stream)
         ae.denoise(noise, ewl.n_steps, out=chunk, stream=stream)
 
-    def act_hook(user, t, have_corr, ms):
+    def act_hook(user, t, have_corr, start, ms):
         ms[0] = timed("act", lambda: act_fn(have_corr))
+        ae.sync(stream)   # a timed-out wait of the single-launch kernel would invalidate the chunk
+        timeline[start:start + H_a].copy_(chunk[0])
         return 0
 
     hooks = jpi.jpi_sched_hooks(jpi.SCHED_VLM_FN(vlm_hook), jpi.SCHED_CORR_FN(corr_hook), jpi.SCHED_ACT_FN(act_hook),
@@ -575,8 +631,8 @@ def bench_loop(args):
     # warm-up (graph capture, tables), then the measured loop with Delta from the warm timings
     for _ in range(max(1, args.warmup)):
         vlm_hook(None, 0, [0.0])
-        corr_hook(None, 0, 10, 1, [0.0], [0.0])
-        act_hook(None, 0, 1, [0.0])
+        corr_hook(None, 0, 10, 1, 0, [0.0], [0.0])
+        act_hook(None, 0, 1, 0, [0.0])
     for k in times:
         times[k].clear()
     calls["corr"] = 0
@@ -704,6 +760,10 @@ def main():
         evs[i][1].record(stream)
     ev1.record(stream)
     torch.cuda.synchronize()
+    # jpi_sync reports a producer wait of the single-launch kernel that timed
+    # out (its output would be invalid): a failed call never counts as timed
+    ae.sync(stream)
+    timed_out = out.cpu().numpy()
     total_ms = ev0.elapsed_time(ev1)
     per_call = sorted(a.elapsed_time(b) for a, b in evs)
     ms_per_call = total_ms / args.steps
@@ -725,6 +785,7 @@ def main():
         for i in range(reps + 1):
             ae.denoise(noise_d, wl.n_steps, out, stream=stream)
             torch.cuda.synchronize()
+            ae.sync(stream)
             st, ms, n = jpi.jpi_debug_kernel_time(ae.ctx)
             jpi.check(st, ae.ctx)
             if i > 0:  # the first call warms the eager path
@@ -748,6 +809,11 @@ def main():
     achieved = kbytes / (k_avg_us * 1e-6) / 1e9
     print("bench: per-kernel %s" % json.dumps(per_kind), file=sys.stderr, flush=True)
 
+    traffic = MEASURED_TRAFFIC.get((kernel_source_hash(), wl.name)) if kname == "persistent" else None
+    traffic_source = ("rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE on this kernel source (sha256 %s...), recorded in "
+                      "profiles/traffic_%s_persistent.md" % (kernel_source_hash()[:12], wl.name)
+                      if traffic is not None else
+                      "none: no counter run on the current kernel source for this workload")
     call_gbs = counts["bytes_per_call"] / (ms_per_call * 1e-3) / 1e9
     call_tflops = counts["flops_per_call"] / (ms_per_call * 1e-3) / 1e12
     mfma_peak = BF16_MFMA_PEAK_TFLOPS if wl.dtype == "bf16" else FP32_MFMA_PEAK_TFLOPS
@@ -774,8 +840,8 @@ def main():
         "roofline": {"bound": "hbm", "kernel": ("k_persist (whole denoise call)" if kname == "persistent"
                                                 else "GEMM (%s)" % kname), "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": (MEASURED_TRAFFIC.get((kernel_source_hash(), wl.name))
-                                 if kname == "persistent" else None),
+                     "traffic": traffic,
+                     "traffic_source": traffic_source,
                      "bytes_per_launch": kbytes, "avg_launch_us": round(k_avg_us, 3),
                      "launches_timed": tot_n},
         "kernels": per_kind,
@@ -789,10 +855,16 @@ def main():
     mp["hbm_frac_of_measured_copy"] = round(result["roofline"]["achieved"] / mp["copy_GBs"], 4) \
         if result["roofline"]["unit"] == "GB/s" else None
     result["measured_peaks"] = mp
+    result["parity"] = {"checked": False, "why": "--no-cpu"}
     if not args.no_cpu:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(wl, weights, K, V, noise)
+        result["cpu_baseline"], ref0 = cpu_baseline(wl, weights, K, V, noise, committed, bool(args.committed_t0))
+        result["parity"] = check_output(timed_out[0], ref0, wl.dtype)
     print(json.dumps(result), flush=True)
+    if not result["parity"].get("ok", True):
+        print("bench: the timed output does not match the oracle (%s)" % json.dumps(result["parity"]),
+              file=sys.stderr, flush=True)
+        sys.exit(3)
 
 
 if __name__ == "__main__":

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define JPI_ABI_VERSION 3
+#define JPI_ABI_VERSION 4
 
 typedef enum {
   JPI_OK = 0,
@@ -244,6 +244,14 @@ jpi_status jpi_debug_gemm(const void* A, const void* W, float* C, int M, int N, 
 jpi_status jpi_debug_attention(const void* q, const void* ks, const void* vs, const void* kp, const void* vp,
                                const int32_t* prefix_len_host, int batch, int n_heads, int H, int P,
                                int Dh, jpi_dtype dt, float* out, void* stream);
+
+/* The context's transposed prefix V, the attention kernels' P.V operand:
+ * [L][max_batch][Dh][ld] of cfg.dtype, value j of rollout b, layer l at
+ * ((l*max_batch + b)*Dh + d)*ld + j.  jpi_bind_prefix fills it from the bound
+ * V; the VLM prefill's in-place hand-off writes it directly (and not the V
+ * buffer of jpi_prefix_buffers).  Read-only for callers (tests inspect it).
+ * Errors: JPI_ERR_ARG (NULL). */
+jpi_status jpi_debug_prefix_vt(jpi_ctx* ctx, void** vt_out, int* ld_out);
 
 /* ---- measurement support (used by the benchmark) ---------------------------- */
 

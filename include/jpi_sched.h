@@ -42,17 +42,30 @@ typedef struct {
 } jpi_sched_config;
 
 /* Model hooks.  Each reports the time it took (measured or simulated) in *ms.
+ * Action indices are absolute: action j is the j-th action the robot
+ * executes.  Chunks are placed on that timeline: the chunk predicted by the
+ * iteration that starts at action t, with n_committed actions committed to
+ * its prediction, covers actions [t + n_committed, t + n_committed +
+ * chunk_len) and replaces whatever an older chunk held there; the first
+ * chunk (before the loop) covers [0, chunk_len).
  *   vlm(t):  observe at action index t and run the VLM (refreshes the prefix
  *            KV buffer B_kv and the hidden state h_t); also called once at start.
- *   corr(t, n_committed, from_vlm): predict the compressed VLM state
- *            n_committed actions ahead from h_t (from_vlm = 1) or from the
- *            hidden-state buffer B_h (from_vlm = 0); write its confidence to *conf.
- *   act(t, have_corr): the action expert predicts a chunk from the
- *            prediction (have_corr = 1) or, at start, from h_0 (have_corr = 0). */
+ *   corr(t, n_committed, from_vlm, chunk_start): predict the compressed VLM
+ *            state n_committed actions ahead from h_t (from_vlm = 1) or from the
+ *            hidden-state buffer B_h (from_vlm = 0), given the committed actions
+ *            a_t .. a_{t+n_committed-1} (Algorithm 1).  chunk_start is the
+ *            first action index of the latest chunk: a_j is that chunk's action
+ *            j - chunk_start when j >= chunk_start and an older chunk's action
+ *            otherwise (the loop can run ahead of the robot, so t may be below
+ *            chunk_start).  Writes its confidence to *conf.
+ *   act(t, have_corr, chunk_start): the action expert predicts the chunk that
+ *            starts at action index chunk_start, from the prediction
+ *            (have_corr = 1) or, at start, from h_0 (have_corr = 0, t = 0,
+ *            chunk_start = 0). */
 typedef struct {
   int (*vlm)(void* user, int64_t t, double* ms);
-  int (*corr)(void* user, int64_t t, int n_committed, int from_vlm, double* conf, double* ms);
-  int (*act)(void* user, int64_t t, int have_corr, double* ms);
+  int (*corr)(void* user, int64_t t, int n_committed, int from_vlm, int64_t chunk_start, double* conf, double* ms);
+  int (*act)(void* user, int64_t t, int have_corr, int64_t chunk_start, double* ms);
   void* user;
 } jpi_sched_hooks;
 

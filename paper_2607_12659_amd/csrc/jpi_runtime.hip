@@ -604,6 +604,13 @@ jpi_status jpi_prefix_buffers(jpi_ctx* c, void** k_out, void** v_out) {
   return JPI_OK;
 }
 
+jpi_status jpi_debug_prefix_vt(jpi_ctx* c, void** vt_out, int* ld_out) {
+  if (!c || !vt_out || !ld_out) return fail(c, JPI_ERR_ARG, "jpi_debug_prefix_vt: NULL argument");
+  *vt_out = c->vpt;
+  *ld_out = c->Ppad;
+  return JPI_OK;
+}
+
 jpi_status jpi_bind_prefix(jpi_ctx* c, const void* k, const void* v, const int32_t* prefix_len_host, int batch,
                            int prefix, void* stream) {
   if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_bind_prefix: ctx is NULL");

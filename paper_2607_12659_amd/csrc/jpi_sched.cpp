@@ -33,7 +33,7 @@ int sim_vlm(void* user, int64_t, double* ms) {
   return 0;
 }
 
-int sim_corr(void* user, int64_t, int, int, double* conf, double* ms) {
+int sim_corr(void* user, int64_t, int, int, int64_t, double* conf, double* ms) {
   jpi_sched_sim* s = static_cast<jpi_sched_sim*>(user);
   *conf = s->n_conf > 0 ? s->conf[s->corr_calls % s->n_conf] : 0.0;
   ++s->corr_calls;
@@ -41,7 +41,7 @@ int sim_corr(void* user, int64_t, int, int, double* conf, double* ms) {
   return 0;
 }
 
-int sim_act(void* user, int64_t, int, double* ms) {
+int sim_act(void* user, int64_t, int, int64_t, double* ms) {
   jpi_sched_sim* s = static_cast<jpi_sched_sim*>(user);
   ++s->act_calls;
   *ms = s->ae_ms;
@@ -64,7 +64,7 @@ jpi_status jpi_sched_run(const jpi_sched_config* cfg, const jpi_sched_hooks* hoo
   // actions yet, so nothing executes during this.
   double ms_vlm = 0.0, ms_act = 0.0;
   if (hooks->vlm(hooks->user, 0, &ms_vlm) != 0) return JPI_ERR_STATE;
-  if (hooks->act(hooks->user, 0, 0, &ms_act) != 0) return JPI_ERR_STATE;
+  if (hooks->act(hooks->user, 0, 0, 0, &ms_act) != 0) return JPI_ERR_STATE;
   st.startup_ms = ms_vlm + ms_act;
 
   double conf = 0.0;  // above any threshold theta < 0: the first iteration skips the VLM
@@ -85,9 +85,11 @@ jpi_status jpi_sched_run(const jpi_sched_config* cfg, const jpi_sched_hooks* hoo
       // predict Delta_ae actions ahead from the hidden-state buffer B_h
       ev.n_committed = cfg->delta_ae;
     }
-    if (hooks->corr(hooks->user, t, ev.n_committed, ev.vlm, &conf, &part) != 0) return JPI_ERR_STATE;
+    // a_t .. a_{t+n-1}: the latest chunk starts at buf_end - chunk_len
+    if (hooks->corr(hooks->user, t, ev.n_committed, ev.vlm, buf_end - cfg->chunk_len, &conf, &part) != 0)
+      return JPI_ERR_STATE;
     ms += part;
-    if (hooks->act(hooks->user, t, 1, &part) != 0) return JPI_ERR_STATE;
+    if (hooks->act(hooks->user, t, 1, ev.t + ev.n_committed, &part) != 0) return JPI_ERR_STATE;
     ms += part;
     ev.conf_out = conf;
     ev.ms = ms;

@@ -32,6 +32,7 @@ class ActionExpert:
                  state_dim: int = 0):
         """variant: jpi.JPI_VARIANT_ADARMS (0) or JPI_VARIANT_ACTION_TIME (1, with state_dim)."""
         self.dims, self.dtype, self.device = dims, dtype, device
+        self.max_batch, self.max_prefix = max_batch, max_prefix
         cfg = _j.jpi_config(dims.n_layers, dims.width, dims.n_heads, dims.n_kv_heads, dims.head_dim,
                             dims.mlp_dim, dims.action_dim, dims.horizon, max_batch, max_prefix, _dt(dtype),
                             rms_eps, rope_base, max_corr, variant, state_dim)

@@ -20,7 +20,7 @@ JPI_F32, JPI_BF16 = 0, 1
 JPI_VARIANT_ADARMS, JPI_VARIANT_ACTION_TIME = 0, 1
 
 EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create", "jpi_destroy", "jpi_set_weight",
-            "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
+            "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_debug_prefix_vt", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
             "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
             "jpi_sched_run", "jpi_sched_sim_hooks", "jpi_vlm_create", "jpi_vlm_destroy", "jpi_vlm_set_weight",
             "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error", "jpi_set_committed_t0", "jpi_bind_robot_state", "jpi_corr_create",
@@ -64,8 +64,8 @@ class jpi_sched_config(ctypes.Structure):
 
 SCHED_VLM_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(ctypes.c_double))
 SCHED_CORR_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
-                                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double))
-SCHED_ACT_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                 ctypes.c_int64, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double))
+SCHED_ACT_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int64,
                                 ctypes.POINTER(ctypes.c_double))
 
 
@@ -113,6 +113,7 @@ _sig = {
     "jpi_set_weight": (_i, [_vp, ctypes.c_char_p, _vp, _i64, _i, _i, _vp]),
     "jpi_finalize_weights": (_i, [_vp, _vp]),
     "jpi_prefix_buffers": (_i, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp)]),
+    "jpi_debug_prefix_vt": (_i, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_i)]),
     "jpi_bind_prefix": (_i, [_vp, _vp, _vp, _vp, _i, _i, _vp]),
     "jpi_bind_state": (_i, [_vp, _vp, _i, _vp, _i, _vp]),
     "jpi_denoise": (_i, [_vp, _vp, _i, _vp, _vp]),
@@ -212,6 +213,12 @@ def jpi_prefix_buffers(ctx):
     k, v = _vp(), _vp()
     st = _lib.jpi_prefix_buffers(ctx, ctypes.byref(k), ctypes.byref(v))
     return st, k.value, v.value
+
+
+def jpi_debug_prefix_vt(ctx):
+    vt, ld = _vp(), _i()
+    st = _lib.jpi_debug_prefix_vt(ctx, ctypes.byref(vt), ctypes.byref(ld))
+    return st, vt.value, ld.value
 
 
 def jpi_bind_prefix(ctx, k, v, prefix_len_host, batch: int, prefix: int, stream=None) -> int:

@@ -141,6 +141,7 @@ class Workload:
     dtype: str           # "f32" or "bf16": storage type of matrices and prefix KV
     seed: int = DEFAULT_SEED
     prefix_len: tuple = field(default=())   # per-rollout valid prefix length; () = all `prefix`
+    mod_gain: float = 1.0  # power of two multiplying every layer's modulation matrix and bias
 
     def valid_lengths(self):
         return list(self.prefix_len) if self.prefix_len else [self.prefix] * self.batch
@@ -190,10 +191,22 @@ def weight_specs(d: Dims):
 
 def make_weights(wl: Workload, std: float = WEIGHT_STD):
     """name -> array.  Matrices are fp32 on the fp32 path and bf16 bit patterns
-    (uint16) on the bf16 path; biases are always fp32."""
+    (uint16) on the bf16 path; biases are always fp32.
+
+    ``wl.mod_gain`` (a power of two, so that the bf16 rounding of the scaled
+    values is the scaled rounding) multiplies the layers' attention and MLP
+    modulation tensors: with N(0, 0.02) weights the adaRMSNorm gates are about
+    0.06, which damps every sublayer; a gain of 8 makes each sublayer move the
+    residual stream by tens of percent."""
+    g = float(wl.mod_gain)
+    m, e = np.frexp(g)
+    if g <= 0 or m != 0.5:
+        raise ValueError("mod_gain must be a power of two")
     out = {}
     for name, shape, is_mat in weight_specs(wl.dims):
         a = normal_f32(wl.seed, name, std, shape)
+        if g != 1.0 and ("attn_mod" in name or "mlp_mod" in name):
+            a = a * np.float32(g)
         if is_mat and wl.dtype == "bf16":
             a = f32_to_bf16_bits(a)
         out[name] = a

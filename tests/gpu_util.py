@@ -160,3 +160,42 @@ def device_view_i16(ptr, shape):
 
 def bf16_bits_to_f64(bits):
     return (np.ascontiguousarray(bits).view(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+# bf16-path bars.  The spec bar is a per-rollout relative L2 error of
+# 2e-2; a norm over a whole chunk can hide one badly wrong element, so every
+# bf16 comparison also bounds each element by 2e-2 of its rollout's largest
+# reference magnitude.
+BF16_REL = 2e-2
+BF16_ELEM = 2e-2
+
+
+def elem_err_per_rollout(got, ref):
+    """max over rollouts of max|got_b - ref_b| / max|ref_b|."""
+    B = got.shape[0]
+    num = np.abs(got - ref).reshape(B, -1).max(1)
+    den = np.abs(ref).reshape(B, -1).max(1)
+    return float((num / den).max())
+
+
+def assert_bf16(got, ref, label="", reg_rel=None, reg_abs=None):
+    """Assert the bf16 bars (relative L2 and element-wise) per rollout, plus
+    optional regression bars (tighter than the contract: a relative L2 and a
+    max-abs well above the measured error).  Returns (rel, max_abs)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if got.ndim == 1:
+        got, ref = got[None], ref[None]
+    rel = rel_l2_per_rollout(got, ref)
+    elem = elem_err_per_rollout(got, ref)
+    mabs = float(np.abs(got - ref).max())
+    if label:
+        print("%s: rel-L2 %.3e elem %.3e max-abs %.3e" % (label, rel, elem, mabs), flush=True)
+    assert np.isfinite(got).all(), label
+    assert rel <= BF16_REL, (label, rel)
+    assert elem <= BF16_ELEM, (label, elem)
+    if reg_rel is not None:
+        assert rel <= reg_rel, (label, rel, reg_rel)
+    if reg_abs is not None:
+        assert mabs <= reg_abs, (label, mabs, reg_abs)
+    return rel, mabs

@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     j = _lib()
-    assert j.jpi_abi_version() == 3
+    assert j.jpi_abi_version() == 4
     for st in range(8):
         assert j.jpi_status_str(st)
     assert j.jpi_status_str(99) == "unknown status"
@@ -123,3 +123,4 @@ def test_build_entry_compiles_everything():
     import importlib
     ge = importlib.import_module("__graft_entry__")
     assert callable(ge.build) and callable(ge.smoke)
+

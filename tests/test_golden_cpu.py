@@ -29,6 +29,22 @@ def _metas():
 def test_every_case_has_a_golden():
     names = {n for n, _ in _metas()}
     assert set(make_golden.CASES) <= names
+    for n in make_golden.VLM_CASES:
+        assert os.path.exists(os.path.join(HERE, "golden", n + ".npz"))
+
+
+@pytest.mark.parametrize("name", sorted(make_golden.VLM_CASES))
+def test_vlm_golden_made_by_current_sources(name):
+    with open(os.path.join(HERE, "golden", name + ".json")) as f:
+        meta = json.load(f)
+    assert meta["vlm_oracle_sha256"] == make_golden.source_hash(*make_golden.vlm_oracle_files()), \
+        "VLM oracle changed since %s was generated: rerun tests/golden/make_golden.py %s" % (name, name)
+    assert meta["vlm_synth_sha256"] == make_golden.source_hash(*make_golden.vlm_synth_files())
+    g = np.load(os.path.join(HERE, "golden", name + ".npz"), allow_pickle=False)
+    L, T = meta["n_layers"], len(meta["tokens"])
+    assert g["K"].shape == (L, T, 256) and g["V"].shape == (L, T, 256) and g["hidden"].shape == (T, 2048)
+    assert list(g["tokens"]) == meta["tokens"] and meta["tokens"][0] == 0 and meta["tokens"][-1] == meta["prefix"] - 1
+    assert all(np.isfinite(g[k]).all() for k in ("K", "V", "hidden"))
 
 
 @pytest.mark.parametrize("name,meta", _metas())

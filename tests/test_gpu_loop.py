@@ -11,7 +11,8 @@ import pytest
 import oracle
 import synth
 import synth.vlm as sv
-from gpu_util import Corr, Vlm, bf16_bits_to_f64, make_expert, rel_l2_per_rollout, torch_cuda
+from gpu_util import (BF16_ELEM, Corr, Vlm, bf16_bits_to_f64, elem_err_per_rollout, make_expert,
+                      rel_l2_per_rollout, torch_cuda)
 from oracle import correction as oc
 from synth import correction as sc
 
@@ -45,6 +46,7 @@ def test_schedule_loop_with_all_models_tiny():
     chunk = torch.empty_like(n_d)
     forced = [1.0, -1.0, 1.0, 1.0, 1.0]
     log = []                          # (kind, inputs, outputs) on the host, in call order
+    timeline, starts = {}, []         # the action buffer B_a on the absolute action index
 
     def host(t):
         return t.cpu().numpy()
@@ -58,22 +60,27 @@ def test_schedule_loop_with_all_models_tiny():
         ms[0] = 1.0
         return 0
 
-    def corr_hook(user, t, n, from_vlm, c, ms):
+    def corr_hook(user, t, n, from_vlm, start, c, ms):
         n = max(1, min(n, awl.dims.horizon))
         src = host(item).copy()       # B_h: the fresh compression after a refresh, else the last item
-        acts = host(chunk)[:, :n].copy()
-        corr.predict(item, chunk, 1, n, item=item)
+        # a_t .. a_{t+n-1} from the action timeline (older chunks below `start`)
+        assert start == starts[-1] and all(j in timeline for j in range(t, t + n))
+        acts = np.stack([timeline[j] for j in range(t, t + n)])[None].astype(np.float32)
+        corr.predict(item, to_device(acts), 1, n, item=item)
         torch.cuda.synchronize()
         log.append(("corr", (src, acts), host(item).copy()))
         c[0] = forced[sum(1 for k in log if k[0] == "corr") - 1]
         ms[0] = 0.1
         return 0
 
-    def act_hook(user, t, have_corr, ms):
+    def act_hook(user, t, have_corr, start, ms):
         ae.bind_state(None, 0, item if have_corr else None)
         ae.denoise(n_d, awl.n_steps, out=chunk)
         ae.sync()
         torch.cuda.synchronize()
+        starts.append(start)
+        for p, a in enumerate(host(chunk)[0]):
+            timeline[start + p] = a
         log.append(("act", host(item).copy() if have_corr else None, host(chunk).copy()))
         ms[0] = 2.0
         return 0
@@ -95,19 +102,28 @@ def test_schedule_loop_with_all_models_tiny():
     Kr, Vr, hid = oracle.vlm_prefill(vwl.dims, vw, emb[0])
     ex = oracle.Expert(awl.dims, aw)
     worst = {"vlm": 0.0, "corr": 0.0, "act": 0.0}
+    worst_elem = dict(worst)
+
+    def track(kind, got, ref):
+        worst[kind] = max(worst[kind], rel_l2_per_rollout(got, ref))
+        worst_elem[kind] = max(worst_elem[kind], elem_err_per_rollout(got, ref))
+
     for kind, inp, out in log:
         if kind == "vlm":
             got_hidden = bf16_bits_to_f64(inp)[0]
-            worst["vlm"] = max(worst["vlm"], rel_l2_per_rollout(got_hidden[None], hid[None]))
+            track("vlm", got_hidden[None], hid[None])
             ref_c = oc.compress(cwl.dims, cw, inp[0].view(np.uint16))   # compression of the GPU's hidden state
-            worst["vlm"] = max(worst["vlm"], rel_l2_per_rollout(out.astype(np.float64), ref_c[None]))
+            track("vlm", out.astype(np.float64), ref_c[None])
         elif kind == "corr":
             src, acts = inp
             ref_item, _ = oc.forward(cwl.dims, cw, acts.astype(np.float64), state=src.astype(np.float64))
-            worst["corr"] = max(worst["corr"], rel_l2_per_rollout(out.astype(np.float64), ref_item))
+            track("corr", out.astype(np.float64), ref_item)
         else:
             ref = oracle.denoise(ex, noise, Kr[:, None], Vr[:, None], [vwl.prefix], awl.n_steps,
                                  corr=None if inp is None else inp.astype(np.float64))
-            worst["act"] = max(worst["act"], rel_l2_per_rollout(out.astype(np.float64), ref))
-    print("worst rel-L2 per hook kind: %s" % {k: "%.2e" % v for k, v in worst.items()}, flush=True)
+            track("act", out.astype(np.float64), ref)
+    print("worst rel-L2 per hook kind: %s; element-wise %s" % ({k: "%.2e" % v for k, v in worst.items()},
+                                                               {k: "%.2e" % v for k, v in worst_elem.items()}),
+          flush=True)
     assert max(worst.values()) <= BF16_TOL
+    assert max(worst_elem.values()) <= BF16_ELEM

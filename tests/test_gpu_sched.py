@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 
 import synth
-from gpu_util import load_golden, make_expert, rel_l2_per_rollout, torch_cuda
+from gpu_util import assert_bf16, load_golden, make_expert, rel_l2_per_rollout, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -48,13 +48,14 @@ def test_schedule_loop_with_the_gpu_action_expert():
             ms[0] = dt
             return 0
 
-        def corr(user, t, n, from_vlm, c, ms):
+        def corr(user, t, n, from_vlm, start, c, ms):
             c[0] = conf[len(outs) % len(conf)]
             ms[0] = 0.0
             return 0
 
-        def act(user, t, have_corr, ms):
+        def act(user, t, have_corr, start, ms):
             out, dt = timed(lambda: ae.denoise(noise, wl.n_steps))
+            ae.sync()   # the single-launch kernel's status: a timed-out wait invalidates the chunk
             outs.append(out.cpu().numpy().astype(np.float64))
             t_act.append(dt)
             ms[0] = dt
@@ -67,7 +68,7 @@ def test_schedule_loop_with_the_gpu_action_expert():
         assert st == jpi.JPI_OK
         assert len(outs) == 10                          # the initial chunk + one per iteration
         for o in outs:
-            assert rel_l2_per_rollout(o, ref) <= 2e-2
+            assert_bf16(o, ref, reg_rel=2e-3, reg_abs=1e-2)
         assert stats.vlm_calls == sum(e.vlm for e in ev) and stats.vlm_calls >= 2
         loop_act = sum(t_act[1:])
         loop_vlm = sum(t_vlm[1:])

@@ -37,6 +37,15 @@ def _kp_layers(ae, L, Pmax, Dh, prefix):
     return bf16_bits_to_f64(kv[:, 0, :prefix])
 
 
+def _vt_layers(ae, L, Dh, _unused=None):
+    """The expert's transposed prefix V of rollout 0, [L][Dh][ld] as fp64."""
+    from paper_2607_12659_amd import jpi
+    st, vt_ptr, ld = jpi.jpi_debug_prefix_vt(ae.ctx)
+    assert st == jpi.JPI_OK
+    raw = device_view_i16(vt_ptr, (L, ae.max_batch, Dh, ld)).cpu().numpy()
+    return bf16_bits_to_f64(raw[:, 0])
+
+
 def ae_prefix_ptrs(ae):
     from paper_2607_12659_amd import jpi
     k = ctypes.c_void_p()
@@ -106,30 +115,50 @@ def test_vlm_gemma_width_two_layers():
 
 
 def test_vlm_full_gemma_into_pi05_expert():
-    # all 18 layers at full size into the pi0.5 expert: K is bit-identical
-    # across two prefills, the expert's actions are finite and repeat exactly
+    """All 18 layers at full size (816 tokens) into the pi0.5 expert: K and V
+    of every layer and the final hidden state against the stored oracle run
+    (tests/golden/gemma2b-p816-l18: 32 evenly spaced token positions), then
+    the expert's actions on that KV repeat exactly across two prefills."""
     torch = torch_cuda()
     from paper_2607_12659_amd.expert import to_device
+    from gpu_util import GOLDEN, assert_bf16
+    import json
+    import os
     vwl = synth_vlm.VLM_WORKLOADS["gemma2b-p816"]
-    print("case gemma2b-p816 full into pi05 expert", flush=True)
+    g = np.load(os.path.join(GOLDEN, "gemma2b-p816-l18.npz"), allow_pickle=False)
+    with open(os.path.join(GOLDEN, "gemma2b-p816-l18.json")) as f:
+        meta = json.load(f)
+    assert meta["n_layers"] == vwl.dims.n_layers == 18 and meta["prefix"] == vwl.prefix
+    tok = g["tokens"]
+    print("case gemma2b-p816 full (18 layers) into pi05 expert", flush=True)
     vlm = Vlm(vwl.dims, synth_vlm.make_vlm_weights(vwl), 1, vwl.prefix)
     ewl = synth.WORKLOADS["pi05-b1"]
     ae = make_expert(ewl, synth.make_weights(ewl), max_batch=1, max_prefix=vwl.prefix)
     try:
         emb = to_device(np.ascontiguousarray(synth_vlm.make_embeddings(vwl), np.float32))
         noise = to_device(np.ascontiguousarray(synth.make_noise(ewl), np.float32))
+        hidden = torch.empty((1, vwl.prefix, vwl.dims.width), dtype=torch.int16, device="cuda")
         outs, ks = [], []
-        for _ in range(2):
-            vlm.prefill(emb, 1, vwl.prefix, ae)
+        for rep in range(2):
+            vlm.prefill(emb, 1, vwl.prefix, ae, hidden if rep == 0 else None)
             out = ae.denoise(noise, ewl.n_steps)
             ae.sync()
             outs.append(out.cpu().numpy())
-            _, k_ptr, _ = ae_prefix_ptrs(ae)
+            _, k_ptr, v_ptr = ae_prefix_ptrs(ae)
             ks.append(device_view_i16(k_ptr, (vwl.dims.n_layers, 1, vwl.prefix, vwl.dims.head_dim)).cpu().numpy())
+            if rep == 0:
+                # the prefill writes V transposed ([L][max_batch][Dh][ld]), the
+                # attention kernels' operand
+                vt = _vt_layers(ae, vwl.dims.n_layers, vwl.dims.head_dim)
+        Kg = bf16_bits_to_f64(ks[0][:, 0][:, tok])
+        Vg = vt[:, :, tok].transpose(0, 2, 1)
+        for l in range(vwl.dims.n_layers):
+            assert_bf16(Kg[l][None], g["K"][l][None].astype(np.float64), "K layer %d" % l)
+            assert_bf16(Vg[l][None], g["V"][l][None].astype(np.float64), "V layer %d" % l)
+        hg = bf16_bits_to_f64(hidden.cpu().numpy())[0][tok]
+        assert_bf16(hg[None], g["hidden"][None].astype(np.float64), "final hidden state")
         assert np.isfinite(outs[0]).all()
         assert np.array_equal(outs[0], outs[1]) and np.array_equal(ks[0], ks[1])
-        # the last layer's keys are far from the embeddings' scale (18 layers ran)
-        assert np.abs(bf16_bits_to_f64(ks[0][-1])).mean() > 0.0
     finally:
         ae.close()
         vlm.close()

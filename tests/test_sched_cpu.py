@@ -128,13 +128,13 @@ def test_python_hooks_drive_the_same_loop():
         ms[0] = 300.0
         return 0
 
-    def corr(user, t, n, from_vlm, conf, ms):
+    def corr(user, t, n, from_vlm, start, conf, ms):
         calls.append(("corr", t, n, from_vlm))
         conf[0] = -1.0 if len(calls) % 5 == 0 else 0.0
         ms[0] = 2.0
         return 0
 
-    def act(user, t, have_corr, ms):
+    def act(user, t, have_corr, start, ms):
         calls.append(("act", t, have_corr))
         ms[0] = 100.0
         return 0
@@ -147,6 +147,57 @@ def test_python_hooks_drive_the_same_loop():
     for e in ev:
         assert e.ms == pytest.approx(102.0 + (300.0 if e.vlm else 0.0))
     # a failing hook stops the loop
-    hooks2 = j.jpi_sched_hooks(j.SCHED_VLM_FN(vlm), j.SCHED_CORR_FN(corr), j.SCHED_ACT_FN(lambda u, t, h, ms: 1), None)
+    hooks2 = j.jpi_sched_hooks(j.SCHED_VLM_FN(vlm), j.SCHED_CORR_FN(corr), j.SCHED_ACT_FN(lambda u, t, h, c, ms: 1),
+                               None)
     st, _, _ = j.jpi_sched_run(cfg, hooks2, 0)
     assert st == j.JPI_ERR_STATE
+
+
+@pytest.mark.parametrize("model_ms", [12.0, 37.0, 260.0])
+def test_hooks_get_the_committed_actions_from_the_timeline(model_ms):
+    """Chunks are placed on the absolute action timeline: act(t, .., start)
+    writes actions [start, start + chunk_len), and corr(t, n, .., start) must
+    find a_t .. a_{t+n-1} there -- from the latest chunk where j >= start,
+    from an older one below it (a loop faster than the robot runs ahead of
+    the execution, so t < start happens).  Checked for a fast, a medium and a
+    slow model against a 20 ms control period."""
+    j = _j()
+    chunk = 10
+    timeline = {}        # action index -> (chunk id, position in the chunk)
+    starts, seen = [], {"behind": 0, "ahead": 0}
+
+    def vlm(user, t, ms):
+        ms[0] = model_ms
+        return 0
+
+    def corr(user, t, n, from_vlm, start, conf, ms):
+        assert start == starts[-1]                        # the latest chunk
+        for a in range(t, t + n):
+            cid, pos = timeline[a]                        # every committed action exists
+            if a >= start:
+                assert cid == len(starts) - 1 and pos == a - start
+            else:
+                assert cid < len(starts) - 1
+        seen["behind" if t < start else "ahead"] += 1
+        conf[0] = 1.0
+        ms[0] = model_ms
+        return 0
+
+    def act(user, t, have_corr, start, ms):
+        if not starts:
+            assert (t, have_corr, start) == (0, 0, 0)
+        else:
+            assert start >= t
+        starts.append(start)
+        for p in range(chunk):
+            timeline[start + p] = (len(starts) - 1, p)
+        ms[0] = model_ms
+        return 0
+
+    hooks = j.jpi_sched_hooks(j.SCHED_VLM_FN(vlm), j.SCHED_CORR_FN(corr), j.SCHED_ACT_FN(act), None)
+    cfg = j.jpi_sched_config(theta=-0.5, delta=4, delta_ae=4, chunk_len=chunk, action_ms=20.0, iterations=40)
+    st, stats, ev = j.jpi_sched_run(cfg, hooks, 40)
+    assert st == j.JPI_OK
+    assert [e.t + e.n_committed for e in ev] == starts[1:]
+    if model_ms < 20.0 * 4 / 2:
+        assert seen["behind"] > 0        # the loop ran ahead of the robot
