@@ -44,6 +44,7 @@
 #ifndef JPI_H_
 #define JPI_H_
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -234,6 +235,26 @@ jpi_status jpi_sync(jpi_ctx* ctx, void* stream);
  * multiple of 32*splitk). */
 jpi_status jpi_debug_gemm(const void* A, const void* W, float* C, int M, int N, int K, jpi_dtype dt,
                           int splitk, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the GEMM of
+ * jpi_debug_gemm -- same arguments, same kernels, same fixed-order split-K
+ * reduction, bitwise the same result -- without any allocation and without
+ * synchronising the stream (the result is ready in stream order).  The
+ * split-K partial slices (splitk * M * N fp32; none when splitk == 1) live in
+ * a static device array of jpi_gemm_noalloc_scratch_bytes() bytes (16 MiB)
+ * that each GPU holds from the library's load until the process ends; larger
+ * requests fail with JPI_ERR_ARG before anything is enqueued.  Every call on
+ * one GPU shares that array: calls whose execution overlaps on one GPU
+ * (different streams, or host threads) race on it and must be ordered by the
+ * caller.  The array keeps the last call's contents; nothing in it needs to
+ * start at zero.  Errors: JPI_ERR_ARG (as jpi_debug_gemm, plus the size
+ * limit), JPI_ERR_HIP (a launch failed); the text of the last failure on the
+ * calling thread is jpi_gemm_noalloc_last_error(). */
+jpi_status jpi_gemm_noalloc(const void* A, const void* W, float* C, int M, int N, int K, jpi_dtype dt, int splitk,
+                            void* stream);
+size_t jpi_gemm_noalloc_scratch_bytes(void);
+const char* jpi_gemm_noalloc_last_error(void);
 
 /* Prefix+self attention of one layer for `batch` rollouts with one shared KV
  * head, as used inside jpi_denoise (queries already rotated):

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libjpi.so")
-SOURCES = ["jpi_kernels.hip", "jpi_flash.hip", "jpi_block.hip", "jpi_variant.hip", "jpi_persist.hip", "jpi_runtime.hip", "jpi_vlm.hip", "jpi_corr.hip", "jpi_sched.cpp"]
+SOURCES = ["jpi_kernels.hip", "jpi_flash.hip", "jpi_block.hip", "jpi_variant.hip", "jpi_persist.hip", "jpi_runtime.hip", "jpi_vlm.hip", "jpi_corr.hip", "jpi_noalloc.hip", "jpi_sched.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
          # no packed-fp32 instructions in device code

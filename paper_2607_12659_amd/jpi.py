@@ -21,7 +21,8 @@ JPI_VARIANT_ADARMS, JPI_VARIANT_ACTION_TIME = 0, 1
 
 EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create", "jpi_destroy", "jpi_set_weight",
             "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_debug_prefix_vt", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
-            "jpi_sync", "jpi_debug_gemm", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
+            "jpi_sync", "jpi_debug_gemm", "jpi_gemm_noalloc", "jpi_gemm_noalloc_scratch_bytes",
+            "jpi_gemm_noalloc_last_error", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
             "jpi_sched_run", "jpi_sched_sim_hooks", "jpi_vlm_create", "jpi_vlm_destroy", "jpi_vlm_set_weight",
             "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error", "jpi_set_committed_t0", "jpi_bind_robot_state", "jpi_corr_create",
             "jpi_corr_destroy", "jpi_corr_set_weight", "jpi_corr_finalize_weights", "jpi_corr_compress",
@@ -119,6 +120,9 @@ _sig = {
     "jpi_denoise": (_i, [_vp, _vp, _i, _vp, _vp]),
     "jpi_sync": (_i, [_vp, _vp]),
     "jpi_debug_gemm": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "jpi_gemm_noalloc": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "jpi_gemm_noalloc_scratch_bytes": (ctypes.c_size_t, []),
+    "jpi_gemm_noalloc_last_error": (ctypes.c_char_p, []),
     "jpi_debug_attention": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
     "jpi_debug_time_kernel": (_i, [_vp, _i]),
     "jpi_debug_kernel_time": (_i, [_vp, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_i)]),
@@ -241,6 +245,18 @@ def jpi_sync(ctx, stream=None) -> int:
 
 def jpi_debug_gemm(A, W, C, M: int, N: int, K: int, dtype: int, splitk: int = 1, stream=None) -> int:
     return _lib.jpi_debug_gemm(addr(A), addr(W), addr(C), M, N, K, dtype, splitk, stream_handle(stream))
+
+
+def jpi_gemm_noalloc(A, W, C, M: int, N: int, K: int, dtype: int, splitk: int = 1, stream=None) -> int:
+    return _lib.jpi_gemm_noalloc(addr(A), addr(W), addr(C), M, N, K, dtype, splitk, stream_handle(stream))
+
+
+def jpi_gemm_noalloc_scratch_bytes() -> int:
+    return _lib.jpi_gemm_noalloc_scratch_bytes()
+
+
+def jpi_gemm_noalloc_last_error() -> str:
+    return (_lib.jpi_gemm_noalloc_last_error() or b"").decode()
 
 
 def jpi_debug_attention(q, ks, vs, kp, vp, prefix_len_host, batch, n_heads, H, P, Dh, dtype, out, stream=None) -> int:

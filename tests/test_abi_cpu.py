@@ -124,3 +124,18 @@ def test_build_entry_compiles_everything():
     ge = importlib.import_module("__graft_entry__")
     assert callable(ge.build) and callable(ge.smoke)
 
+
+def test_noalloc_gemm_rejects_bad_arguments_on_the_host():
+    """jpi_gemm_noalloc checks every argument, including the static scratch
+    limit, before touching a device (no GPU here; the pointers are never
+    dereferenced)."""
+    j = _lib()
+    fake = 0x1000
+    assert j.jpi_gemm_noalloc_scratch_bytes() == 16 << 20
+    assert j.jpi_gemm_noalloc(None, fake, fake, 50, 1024, 1024, j.JPI_BF16, 1) == j.JPI_ERR_ARG
+    assert j.jpi_gemm_noalloc(fake, fake, fake, 0, 1024, 1024, j.JPI_BF16, 1) == j.JPI_ERR_ARG
+    assert j.jpi_gemm_noalloc(fake, fake, fake, 50, 1024, 1000, j.JPI_BF16, 1) == j.JPI_ERR_ARG
+    assert "multiple of" in j.jpi_gemm_noalloc_last_error()
+    # 16 slices of 64 x 8192 fp32 = 32 MiB > 16 MiB
+    assert j.jpi_gemm_noalloc(fake, fake, fake, 64, 8192, 4096, j.JPI_BF16, 16) == j.JPI_ERR_ARG
+    assert "exceeds the static scratch" in j.jpi_gemm_noalloc_last_error()
