@@ -276,6 +276,18 @@ jpi_status jpi_debug_prefix_vt(jpi_ctx* ctx, void** vt_out, int* ld_out);
 
 /* ---- measurement support (used by the benchmark) ---------------------------- */
 
+/* Phase timestamps of the last single-launch denoise (a library built with
+ * the kernel's trace mode, -DJPI_PERSIST_TRACE=1, by
+ * paper_2607_12659_amd/trace_links.py; the normal build returns
+ * JPI_ERR_UNSUPPORTED).  Sets *n_workgroups (the launch's grid), *n_slots
+ * (1 + phases of the call: slot 0 is each workgroup's start, slot 1 + p the
+ * end of phase p, 8 phases per layer) and *ticks_per_us of the counter;
+ * when host_out holds cap >= n_workgroups * n_slots entries it also
+ * synchronises the device and copies the stamps, [workgroup][slot].
+ * Errors: JPI_ERR_ARG (NULL), JPI_ERR_UNSUPPORTED, JPI_ERR_HIP. */
+jpi_status jpi_debug_persist_trace(jpi_ctx* ctx, uint64_t* host_out, int64_t cap, int* n_workgroups, int* n_slots,
+                                   double* ticks_per_us);
+
 /* Kernel kinds of one denoise step, in launch order per layer. */
 typedef enum {
   JPI_KERNEL_NONE = -1,

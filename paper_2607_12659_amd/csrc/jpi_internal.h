@@ -154,6 +154,8 @@ struct PersistArgs {
   unsigned* flags;          // [grid][32] completion flags: the last phase index + 2 each workgroup finished
   unsigned* err;            // set to 1 if a wait for producers timed out
   hipEvent_t ev_start, ev_stop;
+  unsigned long long* trace;  // trace build only: [grid][trace_slots] real-time stamps (else null)
+  int trace_slots;            // 1 + phases recorded per workgroup
 };
 bool persist_supported(jpi_dtype dt, int M, int W, int nH, int Dh, int F, int H, int A, int Pmax);
 int persist_chunks(int P, int H);
@@ -161,6 +163,7 @@ int persist_pick_split(int tiles, int K, int grid);
 int persist_block_threads();
 int persist_max_grid();    // largest grid the completion flags support
 int persist_flag_words();  // size of the completion flag buffer in 32-bit words
+bool persist_trace_build(); // the kernel was compiled with JPI_PERSIST_TRACE (phase timestamps)
 // dst = fragment-ordered copy of the row-major bf16 matrix src [R][K]
 hipError_t launch_frag_order(const void* src, void* dst, int R, int K, hipStream_t s);
 hipError_t persist_occupancy(int Dh, int* blocks_per_cu);

@@ -80,6 +80,13 @@ constexpr int OUT_G = 16;  // action-out projection: 16-byte weight granules per
 #ifndef A_BATCH
 #define A_BATCH 4  // k steps of activation fragments per wave in flight (measured best)
 #endif
+// Trace build (-DJPI_PERSIST_TRACE=1, never the default): every workgroup
+// stores the real-time counter at its start and at the end of every phase,
+// trace[workgroup][1 + phase], so that the critical path of each link can be
+// reconstructed on the host.
+#ifndef JPI_PERSIST_TRACE
+#define JPI_PERSIST_TRACE 0
+#endif
 
 enum : int { EPI_QKV = 0, EPI_GEGLU = 1, EPI_SLICE = 2 };
 
@@ -249,6 +256,13 @@ __device__ __forceinline__ void phase_done(const PersistArgs& a, u32 value) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (threadIdx.x == 0) st4(rsrc(a.flags), blockIdx.x * (FLAG_STRIDE * 4u), value);
+}
+
+// Trace build only: the real-time counter after phase `slot - 1` (slot 0:
+// the workgroup's start) into trace[workgroup][slot].
+__device__ __forceinline__ void trace_mark(const PersistArgs& a, int slot) {
+  if (JPI_PERSIST_TRACE && a.trace && threadIdx.x == 0 && slot < a.trace_slots)
+    a.trace[(size_t)blockIdx.x * a.trace_slots + slot] = __builtin_amdgcn_s_memrealtime();
 }
 
 // ---------------------------------------------------------------------------
@@ -883,6 +897,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     }
   }
   __syncthreads();
+  trace_mark(a, 0);
   lds_t* wt = (lds_t*)s_wt;
   const int last_phase = a.n_steps * L * 8 - 1;
   // ph = -1 is the first step's in-projection; the later ones follow the final
@@ -935,6 +950,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
       inproj_row(a, ti, ti + W, s_hrow, s_bin, s_x, reinterpret_cast<float*>(smem), crow);
     }
     if (ph < last_phase) phase_done(a, (u32)(ph + 2));
+    if (ph >= 0) trace_mark(a, ph + 1);
   }
   if (owner && t < A && ia >= 0) a.x[xrow * A + t] = xreg;
 }
@@ -982,6 +998,8 @@ int persist_block_threads() { return PT; }
 int persist_max_grid() { return MAX_GRID; }
 
 int persist_flag_words() { return FLAG_WORDS; }
+
+bool persist_trace_build() { return JPI_PERSIST_TRACE != 0; }
 
 hipError_t launch_frag_order(const void* src, void* dst, int R, int K, hipStream_t s) {
   if (R % 16 != 0 || K % 32 != 0) return hipErrorInvalidValue;

@@ -139,6 +139,8 @@ struct jpi_ctx {
   // single-launch (persistent) path
   unsigned* pflags = nullptr;  // completion flag lines of the single-launch kernel (one per workgroup)
   unsigned* perr = nullptr;    // set when a wait for producers timed out
+  unsigned long long* ptrace = nullptr;  // trace build only: [max grid][trace_slots] phase timestamps
+  int trace_slots = 0, trace_grid = 0, trace_used = 0;
   int persist_occ = -1;        // workgroups per CU the persistent kernel fits (-1: not queried)
   void* w_frag = nullptr;      // layer weights with every matrix fragment-ordered
   bool frag_ready = false;     // w_frag matches w_layers
@@ -300,7 +302,7 @@ jpi_status jpi_destroy(jpi_ctx* c) {
                   c->w_layers, c->w_in, c->w_t0, c->w_t1, c->w_mod, c->w_out, c->b_in, c->b_t0, c->b_t1, c->b_mod,
                   c->b_out, c->kp, c->vp, c->vpt, c->d_prefix_len, c->rope_tab, c->committed, c->corr, c->x, c->h, c->y, c->q, c->ks,
                   c->vst, c->o, c->z, c->partial, c->opart, c->pflags, c->perr, c->w_frag, c->ysw, c->osw,
-                  c->zsw, c->qsw};
+                  c->zsw, c->qsw, c->ptrace};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   if (c->h_prefix_len) (void)hipHostFree(c->h_prefix_len);
@@ -424,6 +426,11 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   ALLOC(c->z, M * F * es);
   ALLOC(c->pflags, (size_t)persist_flag_words() * sizeof(unsigned));
   ALLOC(c->perr, 256);
+  if (persist_trace_build()) {  // room for 64 Euler steps of every layer's 8 phases
+    c->trace_slots = 1 + 64 * c->L * 8;
+    c->trace_grid = persist_max_grid();
+    ALLOC(c->ptrace, (size_t)c->trace_grid * c->trace_slots * sizeof(unsigned long long));
+  }
   if (g.variant == JPI_VARIANT_ACTION_TIME) {
     const size_t B = c->Bmax, SD = g.state_dim;
     ALLOC(c->w_atm_a, W * W * es);
@@ -601,6 +608,25 @@ jpi_status jpi_prefix_buffers(jpi_ctx* c, void** k_out, void** v_out) {
   if (!c || !k_out || !v_out) return fail(c, JPI_ERR_ARG, "jpi_prefix_buffers: NULL argument");
   *k_out = c->kp;
   *v_out = c->vp;
+  return JPI_OK;
+}
+
+jpi_status jpi_debug_persist_trace(jpi_ctx* c, uint64_t* host_out, int64_t cap, int* n_workgroups, int* n_slots,
+                                   double* ticks_per_us) {
+  if (!c || !n_workgroups || !n_slots || !ticks_per_us)
+    return fail(c, JPI_ERR_ARG, "jpi_debug_persist_trace: NULL argument");
+  if (!c->ptrace) return fail(c, JPI_ERR_UNSUPPORTED, "jpi_debug_persist_trace: library built without the trace mode");
+  *n_workgroups = c->n_cu;
+  *n_slots = c->trace_used;
+  int khz = 0;
+  HIPCHK(c, hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->device));
+  *ticks_per_us = khz / 1000.0;
+  const int64_t need = (int64_t)c->n_cu * c->trace_used;
+  if (!host_out || cap < need) return JPI_OK;  // sizes only
+  HIPCHK(c, hipSetDevice(c->device));
+  HIPCHK(c, hipDeviceSynchronize());
+  HIPCHK(c, hipMemcpy2D(host_out, (size_t)c->trace_used * 8, c->ptrace, (size_t)c->trace_slots * 8,
+                        (size_t)c->trace_used * 8, (size_t)c->n_cu, hipMemcpyDeviceToHost));
   return JPI_OK;
 }
 
@@ -1041,6 +1067,9 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     pa.z = c->zsw;
     pa.flags = c->pflags;
     pa.err = c->perr;
+    pa.trace = c->ptrace;
+    pa.trace_slots = c->trace_slots;
+    c->trace_used = std::min(c->trace_slots, 1 + n_steps * L * 8);
     if (!at) {
       timing(JPI_KERNEL_PERSISTENT, &pa.ev_start, &pa.ev_stop);
       ENQ(launch_persist(pa, c->n_cu, s));

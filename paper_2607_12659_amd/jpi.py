@@ -13,14 +13,17 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libjpi.so")
+# JPI_LIB selects another build of the same library (the trace build of
+# trace_links.py); the default is the in-tree libjpi.so
+LIB_PATH = os.environ.get("JPI_LIB") or os.path.join(_HERE, "libjpi.so")
 
 JPI_OK, JPI_ERR_ARG, JPI_ERR_SHAPE, JPI_ERR_DTYPE, JPI_ERR_STATE, JPI_ERR_OOM, JPI_ERR_HIP, JPI_ERR_UNSUPPORTED = range(8)
 JPI_F32, JPI_BF16 = 0, 1
 JPI_VARIANT_ADARMS, JPI_VARIANT_ACTION_TIME = 0, 1
 
 EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create", "jpi_destroy", "jpi_set_weight",
-            "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_debug_prefix_vt", "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
+            "jpi_finalize_weights", "jpi_prefix_buffers", "jpi_debug_prefix_vt", "jpi_debug_persist_trace",
+            "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
             "jpi_sync", "jpi_debug_gemm", "jpi_gemm_noalloc", "jpi_gemm_noalloc_scratch_bytes",
             "jpi_gemm_noalloc_last_error", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
             "jpi_sched_run", "jpi_sched_sim_hooks", "jpi_vlm_create", "jpi_vlm_destroy", "jpi_vlm_set_weight",
@@ -115,6 +118,8 @@ _sig = {
     "jpi_finalize_weights": (_i, [_vp, _vp]),
     "jpi_prefix_buffers": (_i, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp)]),
     "jpi_debug_prefix_vt": (_i, [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_i)]),
+    "jpi_debug_persist_trace": (_i, [_vp, _vp, _i64, ctypes.POINTER(_i), ctypes.POINTER(_i),
+                                     ctypes.POINTER(ctypes.c_double)]),
     "jpi_bind_prefix": (_i, [_vp, _vp, _vp, _vp, _i, _i, _vp]),
     "jpi_bind_state": (_i, [_vp, _vp, _i, _vp, _i, _vp]),
     "jpi_denoise": (_i, [_vp, _vp, _i, _vp, _vp]),
@@ -217,6 +222,19 @@ def jpi_prefix_buffers(ctx):
     k, v = _vp(), _vp()
     st = _lib.jpi_prefix_buffers(ctx, ctypes.byref(k), ctypes.byref(v))
     return st, k.value, v.value
+
+
+def jpi_debug_persist_trace(ctx):
+    """(status, stamps [workgroups][slots] uint64 or None, ticks per microsecond)."""
+    import numpy as np
+    nw, ns, tpu = _i(), _i(), ctypes.c_double()
+    st = _lib.jpi_debug_persist_trace(ctx, None, 0, ctypes.byref(nw), ctypes.byref(ns), ctypes.byref(tpu))
+    if st != JPI_OK:
+        return st, None, 0.0
+    out = np.zeros((nw.value, ns.value), dtype=np.uint64)
+    st = _lib.jpi_debug_persist_trace(ctx, out.ctypes.data, out.size, ctypes.byref(nw), ctypes.byref(ns),
+                                      ctypes.byref(tpu))
+    return st, out, tpu.value
 
 
 def jpi_debug_prefix_vt(ctx):
