@@ -23,6 +23,7 @@ in HBM.  Prints one JSON line:
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
        python bench.py --calibrate-copy MIB   (a plain device copy, for counter scaling)
+       python bench.py --workload NAME --calls-only N   (N calls and nothing else: a profiler's target)
 """
 from __future__ import annotations
 
@@ -685,6 +686,9 @@ def main():
     ap.add_argument("--committed-t0", action="store_true",
                     help="committed rows at flow time t = 0 (the variant; the default workloads share t)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
+    ap.add_argument("--calls-only", type=int, default=0, metavar="N",
+                    help="set up the workload, run N denoise calls (after one untimed call), sync and exit "
+                         "without a JSON line: a profiler's target")
     args = ap.parse_args()
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
@@ -736,6 +740,16 @@ def main():
     noise_d = to_device(noise)
     out = torch.empty_like(noise_d)
     torch.cuda.synchronize()
+
+    if args.calls_only:
+        ae.denoise(noise_d, wl.n_steps, out, stream=stream)
+        for _ in range(args.calls_only):
+            ae.denoise(noise_d, wl.n_steps, out, stream=stream)
+        torch.cuda.synchronize()
+        ae.sync(stream)
+        print("bench: %d calls of %s done" % (args.calls_only + 1, wl.name), file=sys.stderr, flush=True)
+        ae.close()
+        return
 
     # first call: modulation tables + graph capture + one replay
     t0 = time.perf_counter()

@@ -280,8 +280,10 @@ jpi_status jpi_debug_prefix_vt(jpi_ctx* ctx, void** vt_out, int* ld_out);
  * the kernel's trace mode, -DJPI_PERSIST_TRACE=1, by
  * paper_2607_12659_amd/trace_links.py; the normal build returns
  * JPI_ERR_UNSUPPORTED).  Sets *n_workgroups (the launch's grid), *n_slots
- * (1 + phases of the call: slot 0 is each workgroup's start, slot 1 + p the
- * end of phase p, 8 phases per layer) and *ticks_per_us of the counter;
+ * (1 + 3 x phases of the call, 8 phases per layer: slot 0 is each
+ * workgroup's start; phase p has slots 1 + 3p + {0: the flags of its
+ * producers were seen, 1: its operands were loaded, 2: its end}) and
+ * *ticks_per_us of the counter;
  * when host_out holds cap >= n_workgroups * n_slots entries it also
  * synchronises the device and copies the stamps, [workgroup][slot].
  * Errors: JPI_ERR_ARG (NULL), JPI_ERR_UNSUPPORTED, JPI_ERR_HIP. */

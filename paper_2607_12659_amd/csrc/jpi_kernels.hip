@@ -10,6 +10,7 @@
 // Every reduction (split-K partial sums, attention chunk combine, row norms)
 // is summed in a fixed order, so results are bitwise reproducible.
 #include <math.h>
+#include <stdlib.h>
 
 #include "jpi_device.h"
 #include "jpi_internal.h"
@@ -272,6 +273,166 @@ __global__ __launch_bounds__(512) void k_gemm_big(GemmLaunch g) {
         epilogue_pair<bf16, EPI>(g.ep, out, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i], acc[a][b + 1][i]);
 }
 
+// ---- bf16 GEMM with a deep load pipeline (M > 64).  Both operand tiles move
+// HBM -> LDS by direct-to-LDS buffer loads (no register staging) into a ring
+// of NS stages, so that NS - 1 K slices are in flight while one is consumed:
+// with one slice in flight a workgroup waits a whole memory round trip per
+// slice.  Waits are explicit vmcnt counts and a bare s_barrier (a
+// __syncthreads() fence would drain every outstanding load each slice).  A
+// direct-to-LDS instruction writes 1 KB of LDS linearly (lane l at 16 l), so
+// the bank swizzle is applied through the global addresses: LDS slot s of
+// tile row r holds K chunk s ^ f(r).  Rows past M (or N) lie outside the
+// buffer range and load as zero. ----------------------------------------------
+template <int BM_, int BN_, int NW_, int BK_>
+struct DmaShape {
+  static constexpr int BM = BM_, BN = BN_, NW = NW_, BK = BK_, NS = 4;
+  static constexpr int NT = 64 * NW;
+  static constexpr int VEC = 8;                       // bf16 per 16-byte chunk
+  static constexpr int CPR = BK / VEC;                // chunks per tile row: 8 (BK 64) or 4 (BK 32)
+  static constexpr int RPI = 64 / CPR;                // tile rows per 1 KB load instruction
+  static constexpr int WGN = NW / 2;                  // wave grid 2 x WGN
+  static constexpr int WM = BM / 2, WN = BN / WGN;
+  static constexpr int TM = WM / 16, TN = WN / 16;
+  static constexpr int A_INS = BM / RPI, W_INS = BN / RPI;
+  static constexpr int INS = (A_INS + W_INS) / NW;    // load instructions per wave per stage
+  static constexpr int STAGE = (BM + BN) * BK;        // bf16 elements per stage
+  static_assert((A_INS + W_INS) % NW == 0, "load instructions split evenly over the waves");
+  static_assert(CPR == 8 || CPR == 4, "swizzle defined for 64- and 32-deep slices");
+  static_assert(TN % 2 == 0, "epilogues pair n-subtiles 2t and 2t+1");
+  // LDS slot of chunk c in row r (an involution: also the chunk held by slot c)
+  static __device__ __forceinline__ int swz(int r, int c) {
+    return CPR == 8 ? (c ^ ((r >> 1) & 7)) : (c ^ ((r >> 2) & 3));
+  }
+};
+
+// s_waitcnt with vmcnt = N and the other counters not waited for
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+typedef __attribute__((address_space(3))) char dma_lds_t;
+typedef __attribute__((address_space(3))) const bf16x8 dma_lds_frag;
+
+// One 1 KB direct-to-LDS load: 16 bytes per lane from base + byte offset
+// `off` (zero past `bytes`) into LDS at dst + 16 * lane.
+__device__ __forceinline__ void dma_load_1k(const void* base, unsigned bytes, unsigned off, dma_lds_t* dst) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000), dst, 16, off, 0, 0, 0);
+}
+
+// Issue slice kt into its ring stage: this wave's share of the 1 KB
+// direct-to-LDS instructions; lane (lr, ls) loads tile row j * RPI + lr, K
+// chunk swz(row, ls), into LDS slot ls of that row.
+template <typename S>
+__device__ __forceinline__ void dma_issue(const GemmLaunch& g, char* ring, int wave, int lr, int ls, int m0, int n0,
+                                          int kbeg, int kt) {
+  const int K = g.K, k0 = kbeg + kt * S::BK;
+  const unsigned a_bytes = (unsigned)((size_t)g.M * K * 2), w_bytes = (unsigned)((size_t)g.N * K * 2);
+  dma_lds_t* st = (dma_lds_t*)ring + (kt % S::NS) * (S::STAGE * 2);
+#pragma unroll
+  for (int i = 0; i < S::INS; ++i) {
+    const int j = wave + S::NW * i;  // instruction index within the stage (uniform)
+    if (j < S::A_INS) {
+      const int r = j * S::RPI + lr;
+      dma_load_1k(g.A, a_bytes, (unsigned)(((size_t)(m0 + r) * K + k0 + S::swz(r, ls) * S::VEC) * 2), st + j * 1024);
+    } else {
+      const int jw = j - S::A_INS, r = jw * S::RPI + lr;
+      dma_load_1k(g.W, w_bytes, (unsigned)(((size_t)(n0 + r) * K + k0 + S::swz(r, ls) * S::VEC) * 2),
+                  st + S::BM * S::BK * 2 + jw * 1024);
+    }
+  }
+}
+
+template <typename S, EpiKind EPI>
+__global__ __launch_bounds__(S::NT) void k_gemm_dma(GemmLaunch g) {
+  typedef dma_lds_t lds_t;
+  typedef dma_lds_frag lds_frag;
+  using MF = Mfma<bf16>;
+  __shared__ __attribute__((aligned(1024))) char ring[S::NS * S::STAGE * 2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / S::WGN, wn = wave % S::WGN;
+  const int m0 = blockIdx.y * S::BM, n0 = blockIdx.x * S::BN;
+  const int M = g.M, N = g.N, K = g.K;
+  const int kper = K / g.splitk, kbeg = blockIdx.z * kper, nkt = kper / S::BK;
+  const int lr = lane / S::CPR, ls = lane % S::CPR;
+  f32x4 acc[S::TM][S::TN];
+#pragma unroll
+  for (int a = 0; a < S::TM; ++a)
+#pragma unroll
+    for (int b = 0; b < S::TN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int fr = lane & 15, fc = lane >> 4;  // fragment row, 16-byte K chunk within a 32-deep step
+
+#pragma unroll
+  for (int s = 0; s < S::NS - 1; ++s)
+    if (s < nkt) dma_issue<S>(g, ring, wave, lr, ls, m0, n0, kbeg, s);
+  for (int kt = 0; kt < nkt; ++kt) {
+    // slice kt has landed once at most min(NS - 2, nkt - 1 - kt) later slices are pending
+    const int later = min(S::NS - 2, nkt - 1 - kt);
+    if (later >= 2) wait_vm<2 * S::INS>();
+    else if (later == 1) wait_vm<S::INS>();
+    else wait_vm<0>();
+    __builtin_amdgcn_s_barrier();  // every wave's part of slice kt; slice kt - 1 fully consumed
+    if (kt + S::NS - 1 < nkt) dma_issue<S>(g, ring, wave, lr, ls, m0, n0, kbeg, kt + S::NS - 1);
+    const lds_t* As = (const lds_t*)ring + (kt % S::NS) * (S::STAGE * 2);
+    const lds_t* Ws = As + S::BM * S::BK * 2;
+#pragma unroll
+    for (int kk = 0; kk < S::BK; kk += MF::KSUB) {
+      const int c = kk / S::VEC + fc;
+      MF::frag af[S::TM], bfr[S::TN];
+#pragma unroll
+      for (int a = 0; a < S::TM; ++a) {
+        const int r = wm * S::WM + a * 16 + fr;
+        af[a] = *(lds_frag*)(As + (r * S::BK + S::swz(r, c) * S::VEC) * 2);
+      }
+#pragma unroll
+      for (int b = 0; b < S::TN; ++b) {
+        const int r = wn * S::WN + b * 16 + fr;
+        bfr[b] = *(lds_frag*)(Ws + (r * S::BK + S::swz(r, c) * S::VEC) * 2);
+      }
+#pragma unroll
+      for (int a = 0; a < S::TM; ++a)
+#pragma unroll
+        for (int b = 0; b < S::TN; ++b) acc[a][b] = MF::run(af[a], bfr[b], acc[a][b]);
+    }
+  }
+
+  const int rbase = m0 + wm * S::WM + (lane >> 4) * 4;
+  const int cbase = n0 + wn * S::WN + fr;
+  float* out = g.ep.out_f32 ? g.ep.out_f32 + (size_t)blockIdx.z * M * N : nullptr;
+#pragma unroll
+  for (int a = 0; a < S::TM; ++a)
+#pragma unroll
+    for (int b = 0; b < S::TN; b += 2)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        epilogue_pair<bf16, EPI>(g.ep, out, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i], acc[a][b + 1][i]);
+}
+
+typedef DmaShape<128, 128, 4, 64> DmaMid;   // one slice: 32 KB; ring 128 KB (a 256 x 256, 8-wave, 32-deep
+                                            // shape fits the same ring; slower at M = 3200 than two
+                                            // register-staged workgroups per unit)
+
+template <typename S>
+static hipError_t launch_dma(const GemmLaunch& g, hipStream_t s) {
+  dim3 grid((g.N + S::BN - 1) / S::BN, (g.M + S::BM - 1) / S::BM, g.splitk);
+  switch (g.epi) {
+    case EPI_STORE_F32: JPI_LAUNCH((k_gemm_dma<S, EPI_STORE_F32>), grid, dim3(S::NT), 0, s, g.ev_start, g.ev_stop, g); break;
+    case EPI_QKV: JPI_LAUNCH((k_gemm_dma<S, EPI_QKV>), grid, dim3(S::NT), 0, s, g.ev_start, g.ev_stop, g); break;
+    case EPI_GEGLU: JPI_LAUNCH((k_gemm_dma<S, EPI_GEGLU>), grid, dim3(S::NT), 0, s, g.ev_start, g.ev_stop, g); break;
+  }
+  return hipGetLastError();
+}
+
+static bool gemm_pipe_enabled() {
+  static const int on = [] {
+    const char* e = getenv("JPI_GEMM_PIPE");
+    return e && e[0] == '0' ? 0 : 1;
+  }();
+  return on != 0;
+}
+
 static hipError_t launch_big(const GemmLaunch& g, hipStream_t s) {
   dim3 grid((g.N + BigShape::BN - 1) / BigShape::BN, (g.M + BigShape::BM - 1) / BigShape::BM, g.splitk);
   switch (g.epi) {
@@ -427,6 +588,14 @@ hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s) {
     // unless that leaves the grid short and the epilogue cannot be split over K
     const int n_cu = g.n_cu > 0 ? g.n_cu : 256;
     auto tiles = [&](int bm, int bn) { return ((g.M + bm - 1) / bm) * ((g.N + bn - 1) / bn) * g.splitk; };
+    // the direct-to-LDS pipeline (one 128 KB ring per compute unit) wins where one
+    // round of 128 x 128 tiles covers the chip and no more (measured: M = 400
+    // GateUp 25.1 -> 19.6 us, Down 16.2 -> 13.4 us); with more tiles the
+    // register-staged kernel's two workgroups per unit win, with fewer the
+    // smaller tiles below
+    if (gemm_pipe_enabled() && g.M <= 512 && tiles(128, 128) >= n_cu && tiles(128, 128) <= n_cu + n_cu / 4 &&
+        (g.K / g.splitk) % DmaMid::BK == 0 && (size_t)g.N * g.K * 2 < (1u << 31))
+      return launch_dma<DmaMid>(g, s);
     if (tiles(256, 256) >= n_cu) return launch_big(g, s);
     if (tiles(128, 128) >= n_cu || g.epi == EPI_STORE_F32) return launch_gemm_t<bf16, 128, 128>(g, s);
     if (tiles(128, 64) >= n_cu) return launch_gemm_t<bf16, 128, 64>(g, s);

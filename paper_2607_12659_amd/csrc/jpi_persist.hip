@@ -181,6 +181,36 @@ __device__ __forceinline__ void load_wtile(lds_t* lds, const bf16* W, int KS, in
   }
 }
 
+// trace build: the first two stamps of the current phase (thread 0)
+__shared__ unsigned long long s_note[2];
+
+// Trace build only.  Slot 0 of trace[workgroup][...] is the workgroup's
+// start; phase ph has slots 1 + 3 ph + {0: its producers seen, 1: its
+// operands loaded, 2: its end}.  A workgroup with no work in a phase records
+// the phase's end time in all three.  s_note holds the first two stamps of
+// the current phase until the phase ends.
+__device__ __forceinline__ void trace_start(const PersistArgs& a, unsigned long long* s_note) {
+  if (JPI_PERSIST_TRACE && a.trace && threadIdx.x == 0) {
+    a.trace[(size_t)blockIdx.x * a.trace_slots] = __builtin_amdgcn_s_memrealtime();
+    s_note[0] = s_note[1] = 0ull;
+  }
+}
+// kind 0: the producers' flags were seen; kind 1: the phase's operands are loaded
+__device__ __forceinline__ void trace_note(unsigned long long* s_note, int kind) {
+  if (JPI_PERSIST_TRACE && threadIdx.x == 0 && s_note[kind] == 0ull) s_note[kind] = __builtin_amdgcn_s_memrealtime();
+}
+__device__ __forceinline__ void trace_end(const PersistArgs& a, unsigned long long* s_note, int ph) {
+  if (JPI_PERSIST_TRACE && a.trace && threadIdx.x == 0 && 3 + 3 * ph < a.trace_slots) {
+    const unsigned long long t = __builtin_amdgcn_s_memrealtime();
+    unsigned long long* row = a.trace + (size_t)blockIdx.x * a.trace_slots + 1 + 3 * ph;
+    const unsigned long long w = s_note[0] ? s_note[0] : t;
+    row[0] = w;
+    row[1] = s_note[1] ? s_note[1] : w;
+    row[2] = t;
+    s_note[0] = s_note[1] = 0ull;
+  }
+}
+
 // Phase completion flags.  After phase ph a workgroup confirms its stores
 // (s_waitcnt vmcnt(0)) and writes ph + 2 into its own 128-byte flag line;
 // the values only grow within a launch.  A workgroup that has work in phase
@@ -249,6 +279,7 @@ __device__ __forceinline__ void wait_producers(const PersistArgs& a, const Deps&
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // s_abort
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
+  trace_note(s_note, 0);
 }
 
 // End of phase ph: every wave's stores are complete, then the flag.
@@ -256,13 +287,6 @@ __device__ __forceinline__ void phase_done(const PersistArgs& a, u32 value) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (threadIdx.x == 0) st4(rsrc(a.flags), blockIdx.x * (FLAG_STRIDE * 4u), value);
-}
-
-// Trace build only: the real-time counter after phase `slot - 1` (slot 0:
-// the workgroup's start) into trace[workgroup][slot].
-__device__ __forceinline__ void trace_mark(const PersistArgs& a, int slot) {
-  if (JPI_PERSIST_TRACE && a.trace && threadIdx.x == 0 && slot < a.trace_slots)
-    a.trace[(size_t)blockIdx.x * a.trace_slots + slot] = __builtin_amdgcn_s_memrealtime();
 }
 
 // ---------------------------------------------------------------------------
@@ -300,6 +324,7 @@ __device__ __forceinline__ void gemm_chunk(rsrc_t ra, int mgroups, int KS, int k
     if (s0 == 0) {  // every wave's part of the tile has landed
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
+      trace_note(s_note, 1);
     }
 #pragma unroll
     for (int c = 0; c < BATCH; ++c) {
@@ -501,6 +526,7 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
       *reinterpret_cast<u32x4*>(&Vt[d * LDV + kc * 8]) = vr[u];
     }
     __syncthreads();
+    trace_note(s_note, 1);
     // S^T = K q^T with the operands swapped, so that a lane holds one query
     // row (fr) and keys jj*16 + 4g + e (g = lane / 16): the softmax of a row
     // needs only the four lanes that share fr, and P stays in registers as
@@ -628,6 +654,7 @@ __device__ __forceinline__ void phase_combine(const PersistArgs& a, char* smem) 
     sl[t] = lsum;
     sacc[t] = acc;
     __syncthreads();
+    trace_note(s_note, 1);
     if (live && g == 0) {
       const int b0 = hf * TPR + q4;
       float mx = -INFINITY;
@@ -782,6 +809,7 @@ __device__ __forceinline__ void phase_rows(const PersistArgs& a, const RowJob& r
     *hp = *hp + g4 * sum;
   }
   __syncthreads();
+  trace_note(s_note, 1);
   float ss = 0.f;
   for (int k = t; k < W; k += PT) ss += hrow[k] * hrow[k];
   const float rs = 1.0f / sqrtf(block_sum_wg(ss, red) / (float)W + a.eps);
@@ -896,8 +924,8 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
       s_x[t] = xreg;
     }
   }
+  trace_start(a, s_note);
   __syncthreads();
-  trace_mark(a, 0);
   lds_t* wt = (lds_t*)s_wt;
   const int last_phase = a.n_steps * L * 8 - 1;
   // ph = -1 is the first step's in-projection; the later ones follow the final
@@ -950,7 +978,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
       inproj_row(a, ti, ti + W, s_hrow, s_bin, s_x, reinterpret_cast<float*>(smem), crow);
     }
     if (ph < last_phase) phase_done(a, (u32)(ph + 2));
-    if (ph >= 0) trace_mark(a, ph + 1);
+    if (ph >= 0) trace_end(a, s_note, ph);
   }
   if (owner && t < A && ia >= 0) a.x[xrow * A + t] = xreg;
 }

@@ -426,8 +426,8 @@ jpi_status jpi_create(const jpi_config* cfg, int device, jpi_ctx** out) {
   ALLOC(c->z, M * F * es);
   ALLOC(c->pflags, (size_t)persist_flag_words() * sizeof(unsigned));
   ALLOC(c->perr, 256);
-  if (persist_trace_build()) {  // room for 64 Euler steps of every layer's 8 phases
-    c->trace_slots = 1 + 64 * c->L * 8;
+  if (persist_trace_build()) {  // room for 64 Euler steps of every layer's 8 phases, 3 stamps each
+    c->trace_slots = 1 + 3 * 64 * c->L * 8;
     c->trace_grid = persist_max_grid();
     ALLOC(c->ptrace, (size_t)c->trace_grid * c->trace_slots * sizeof(unsigned long long));
   }
@@ -1069,7 +1069,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     pa.err = c->perr;
     pa.trace = c->ptrace;
     pa.trace_slots = c->trace_slots;
-    c->trace_used = std::min(c->trace_slots, 1 + n_steps * L * 8);
+    c->trace_used = std::min(c->trace_slots, 1 + 3 * n_steps * L * 8);
     if (!at) {
       timing(JPI_KERNEL_PERSISTENT, &pa.ev_start, &pa.ev_stop);
       ENQ(launch_persist(pa, c->n_cu, s));

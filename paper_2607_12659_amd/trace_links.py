@@ -10,8 +10,10 @@ over all (step, layer) pairs of
     link(p) = last workgroup to finish phase p  -  last to finish phase p - 1
 
 (the time from the last producer of the previous phase finishing to the last
-workgroup of this phase finishing), plus their sum per layer and the whole
-call.  The trace build is for measurement only; the stamps cost one store per
+workgroup of this phase finishing), split for the workgroup that finished
+last into waiting for its producers' flags, loading its operands, and the
+rest (compute, stores and their confirmation), plus the sum per layer and
+the whole call.  The trace build is for measurement only; the stamps cost one store per
 workgroup and phase.
 
     python -m paper_2607_12659_amd.trace_links --build
@@ -48,15 +50,25 @@ def build_trace_lib() -> str:
 
 
 def analyse(stamps, ticks_per_us, n_steps, n_layers):
-    """Per-link durations (us) from the stamps [workgroups][1 + phases]."""
+    """Per-link durations (us) from the stamps [workgroups][1 + 3 phases].
+
+    Returns [steps][layers][8][4]: the link (last workgroup to finish this
+    phase minus last to finish the previous one) and, for the workgroup that
+    finished last, its split into waiting for the producers' flags, loading
+    the operands, and the rest (compute, stores, store confirmation)."""
     import numpy as np
-    end = stamps[:, 1:].astype(np.float64).max(axis=0)           # last workgroup to finish each phase
-    start = float(stamps[:, 0].astype(np.float64).min())
-    prev = np.concatenate([[start], end[:-1]])
-    link = (end - prev) / ticks_per_us
     n = n_steps * n_layers * 8
-    link = link[:n].reshape(n_steps, n_layers, 8)
-    return link
+    st = stamps[:, 1:1 + 3 * n].astype(np.float64).reshape(stamps.shape[0], n, 3)
+    end = st[:, :, 2]
+    crit = end.argmax(axis=0)                                      # workgroup that finished last
+    t_end = end.max(axis=0)
+    start = float(stamps[:, 0].astype(np.float64).min())
+    prev = np.concatenate([[start], t_end[:-1]])
+    seen = st[crit, np.arange(n), 0]
+    loaded = st[crit, np.arange(n), 1]
+    out = np.stack([t_end - prev, np.maximum(seen - prev, 0.0), loaded - np.maximum(seen, prev),
+                    t_end - loaded], axis=1) / ticks_per_us
+    return out.reshape(n_steps, n_layers, 8, 4)
 
 
 def run(workload: str, calls: int):
@@ -84,12 +96,14 @@ def run(workload: str, calls: int):
         if i > 0:  # the first call builds tables and captures the graph
             links.append(analyse(stamps, tpu, wl.n_steps, wl.dims.n_layers))
     ae.close()
-    link = np.stack(links)                                          # [calls][steps][layers][8]
-    med = np.median(link.reshape(-1, 8), axis=0)
-    per_layer = np.median(link.sum(axis=3).reshape(-1))
-    call_us = float(np.median(link.sum(axis=(1, 2, 3))))
-    return {"workload": workload, "calls": calls, "link_us_median": {PHASES[i]: round(float(med[i]), 2)
-                                                                     for i in range(8)},
+    link = np.stack(links)                                          # [calls][steps][layers][8][4]
+    med = np.median(link.reshape(-1, 8, 4), axis=0)
+    per_layer = np.median(link[..., 0].sum(axis=3).reshape(-1))
+    call_us = float(np.median(link[..., 0].sum(axis=(1, 2, 3))))
+    return {"workload": workload, "calls": calls,
+            "links": {PHASES[i]: {"link": round(float(med[i, 0]), 2), "wait": round(float(med[i, 1]), 2),
+                                  "load": round(float(med[i, 2]), 2), "rest": round(float(med[i, 3]), 2)}
+                      for i in range(8)},
             "layer_us_median": round(float(per_layer), 2), "call_us_median": round(call_us, 1)}
 
 
@@ -113,12 +127,12 @@ def main():
         sys.exit(subprocess.call(cmd, env=env, cwd=ROOT))
     sys.path.insert(0, ROOT)
     res = run(args.workload, args.calls)
-    print("| link | median us |")
-    print("|---|---|")
-    for k, v in res["link_us_median"].items():
-        print("| %s | %.2f |" % (k, v))
-    print("| one layer (sum) | %.2f |" % res["layer_us_median"])
-    print("| whole call | %.1f |" % res["call_us_median"])
+    print("| link | median us | critical workgroup: wait for flags | load operands | compute + stores |")
+    print("|---|---|---|---|---|")
+    for k, v in res["links"].items():
+        print("| %s | %.2f | %.2f | %.2f | %.2f |" % (k, v["link"], v["wait"], v["load"], v["rest"]))
+    print("| one layer (sum) | %.2f | | | |" % res["layer_us_median"])
+    print("| whole call | %.1f | | | |" % res["call_us_median"])
     if args.json:
         with open(args.json, "w") as f:
             json.dump(res, f, indent=1)
