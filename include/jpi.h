@@ -218,7 +218,18 @@ jpi_status jpi_set_committed_t0(jpi_ctx* ctx, int enable);
  * call per (batch, prefix, n_steps, n_fixed, n_corr) builds the
  * modulation tables for the N step times and captures the N-step loop into a
  * HIP graph; later calls replay it.  Errors: JPI_ERR_STATE (weights not
- * finalized or no prefix bound), JPI_ERR_ARG (NULL, n_steps < 1). */
+ * finalized or no prefix bound), JPI_ERR_ARG (NULL, n_steps < 1).
+ *
+ * Co-residency: on the single-launch path (bf16, batch * (n_corr + H) <= 64)
+ * the whole loop is one kernel of one workgroup per compute unit whose
+ * workgroups wait for each other through memory.  That needs every
+ * workgroup resident at once: do not let other device work (another stream,
+ * another context or process on the same GPU) run concurrently with it.  If
+ * some workgroups cannot start, the others wait a bounded number of polls,
+ * then stop; the launch still terminates, the actions are invalid, and the
+ * next jpi_sync returns JPI_ERR_HIP.  A caller that reads actions_dev
+ * therefore checks the status of jpi_sync (not only of a stream
+ * synchronisation) before using them. */
 jpi_status jpi_denoise(jpi_ctx* ctx, const float* noise_dev, int n_steps, float* actions_dev, void* stream);
 
 /* Synchronise `stream` and report asynchronous HIP errors as JPI_ERR_HIP,

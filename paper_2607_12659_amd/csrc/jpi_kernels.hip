@@ -413,6 +413,7 @@ __global__ __launch_bounds__(S::NT) void k_gemm_dma(GemmLaunch g) {
 typedef DmaShape<128, 128, 4, 64> DmaMid;   // one slice: 32 KB; ring 128 KB (a 256 x 256, 8-wave, 32-deep
                                             // shape fits the same ring; slower at M = 3200 than two
                                             // register-staged workgroups per unit)
+typedef DmaShape<64, 64, 4, 64> DmaSmall;   // one slice: 16 KB; ring 64 KB (two workgroups per unit)
 
 template <typename S>
 static hipError_t launch_dma(const GemmLaunch& g, hipStream_t s) {
@@ -596,6 +597,11 @@ hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s) {
     if (gemm_pipe_enabled() && g.M <= 512 && tiles(128, 128) >= n_cu && tiles(128, 128) <= n_cu + n_cu / 4 &&
         (g.K / g.splitk) % DmaMid::BK == 0 && (size_t)g.N * g.K * 2 < (1u << 31))
       return launch_dma<DmaMid>(g, s);
+    // fewer 128 x 128 tiles than units and no K split (QKV at M = 400: 80 tiles): 64 x 64 tiles on the
+    // pipelined kernel, two workgroups per unit (measured 20.0 -> 12.7 us; on split-K shapes no gain)
+    if (gemm_pipe_enabled() && g.M <= 512 && tiles(128, 128) < n_cu && g.splitk == 1 && g.K % DmaSmall::BK == 0 &&
+        (size_t)g.N * g.K * 2 < (1u << 31))
+      return launch_dma<DmaSmall>(g, s);
     if (tiles(256, 256) >= n_cu) return launch_big(g, s);
     if (tiles(128, 128) >= n_cu || g.epi == EPI_STORE_F32) return launch_gemm_t<bf16, 128, 128>(g, s);
     if (tiles(128, 64) >= n_cu) return launch_gemm_t<bf16, 128, 64>(g, s);
