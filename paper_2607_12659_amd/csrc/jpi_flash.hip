@@ -4,21 +4,25 @@
 // the layer followed by the action tokens' own (Appendix, action expert).
 // All query heads share the single KV head, so one rollout's nH x H query rows
 // form one [nH*H][Dh] matrix (row r = head * H + i) against one key sequence.
-// A workgroup takes 128 of those rows (8 waves x 16) and a range of 64-key
-// blocks, and streams each block's K and V^T once through double-buffered LDS
-// with a running (max, sum) per row (online softmax).  With one key range the
-// workgroup writes the normalised output; with several it writes a bf16
-// partial normalised by its own sum plus (max, sum), merged by k_flash_merge.
+// A workgroup (eight waves, two per SIMD) takes 128 of those rows, 16 per
+// wave, and a range of 32-key blocks.  The blocks stream through a
+// four-stage LDS ring by direct-to-LDS buffer loads, up to three blocks ahead
+// of the one being multiplied, so the loads of later blocks overlap the
+// products of this one.  A running (max, sum) per row gives the online
+// softmax.
+// With one key range the workgroup writes the normalised output; with several
+// it writes a bf16 partial normalised by its own sum plus (max, sum), merged
+// by k_flash_merge.
 //
 // Products use v_mfma_f32_16x16x32_bf16 with the operands swapped:
 // S^T = K q^T puts one query row in each lane (lane % 16) and four keys of a
 // 16-key tile in its four result elements; O^T = V^T P^T then takes P^T
 // straight from those registers.  The K rows of the two 16-key tiles of a
-// 32-key group are interleaved (tile jj, A row 4g + e <-> key 8g + 4jj + e)
-// so that a lane's eight probabilities are eight consecutive keys, which
-// makes each V^T operand one 16-byte piece of a V^T row.
+// block are interleaved (tile jj, A row 4g + e <-> key 8g + 4jj + e) so that
+// a lane's eight probabilities are eight consecutive keys, which makes each
+// V^T operand one 16-byte piece of a V^T row.
 //
-// Key order: the action keys come first (blocks of 64, masked past H), then
+// Key order: the action keys come first (blocks of 32, masked past H), then
 // the prefix (masked past prefix_len[b]).  The softmax does not depend on the
 // order.  Masked keys get probability 0 and their V entries are zeroed, so
 // stale or non-finite memory in unused slots never reaches the output.
@@ -35,17 +39,25 @@ typedef u32 u32x2 __attribute__((ext_vector_type(2)));
 
 template <int DH>
 struct Flash {
-  static constexpr int NW = 8;             // waves per workgroup (two per SIMD)
-  static constexpr int KB = 64;            // keys per block
-  static constexpr int QT = 16 * NW;       // query rows per workgroup (16 per wave)
-  static constexpr int NST = DH / 32;      // k steps of S^T over the head dim
-  static constexpr int NT = DH / 16;       // 16-wide output tiles over the head dim
-  static constexpr int KFR = 4 * NST;      // 1 KB K fragments per block (4 key tiles)
-  static constexpr int VFR = 2 * NT;       // 1 KB V^T fragments per block (2 key groups)
-  static constexpr int KLD = KFR / NW;     // K fragments loaded per wave
-  static constexpr int VLD = VFR / NW;
+  static constexpr int NW = 8;              // waves per workgroup (two per SIMD)
+  static constexpr int RT = 1;              // 16-row query tiles per wave
+  static constexpr int KB = 32;             // keys per block
+  static constexpr int NS = 4;              // ring stages: three blocks in flight while one is multiplied
+  static constexpr int QT = 16 * RT * NW;   // query rows per workgroup
+  static constexpr int NST = DH / 32;       // k steps of S^T over the head dim
+  static constexpr int NT = DH / 16;        // 16-wide output tiles over the head dim
+  static constexpr int KFR = 2 * NST;       // 1 KB K fragments per block (two key tiles)
+  static constexpr int VFR = NT;            // 1 KB V^T fragments per block
+  static constexpr int LDW = (KFR + VFR) / NW;  // direct-to-LDS loads per wave per block
   static constexpr int STAGE = (KFR + VFR) * 1024;
-  static_assert(KLD >= 1 && KFR % NW == 0 && VLD >= 1 && VFR % NW == 0, "fragments per wave");
+  static_assert((KFR + VFR) % NW == 0 && LDW >= 1, "fragments split evenly over the waves");
+  // fragment w + NW * u is a K fragment iff is_k(w, u); with KFR a multiple of
+  // NW that depends on u alone, so every wave's load sequence is known when
+  // compiling (which keeps the compiler's count of outstanding loads exact)
+  static __device__ __forceinline__ bool is_k(int w, int u) {
+    return KFR % NW == 0 ? u < KFR / NW : w + NW * u < KFR;
+  }
+  static_assert(2 * LDW < 64, "vmcnt range");
 };
 
 constexpr int FLASH_MAX_SPLITS = 16;
@@ -56,6 +68,12 @@ __device__ __forceinline__ u32x4 mask8(u32x4 v, int n_ok) {
 #pragma unroll
   for (int q = 0; q < 4; ++q) v[q] &= (2 * q < n_ok ? 0x0000ffffu : 0u) | (2 * q + 1 < n_ok ? 0xffff0000u : 0u);
   return v;
+}
+
+// s_waitcnt: vmcnt = N, lgkmcnt = 0 when L, other counters not waited for
+template <int N, bool L>
+__device__ __forceinline__ void flash_wait() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | ((L ? 0 : 15) << 8));
 }
 
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
@@ -72,65 +90,43 @@ __device__ __forceinline__ rsrc_t rsrc(const void* base, int64_t bytes) {
 // it read as zero.
 struct FlashSrc {
   rsrc_t k_act, v_act, k_pre, v_pre;
-  int nbs;  // action blocks (they come first)
+  int nbs, H, pl;  // action blocks (they come first), action keys, prefix keys
 };
 
-// block jb: first key and number of valid keys of its source
-__device__ __forceinline__ void flash_block(const FlashSrc& src, int H, int pl, int jb, bool& act, int& key0,
-                                            int& n_ok) {
-  act = jb < src.nbs;
-  key0 = (act ? jb : jb - src.nbs) * 64;
-  n_ok = act ? H : pl;
-}
-
-// Direct-to-LDS loads of one block into one LDS stage.  Wave w loads
-// fragments w, w + NW, ...  K fragment f = kt * NST + st (kt = 2 * group +
-// tile): lane row 4g' + e of the A operand is key 32 * group + 8g' +
-// 4 * tile + e, k values st * 32 + 8g .. + 8 (g = lane / 16, g' and e from
-// lane % 16).  V^T fragment f = group * NT + nt: dim nt * 16 + lane % 16,
-// keys 32 * group + 8g .. + 8.  The per-lane part of each address (koff,
-// voff) is fixed for the launch; the per-fragment part (sk, sv) is uniform
-// and, with the block's first key, goes in the scalar offset.
+// Direct-to-LDS loads of block jb into one ring stage.  Wave w loads
+// fragments w, w + NW, ...: the first KFR are K fragments f = kt * NST + st
+// (lane row 4g' + e of the A operand is key 8g' + 4kt + e, k values
+// st * 32 + 8g .. + 8; g = lane / 16, g' and e from lane % 16), the next VFR
+// are V^T fragments nt (dim nt * 16 + lane % 16, keys 8g .. + 8).  The
+// per-lane part of each address (koff, vaoff, vpoff) is fixed for the
+// launch; the per-fragment part and the block's first key go in the scalar
+// offset.  Returns the block's valid key count (>= 1).
 template <int DH>
-struct FlashDma {
-  u32 sk[Flash<DH>::KLD], sva[Flash<DH>::VLD], svp[Flash<DH>::VLD];
-};
-
-template <int DH>
-__device__ __forceinline__ FlashDma<DH> flash_dma_offsets(int vst_ld, int vpt_ld) {
+__device__ __forceinline__ int flash_issue(lds_t* stage, const FlashSrc& src, int jb, u32 koff, u32 vaoff, u32 vpoff,
+                                           int vst_ld, int vpt_ld) {
   using FS = Flash<DH>;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  FlashDma<DH> d;
-#pragma unroll
-  for (int u = 0; u < FS::KLD; ++u) {
-    const int fi = w + FS::NW * u, kt = fi / FS::NST, st = fi - kt * FS::NST;
-    d.sk[u] = (u32)(((32 * (kt >> 1) + 4 * (kt & 1)) * DH + st * 32) * 2);
-  }
-#pragma unroll
-  for (int u = 0; u < FS::VLD; ++u) {
-    const int fi = w + FS::NW * u, grp = fi / FS::NT, nt = fi - grp * FS::NT;
-    d.sva[u] = (u32)((nt * 16 * vst_ld + 32 * grp) * 2);
-    d.svp[u] = (u32)((nt * 16 * vpt_ld + 32 * grp) * 2);
-  }
-  return d;
-}
-
-template <int DH>
-__device__ __forceinline__ void flash_dma(lds_t* stage, const FlashSrc& src, const FlashDma<DH>& d, u32 koff,
-                                          u32 vaoff, u32 vpoff, bool act, int key0) {
-  using FS = Flash<DH>;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool act = jb < src.nbs;
+  const int key0 = (act ? jb : jb - src.nbs) * FS::KB;
   const rsrc_t rk = act ? src.k_act : src.k_pre;
   const rsrc_t rv = act ? src.v_act : src.v_pre;
   const u32 voff = act ? vaoff : vpoff;
-  const u32 kb = (u32)(key0 * DH * 2), vb = (u32)(key0 * 2);
+  const int vld = act ? vst_ld : vpt_ld;
 #pragma unroll
-  for (int u = 0; u < FS::KLD; ++u)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, stage + (w + FS::NW * u) * 1024, 16, koff, kb + d.sk[u], 0, 0);
-#pragma unroll
-  for (int u = 0; u < FS::VLD; ++u)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, stage + (FS::KFR + w + FS::NW * u) * 1024, 16, voff,
-                                             vb + (act ? d.sva[u] : d.svp[u]), 0, 0);
+  for (int u = 0; u < FS::LDW; ++u) {
+    const int fi = w + FS::NW * u;
+    if (FS::is_k(w, u)) {
+      const int kt = fi / FS::NST, st = fi - kt * FS::NST;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, stage + fi * 1024, 16, koff,
+                                               (u32)(((key0 + 4 * kt) * DH + st * 32) * 2), 0, 0);
+    } else {
+      const int nt = fi - FS::KFR;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, stage + fi * 1024, 16, voff, (u32)((nt * 16 * vld + key0) * 2),
+                                               0, 0);
+    }
+  }
+  const int n = (act ? src.H : src.pl) - key0;
+  return n < FS::KB ? n : FS::KB;
 }
 
 // After this thread's direct-to-LDS loads of a block have landed: zero the
@@ -142,118 +138,118 @@ __device__ __forceinline__ void flash_fix(char* stage, int n_valid) {
   using FS = Flash<DH>;
   if (n_valid >= FS::KB) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n_ok = n_valid - 8 * (lane >> 4);
+  if (n_ok >= 8) return;
 #pragma unroll
-  for (int u = 0; u < FS::VLD; ++u) {
-    const int fi = w + FS::NW * u, grp = fi / FS::NT;
-    const int n_ok = n_valid - (32 * grp + 8 * (lane >> 4));
-    if (n_ok < 8) {
-      u32x4* p = reinterpret_cast<u32x4*>(stage + ((FS::KFR + fi) * 64 + lane) * 16);
+  for (int u = 0; u < FS::LDW; ++u) {
+    const int fi = w + FS::NW * u;
+    if (!FS::is_k(w, u)) {
+      u32x4* p = reinterpret_cast<u32x4*>(stage + (fi * 64 + lane) * 16);
       *p = mask8(*p, n_ok);
     }
   }
 }
 
-// One 64-key block for this wave's 16 query rows.
-// Softmax in the log2 domain against a fixed per-row reference m_ref: the
-// maximum of the row's first block.  A later block whose maximum exceeds the
-// reference by more than FLASH_LIMIT (probabilities up to 2^FLASH_LIMIT) asks
-// for a restart of the key range with that maximum as the new reference
-// (the return value); the output is never rescaled.  The reference is the
-// same in the four lanes of a row.  Keys n_valid .. 63 of the block are masked.
+// Maximum over the four lanes that hold one query row (lanes r, r + 16,
+// r + 32, r + 48): two lane-swap instructions, no LDS round trip.  (The
+// swapped pair is copied into scalars before the bit casts: a bit cast of an
+// element of the returned vector reads element 0 for both.)
+__device__ __forceinline__ float row4_max(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(u32, v), __builtin_bit_cast(u32, v), false, false);
+  const u32 a0 = a[0], a1 = a[1];
+  v = fmaxf(__builtin_bit_cast(float, a0), __builtin_bit_cast(float, a1));
+  const auto b = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(u32, v), __builtin_bit_cast(u32, v), false, false);
+  const u32 b0 = b[0], b1 = b[1];
+  return fmaxf(__builtin_bit_cast(float, b0), __builtin_bit_cast(float, b1));
+}
+
+// One 32-key block for this wave's 16-row query tiles.
+// Softmax in the log2 domain against a per-row reference m_ref: the maximum
+// of the row's first block.  A later block whose maximum exceeds the
+// reference by more than FLASH_LIMIT (probabilities up to 2^FLASH_LIMIT)
+// moves the reference up to that maximum and rescales the row's running
+// output and sum by 2^(old - new); otherwise the reference stays, so rows
+// whose scores stay within that headroom are never rescaled.  The reference
+// is the same in the four lanes of a row.  Keys n_valid .. 31 of the block
+// are masked.
 template <int DH>
-__device__ __forceinline__ bool flash_compute(const char* cur, int n_valid, const bf16x8 (&qf)[Flash<DH>::NST],
-                                              f32x4 (&o)[Flash<DH>::NT], float& m_ref, float& l_run, float qscale) {
+__device__ __forceinline__ void flash_compute(const char* cur, int n_valid,
+                                              const bf16x8 (&qf)[Flash<DH>::RT][Flash<DH>::NST],
+                                              f32x4 (&o)[Flash<DH>::RT][Flash<DH>::NT], float (&m_ref)[Flash<DH>::RT],
+                                              float (&l_run)[Flash<DH>::RT], float qscale) {
   using FS = Flash<DH>;
   using MF = Mfma<bf16>;
-  constexpr int NST = FS::NST, NT = FS::NT;
+  constexpr int NST = FS::NST, NT = FS::NT, RT = FS::RT;
   const int lane = threadIdx.x & 63, g = lane >> 4;
-  f32x4 sc[4];
+  // S^T = K q^T: all K fragments of the block are read from LDS first, then multiplied
+  MF::frag kf[NST][2];
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt) sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // S^T = K q^T: K fragments of k step st + 1 are read from LDS while step st multiplies
-  MF::frag kf[2][4];
+  for (int st = 0; st < NST; ++st)
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt) kf[0][kt] = *reinterpret_cast<const MF::frag*>(cur + (kt * NST * 64 + lane) * 16);
+    for (int kt = 0; kt < 2; ++kt) kf[st][kt] = *reinterpret_cast<const MF::frag*>(cur + ((kt * NST + st) * 64 + lane) * 16);
+  f32x4 sc[RT][2];
 #pragma unroll
-  for (int st = 0; st < NST; ++st) {
-    if (st + 1 < NST) {
+  for (int rt = 0; rt < RT; ++rt) sc[rt][0] = sc[rt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-        kf[(st + 1) & 1][kt] = *reinterpret_cast<const MF::frag*>(cur + ((kt * NST + st + 1) * 64 + lane) * 16);
-    }
+  for (int st = 0; st < NST; ++st)
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt) sc[kt] = MF::run(kf[st & 1][kt], qf[st], sc[kt]);
-  }
-  // instruction order: the next step's 4 LDS reads, then this step's 4 products
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-  for (int st = 0; st < NST; ++st) {
-    if (st + 1 < NST) __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-  }
+      for (int rt = 0; rt < RT; ++rt) sc[rt][kt] = MF::run(kf[st][kt], qf[rt][st], sc[rt][kt]);
+  // the V^T fragments are read while the softmax runs
+  MF::frag vf[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) vf[nt] = *reinterpret_cast<const MF::frag*>(cur + ((FS::KFR + nt) * 64 + lane) * 16);
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * NST, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, 2 * NST * RT, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, NT, 0);
 
-  float m = -INFINITY;
+  if (n_valid < FS::KB) {
+    asm volatile("" ::: "memory");  // a real branch: full blocks skip the masking
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt)
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sc[rt][kt][e] = 8 * g + 4 * kt + e < n_valid ? sc[rt][kt][e] : -INFINITY;
+  }
+  MF::frag pb[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) m = fmaxf(m, sc[rt][kt][e]);
+    const float mx = row4_max(m) * qscale;  // finite: the block holds a valid key
+    const bool over = mx > m_ref[rt] + FLASH_LIMIT;  // always on the row's first block (m_ref = -inf)
+    if (__any(over)) {
+      // 2^(-inf) = 0 on the first block, where the output and sum are still zero
+      const float f = over ? __builtin_amdgcn_exp2f(m_ref[rt] - mx) : 1.f;
+      l_run[rt] *= f;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) o[rt][nt] *= f;
+      m_ref[rt] = over ? mx : m_ref[rt];
+    }
+    // P^T as the B operand: slot j of the lane's eight <-> key 8g + j.  The
+    // row sum adds the same bf16-rounded probabilities that weight V, so a
+    // row dominated by one key returns that key's value row exactly.
+    float sum = 0.f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      if (n_valid < FS::KB) {
-        const int key = 32 * (kt >> 1) + 8 * g + 4 * (kt & 1) + e;
-        sc[kt][e] = key < n_valid ? sc[kt][e] : -INFINITY;
-      }
-      m = fmaxf(m, sc[kt][e]);
-    }
-  m = fmaxf(m, __shfl_xor(m, 16, 64));
-  m = fmaxf(m, __shfl_xor(m, 32, 64));
-  const float mx = m * qscale;  // finite: the block holds a valid key
-  const bool first = m_ref == -INFINITY, over = mx > m_ref + FLASH_LIMIT;
-  const bool restart = over && !first;
-  m_ref = over ? mx : m_ref;
-
-#pragma unroll
-  for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) sc[kt][e] = __builtin_amdgcn_exp2f(fmaf(sc[kt][e], qscale, -m_ref));
-  // P^T as the B operand: slot 8g + j of key group grp <-> key 32 grp + 8g + j.
-  // The row sum adds the same bf16-rounded probabilities that weight V, so a
-  // row dominated by one key returns that key's value row exactly.
-  MF::frag pb[2];
-  float sum = 0.f;
-#pragma unroll
-  for (int grp = 0; grp < 2; ++grp)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const bf16 lo = static_cast<bf16>(sc[2 * grp][e]), hi = static_cast<bf16>(sc[2 * grp + 1][e]);
-      pb[grp][e] = lo;
-      pb[grp][4 + e] = hi;
+      const bf16 lo = static_cast<bf16>(__builtin_amdgcn_exp2f(fmaf(sc[rt][0][e], qscale, -m_ref[rt])));
+      const bf16 hi = static_cast<bf16>(__builtin_amdgcn_exp2f(fmaf(sc[rt][1][e], qscale, -m_ref[rt])));
+      pb[rt][e] = lo;
+      pb[rt][4 + e] = hi;
       sum += static_cast<float>(lo) + static_cast<float>(hi);
     }
-  l_run += sum;
-  // O^T += V^T P^T: V^T fragments read four at a time, one group ahead of the products
-  constexpr int NVG = 2 * NT / 4;
-  MF::frag vf[2][4];
-#pragma unroll
-  for (int v = 0; v < 4; ++v) vf[0][v] = *reinterpret_cast<const MF::frag*>(cur + ((FS::KFR + v) * 64 + lane) * 16);
-#pragma unroll
-  for (int vg = 0; vg < NVG; ++vg) {
-    if (vg + 1 < NVG) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        vf[(vg + 1) & 1][v] = *reinterpret_cast<const MF::frag*>(cur + ((FS::KFR + 4 * (vg + 1) + v) * 64 + lane) * 16);
-    }
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int fi = 4 * vg + v, grp = fi / NT, nt = fi - grp * NT;
-      o[nt] = MF::run(vf[vg & 1][v], pb[grp], o[nt]);
-    }
+    l_run[rt] += sum;
   }
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+  // O^T += V^T P^T
 #pragma unroll
-  for (int vg = 0; vg < NVG; ++vg) {
-    if (vg + 1 < NVG) __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
-  }
-  return __any(restart);
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) o[rt][nt] = MF::run(vf[nt], pb[rt], o[rt][nt]);
 }
 
 // Work items (rollout, 128-row query tile, key range) in that order, T of
@@ -264,9 +260,11 @@ template <int DH>
 __global__ __launch_bounds__(512) void k_flash(AttnLaunch a, int S, int nqt, void* part, float2* ml) {
   using FS = Flash<DH>;
   using MF = Mfma<bf16>;
-  constexpr int NST = FS::NST, NT = FS::NT, KB = FS::KB;
-  __shared__ __attribute__((aligned(16))) char lds[2 * FS::STAGE];
-  __shared__ int s_restart;
+  constexpr int NST = FS::NST, NT = FS::NT, RT = FS::RT, NS = FS::NS, LDW = FS::LDW;
+  // one LDS array: the compiler then does not make the ring's LDS reads wait
+  // for every outstanding direct-to-LDS load
+  __shared__ __attribute__((aligned(1024))) char lds[NS * FS::STAGE];
+  static_assert(FS::NW * 64 == 512, "launch bounds");
 
   const int item = (int)(blockIdx.x % 8) * (int)(gridDim.x / 8) + (int)(blockIdx.x / 8);
   if (item >= a.B * nqt * S) return;
@@ -276,16 +274,21 @@ __global__ __launch_bounds__(512) void k_flash(AttnLaunch a, int S, int nqt, voi
   const int g = lane >> 4, fr = lane & 15;
   const int pl = a.prefix_len[b];
   FlashSrc src;
-  src.nbs = (H + KB - 1) / KB;
-  const int nb = src.nbs + (pl + KB - 1) / KB;
+  src.nbs = (H + FS::KB - 1) / FS::KB;
+  src.H = H;
+  src.pl = pl;
+  const int nb = src.nbs + (pl + FS::KB - 1) / FS::KB;
   const int jb0 = (int)((int64_t)split * nb / S), jb1 = (int)((int64_t)(split + 1) * nb / S);
-  const int row0 = qt * FS::QT + w * 16;  // this wave's first query row
+  const int nblk = jb1 - jb0;
+  const int row0 = qt * FS::QT + w * 16 * RT;  // this wave's first query row
 
   // each split writes its (max, sum) even when it has no keys
-  if (jb0 == jb1) {
+  if (nblk == 0) {
     if (S > 1) {
-      const int r = qt * FS::QT + threadIdx.x;
-      if (threadIdx.x < FS::QT && r < R) ml[((size_t)split * a.B + b) * R + r] = float2{-INFINITY, 0.f};
+      for (int t = threadIdx.x; t < FS::QT; t += FS::NW * 64) {
+        const int r = qt * FS::QT + t;
+        if (r < R) ml[((size_t)split * a.B + b) * R + r] = float2{-INFINITY, 0.f};
+      }
     }
     return;
   }
@@ -298,105 +301,107 @@ __global__ __launch_bounds__(512) void k_flash(AttnLaunch a, int S, int nqt, voi
   const int vst_ld = (int)a.vst_ld, vpt_ld = (int)a.vpt_dstride;
   const u32 koff = (u32)(((8 * (fr >> 2) + (fr & 3)) * DH + 8 * g) * 2);
   const u32 vaoff = (u32)((fr * vst_ld + 8 * g) * 2), vpoff = (u32)((fr * vpt_ld + 8 * g) * 2);
-  const FlashDma<DH> dofs = flash_dma_offsets<DH>(vst_ld, vpt_ld);
-  if (threadIdx.x == 0) s_restart = 0;
 
-  lds_t* lds3 = (lds_t*)lds;
-  bool act;
-  int key0, n_ok;
-  flash_block(src, H, pl, jb0, act, key0, n_ok);
-  flash_dma<DH>(lds3, src, dofs, koff, vaoff, vpoff, act, key0);
-
-  // query fragments (B operand of S^T): lane holds row fr, dims st*32 + 8g .. + 8
-  MF::frag qf[NST];
+  // query fragments (B operand of S^T): lane holds row fr of tile rt, dims st*32 + 8g .. + 8
+  MF::frag qf[RT][NST];
   const bf16* qb = reinterpret_cast<const bf16*>(a.q) + (size_t)b * R * DH;
-  {
-    const int r = row0 + fr;
 #pragma unroll
-    for (int st = 0; st < NST; ++st) qf[st] = r < R ? MF::load(qb + (size_t)r * DH + st * 32 + 8 * g) : MF::frag{};
+  for (int rt = 0; rt < RT; ++rt) {
+    const int r = row0 + 16 * rt + fr;
+#pragma unroll
+    for (int st = 0; st < NST; ++st) qf[rt][st] = r < R ? MF::load(qb + (size_t)r * DH + st * 32 + 8 * g) : MF::frag{};
   }
   const bool active = row0 < R;  // wave has query rows (uniform per wave)
 
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  flash_fix<DH>(lds, n_ok - key0);
-  __syncthreads();
+  lds_t* ring = (lds_t*)lds;
+  // valid keys of the blocks in the ring, by stage.  The first NS - 1 blocks
+  // are issued whatever the range's length (a block past the range reads
+  // zeros or other keys into a stage that is never multiplied), so that the
+  // count of loads issued after the query fragments is fixed: waiting until
+  // at most that many are pending means the fragments have landed, without
+  // draining the ring.
+  int nval[NS];
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    nval[s] = flash_issue<DH>(ring + s * FS::STAGE, src, jb0 + s, koff, vaoff, vpoff, vst_ld, vpt_ld);
+  flash_wait<(NS - 1) * LDW, false>();
 
   // log2-domain scores: s * log2(e) / sqrt(Dh)
   const float qscale = 1.4426950408889634f / sqrtf((float)DH);
-  f32x4 o[NT];
+  f32x4 o[RT][NT];
+  float m_ref[RT], l_run[RT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_ref = -INFINITY, l_run = 0.f;
+  for (int rt = 0; rt < RT; ++rt) {
+    m_ref[rt] = -INFINITY;
+    l_run[rt] = 0.f;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) o[rt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
 
-  for (int jb = jb0;;) {
-    const char* cur = lds + ((jb - jb0) & 1) * FS::STAGE;
-    char* nxt = lds + ((jb - jb0 + 1) & 1) * FS::STAGE;
-    const int n_valid = n_ok - key0;  // valid keys of block jb (>= 1)
-    const bool more = jb + 1 < jb1;
-    if (more) {
-      flash_block(src, H, pl, jb + 1, act, key0, n_ok);
-      flash_dma<DH>(lds3 + ((jb - jb0 + 1) & 1) * FS::STAGE, src, dofs, koff, vaoff, vpoff, act, key0);
-    }
-    if (active && flash_compute<DH>(cur, n_valid, qf, o, m_ref, l_run, qscale) && lane == 0) s_restart = 1;
-    if (more) {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      flash_fix<DH>(nxt, n_ok - key0);
-    }
-    __syncthreads();
-    if (s_restart) {
-      // a row's scores outgrew its reference: start the key range again with
-      // the new references (rare; the references only grow)
-      __syncthreads();
-      if (threadIdx.x == 0) s_restart = 0;
-      l_run = 0.f;
+  for (int j = 0; j < nblk; ++j) {
+    const int slot = j % NS;
+    int n_valid = 0;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      jb = jb0;
-      flash_block(src, H, pl, jb0, act, key0, n_ok);
-      flash_dma<DH>(lds3, src, dofs, koff, vaoff, vpoff, act, key0);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      flash_fix<DH>(lds, n_ok - key0);
-      __syncthreads();
-      continue;
+    for (int s = 0; s < NS; ++s) n_valid = s == slot ? nval[s] : n_valid;
+    // block j has landed once at most min(NS - 2, nblk - 1 - j) later blocks
+    // of the range are pending (blocks issued past the range, when it is
+    // shorter than NS - 1, only make this wait longer)
+    const int later = nblk - 1 - j;
+    if (later >= 2) flash_wait<2 * LDW, false>();
+    else if (later == 1) flash_wait<LDW, false>();
+    else flash_wait<0, false>();
+    flash_fix<DH>(lds + slot * FS::STAGE, n_valid);
+    // the V^T masks visible; every wave's part of block j landed; block j - 1
+    // fully consumed, so its stage can take block j + NS - 1
+    flash_wait<63, true>();
+    __builtin_amdgcn_s_barrier();
+    if (j + NS - 1 < nblk) {
+      const int ns = (j + NS - 1) % NS;
+      const int nv = flash_issue<DH>(ring + ns * FS::STAGE, src, jb0 + j + NS - 1, koff, vaoff, vpoff, vst_ld, vpt_ld);
+#pragma unroll
+      for (int s = 0; s < NS; ++s) nval[s] = s == ns ? nv : nval[s];
     }
-    if (++jb == jb1) break;
+    if (active) flash_compute<DH>(lds + slot * FS::STAGE, n_valid, qf, o, m_ref, l_run, qscale);
   }
   if (!active) return;
 
-  // O^T: lane holds dims nt*16 + 4g .. + 4 of query row fr
-  float l = l_run;
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
-  const int r = row0 + fr;
-  if (r >= R) return;
-  const float rl = 1.0f / l;
+  // O^T: lane holds dims nt*16 + 4g .. + 4 of query row fr of each tile
   typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-  if (S == 1) {
-    const int hn = r / H, i = r - hn * H;
-    const size_t base = ((size_t)b * H + i) * (size_t)a.nH * DH + (size_t)hn * DH + 4 * g;
-    if (a.out_f32) {
-      float* out = reinterpret_cast<float*>(a.out) + base;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) *reinterpret_cast<f32x4*>(out + nt * 16) = o[nt] * rl;
+  for (int rt = 0; rt < RT; ++rt) {
+    float l = l_run[rt];
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const int r = row0 + 16 * rt + fr;
+    if (r >= R) continue;
+    const float rl = 1.0f / l;
+    if (S == 1) {
+      const int hn = r / H, i = r - hn * H;
+      const size_t base = ((size_t)b * H + i) * (size_t)a.nH * DH + (size_t)hn * DH + 4 * g;
+      if (a.out_f32) {
+        float* out = reinterpret_cast<float*>(a.out) + base;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) *reinterpret_cast<f32x4*>(out + nt * 16) = o[rt][nt] * rl;
+      } else {
+        bf16* out = reinterpret_cast<bf16*>(a.out) + base;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const f32x4 v = o[rt][nt] * rl;
+          *reinterpret_cast<bf16x4*>(out + nt * 16) = bf16x4{static_cast<bf16>(v[0]), static_cast<bf16>(v[1]),
+                                                             static_cast<bf16>(v[2]), static_cast<bf16>(v[3])};
+        }
+      }
     } else {
-      bf16* out = reinterpret_cast<bf16*>(a.out) + base;
+      const size_t rowi = ((size_t)split * a.B + b) * R + r;
+      bf16* out = reinterpret_cast<bf16*>(part) + rowi * DH + 4 * g;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const f32x4 v = o[nt] * rl;
-        *reinterpret_cast<bf16x4*>(out + nt * 16) =
-            bf16x4{static_cast<bf16>(v[0]), static_cast<bf16>(v[1]), static_cast<bf16>(v[2]), static_cast<bf16>(v[3])};
+        const f32x4 v = o[rt][nt] * rl;
+        *reinterpret_cast<bf16x4*>(out + nt * 16) = bf16x4{static_cast<bf16>(v[0]), static_cast<bf16>(v[1]),
+                                                           static_cast<bf16>(v[2]), static_cast<bf16>(v[3])};
       }
+      if (g == 0) ml[rowi] = float2{m_ref[rt], l};
     }
-  } else {
-    const size_t rowi = ((size_t)split * a.B + b) * R + r;
-    bf16* out = reinterpret_cast<bf16*>(part) + rowi * DH + 4 * g;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const f32x4 v = o[nt] * rl;
-      *reinterpret_cast<bf16x4*>(out + nt * 16) =
-          bf16x4{static_cast<bf16>(v[0]), static_cast<bf16>(v[1]), static_cast<bf16>(v[2]), static_cast<bf16>(v[3])};
-    }
-    if (g == 0) ml[rowi] = float2{m_ref, l};
   }
 }
 
@@ -444,7 +449,7 @@ __global__ __launch_bounds__(256) void k_flash_merge(AttnLaunch a, int S, const 
 // Key ranges per (rollout, 128-row tile): enough workgroups to cover the
 // chip once, at least two key blocks per range.
 int flash_splits(int B, int nH, int H, int P, int n_cu) {
-  const int KB = 64;
+  const int KB = 32;
   const int nqt = (nH * H + 127) / 128;
   const int nb = (H + KB - 1) / KB + (P + KB - 1) / KB;
   int s = (n_cu + B * nqt - 1) / (B * nqt);
