@@ -16,7 +16,8 @@
 //             per-chunk max, probability sum and output row / sum (bf16)
 //   2 COMB    chunk combine per (rollout, head, query row) -> o
 //   3 OPROJ   o x W_o, split-K slices -> part
-//   4 ROWS    row owner: residual += gate * sum of slices; MLP adaRMSNorm -> y
+//   4 ROWS    row owner: residual += gate * sum of slices (polled, not
+//             flagged); MLP adaRMSNorm -> y
 //   5 GATEUP  y x [gate|up], GeGLU epilogue -> z
 //   6 DOWN    z x W_down, split-K slices -> part
 //   7 ROWS    row owner: residual update + next layer's attention norm, or
@@ -45,10 +46,15 @@
 // launch (activations, slices, attention partials, the action rows' K and V,
 // completion flags) is stored and loaded with device-scope coherent buffer
 // accesses (cache policy sc1); a completion flag is stored only after
-// s_waitcnt vmcnt(0) confirms the workgroup's stores.  No agent-scope fences
-// are used (on gfx950 they serialise across the chip).  Weights, the prefix K,
-// the prefix part of the transposed V, the modulation table and the RoPE
-// table are read-only during the launch and use plain loads.
+// s_waitcnt vmcnt(0) confirms the workgroup's stores.  The split-K slices are
+// the exception: each word has one reader (its row owner), which polls the
+// words themselves until they leave the EMPTY pattern and writes EMPTY back,
+// so their producers neither wait for store confirmation nor store a flag
+// (the confirmation round trip and the flag hop leave the critical path).
+// No agent-scope fences are used (on gfx950 they serialise across the chip).
+// Weights, the prefix K, the prefix part of the transposed V, the modulation
+// table and the RoPE table are read-only during the launch and use plain
+// loads.
 //
 // Every wait is bounded: after SPIN_LIMIT polls the workgroup records
 // an error word and stops waiting, so a launch always terminates; the host
@@ -122,6 +128,21 @@ __device__ __forceinline__ u32 poll4(rsrc_t r, u32 off) {
   asm volatile("" ::: "memory");
   return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, CPOL_DEV);
 }
+// A 16-byte polling load (see poll4).
+__device__ __forceinline__ u32x4 poll16(rsrc_t r, u32 off) {
+  asm volatile("" ::: "memory");
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, CPOL_DEV);
+}
+// Split-K slices travel without completion flags: every 32-bit word of the
+// slice buffer holds EMPTY until its producer writes a value, and the row
+// owner that reads it (its only reader) writes EMPTY back.  Producers
+// canonicalise NaN, so a value never has the EMPTY pattern.
+constexpr u32 EMPTY = 0xffffffffu;
+__device__ __forceinline__ bool has_empty(u32x4 v) {
+  return v[0] == EMPTY || v[1] == EMPTY || v[2] == EMPTY || v[3] == EMPTY;
+}
+__device__ __forceinline__ u32 f2u_value(float v) { return v == v ? __builtin_bit_cast(u32, v) : 0x7fc00000u; }
+
 __device__ __forceinline__ void st4(rsrc_t r, u32 off, u32 v) { __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, CPOL_DEV); }
 __device__ __forceinline__ void st16(rsrc_t r, u32 off, u32x4 v) {
   __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, CPOL_DEV);
@@ -404,8 +425,8 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
       if (row >= M) continue;
       if (j.kind == EPI_SLICE) {
         const u32 base = (u32)(((size_t)s * M + row) * Wd + col) * 4u;
-        st4(rp, base, f2u(lo[e]));
-        st4(rp, base + 64u, f2u(hi[e]));
+        st4(rp, base, f2u_value(lo[e]));
+        st4(rp, base + 64u, f2u_value(hi[e]));
       } else if (j.kind == EPI_GEGLU) {  // gate/up rows interleaved in 16-row groups
         st_bf16(rz, frag_off(row, t * 16 + fr, a.F / 32) * 2u, gelu_tanh(lo[e]) * hi[e]);
       } else {
@@ -437,7 +458,7 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
 // ---- phase 1: attention chunk partials ----------------------------------------
 template <int DH>
 __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* smem, const Deps& deps, u32 value,
-                                           u32* s_abort, lds_t* wt) {
+                                           u32* s_abort, lds_t* wt, char* stage) {
   // The workgroup stages the chunk's K and V^T in LDS with coalesced loads
   // (one workgroup barrier); after that every wave works alone on its 16 query rows,
   // with P and the partial output in registers.
@@ -448,6 +469,7 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
   static_assert(KCH >= 1 && VCH >= 1, "chunk too small for the workgroup");
   static_assert(KC == MF::KSUB, "one P.V step per chunk");
   static_assert((KC * LDK + DH * LDV) * 2 <= SMEM_BYTES, "attention LDS");
+  static_assert(NWV * 16 * (DH * 2 + 16) <= WT_STEPS * 2 * 1024, "attention output staging");
   bf16* Ks = reinterpret_cast<bf16*>(smem);
   bf16* Vt = Ks + KC * LDK;
   const int H = a.H, nH = a.nH, C = a.C;
@@ -582,18 +604,28 @@ __device__ __forceinline__ void phase_attn(const PersistArgs& a, int l, char* sm
       const MF::frag va = __builtin_bit_cast(MF::frag, u32x4{v0[0], v0[1], v1[0], v1[1]});
       o[nt] = MF::run(va, pb, f32x4{0.f, 0.f, 0.f, 0.f});
     }
-    // O^T: lane holds dims nt*16 + 4g .. +4 of query row fr: whole 16-byte
-    // pieces of a row-major partial row
-    const size_t slot = ((size_t)b * nH + hn) * C + c;
-    const int i = w * 16 + fr;
-    if (i < H) {
-      // the chunk's output divided by its probability sum, in bf16 (the
-      // combine weights it by the sum again, in fp32)
-      const u32 base = (u32)(((slot * H + i) * DH + 4 * g) * 2);
-      const float rl = sum > 0.f ? 1.0f / sum : 0.f;
+    // O^T: lane holds dims nt*16 + 4g .. +4 of query row w*16 + fr.  The
+    // chunk's output rows, divided by their probability sums in bf16 (the
+    // combine weights them by the sums again, in fp32), are row-major and
+    // contiguous per wave in memory; they leave through LDS so that every
+    // global store instruction writes whole 128-byte lines (scattered partial
+    // lines cost several times more to store and confirm).
+    constexpr int SROW = DH * 2 + 16;  // staged row stride in bytes (spreads the LDS banks)
+    char* stw = stage + w * 16 * SROW;
+    const float rl = sum > 0.f ? 1.0f / sum : 0.f;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) st8(ro, base + (u32)nt * 32u, pack4_bf16(o[nt] * rl));
-      if (g == 0) st8(rml, (u32)((slot * H + i) * 8), u32x2{f2u(mx), f2u(sum)});
+    for (int nt = 0; nt < NT; ++nt)
+      *reinterpret_cast<u32x2*>(stw + fr * SROW + nt * 32 + 8 * g) = pack4_bf16(o[nt] * rl);
+    const size_t slot = ((size_t)b * nH + hn) * C + c;
+    const int nrows = min(16, H - w * 16);  // rows of this wave that exist
+    if (nrows > 0) {
+      const u32 base = (u32)(((slot * H + w * 16) * DH) * 2);
+      const int bytes = nrows * DH * 2;
+      for (int off = lane * 16; off < bytes; off += 1024) {
+        const int row = off / (DH * 2), col = off - row * (DH * 2);
+        st16(ro, base + (u32)off, *reinterpret_cast<const u32x4*>(stw + row * SROW + col));
+      }
+      if (g == 0 && fr < nrows) st8(rml, (u32)((slot * H + w * 16 + fr) * 8), u32x2{f2u(mx), f2u(sum)});
     }
     __syncthreads();  // LDS reused by the next item
   }
@@ -772,7 +804,7 @@ struct RowJob {
 
 // ---- phases 4, 7: row owner updates -----------------------------------------------
 __device__ __forceinline__ void phase_rows(const PersistArgs& a, const RowJob& r, float& xreg, float* hrow,
-                                           const float* bin, float* xs, char* smem) {
+                                           const float* bin, float* xs, char* smem, u32* s_abort) {
   const int m = blockIdx.x, W = a.W, A = a.A, t = threadIdx.x;
   if (m >= a.M) return;
   float* red = reinterpret_cast<float*>(smem);  // [NWV]
@@ -793,18 +825,39 @@ __device__ __forceinline__ void phase_rows(const PersistArgs& a, const RowJob& r
   }
   f32x4 sc[NGRP], sh[NGRP];
   load_mod(a, r.scale, r.shift, sc, sh);
-  const rsrc_t rp = rsrc(a.part, (u32)((size_t)r.S * a.M * W * 4));  // slices z >= S read as zero
+  // The slices of this row: polled until no word is EMPTY (bounded), then
+  // reset to EMPTY for the next writer.
+  const rsrc_t rp = rsrc(a.part, (u32)((size_t)r.S * a.M * W * 4));
+  trace_note(s_note, 0);
 #pragma unroll
   for (int jg = 0; jg < NGRP; ++jg) {
     const int k4 = 4 * t + 4 * PT * jg;
     if (k4 >= W) break;
-    f32x4 v[RMAX_S];
+    u32x4 v[RMAX_S];
 #pragma unroll
-    for (int z = 0; z < RMAX_S; ++z) v[z] = as_f4(ld16(rp, (u32)(((size_t)z * a.M + m) * W + k4) * 4u));
+    for (int z = 0; z < RMAX_S; ++z)
+      v[z] = z < r.S ? poll16(rp, (u32)(((size_t)z * a.M + m) * W + k4) * 4u) : u32x4{0u, 0u, 0u, 0u};
+    for (u32 spins = 0;; ++spins) {
+      u32 pend = 0u;
+#pragma unroll
+      for (int z = 0; z < RMAX_S; ++z) pend |= (z < r.S && has_empty(v[z]) ? 1u : 0u) << z;
+      if (pend == 0u) break;
+      if (spins > SPIN_LIMIT || *s_abort != 0u) {
+        *s_abort = 1u;
+        st4(rsrc(a.err), 0, 1u);
+        break;
+      }
+#pragma unroll
+      for (int z = 0; z < RMAX_S; ++z)
+        if ((pend >> z) & 1u) v[z] = poll16(rp, (u32)(((size_t)z * a.M + m) * W + k4) * 4u);
+    }
+#pragma unroll
+    for (int z = 0; z < RMAX_S; ++z)
+      if (z < r.S) st16(rp, (u32)(((size_t)z * a.M + m) * W + k4) * 4u, u32x4{EMPTY, EMPTY, EMPTY, EMPTY});
     const f32x4 g4 = *reinterpret_cast<const f32x4*>(r.gate + k4);
-    f32x4 sum = v[0];
+    f32x4 sum = as_f4(v[0]);
 #pragma unroll
-    for (int z = 1; z < RMAX_S; ++z) sum += v[z];
+    for (int z = 1; z < RMAX_S; ++z) sum += as_f4(v[z]);
     f32x4* hp = reinterpret_cast<f32x4*>(hrow + k4);
     *hp = *hp + g4 * sum;
   }
@@ -860,7 +913,7 @@ __device__ __forceinline__ GemmJob make_job(const PersistArgs& a, int p, int l) 
 __device__ __forceinline__ Deps phase_deps(const PersistArgs& a, int p, const GemmJob& j) {
   const int G = gridDim.x, bid = blockIdx.x;
   const int M = a.M, H = a.H, nH = a.nH, Dh = a.Dh, C = a.C;
-  if (p == 4 || p == 7) return bid < M ? deps_all() : deps_none();  // row phases: every slice producer
+  if (p == 4 || p == 7) return deps_none();  // row phases poll the slice data instead of flags
   if (p == 0 || p == 5) return bid < j.tiles ? Deps{0, M, 0, 0} : deps_none();  // QKV, GateUp: the row owners
   if (p == 1) {  // attention: the QKV tiles of this head, and of k and v if the chunk holds action keys
     const int n_items = a.B * nH * C;
@@ -941,10 +994,11 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     const GemmJob job = make_job(a, gemm ? p : 0, l);
     // producers of this phase's inputs finished phase ph - 1 (attention waits
     // inside, after loading the prefix part of its chunk)
-    if (ph >= 0 && p != 1) wait_producers(a, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, gemm, job, wt);
+    const bool rows = p == 4 || p == 7;
+    if (ph >= 0 && p != 1 && !rows) wait_producers(a, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, gemm, job, wt);
     if (p < 0) {
     } else if (p == 1) {
-      phase_attn<DH>(a, l, smem, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, wt);
+      phase_attn<DH>(a, l, smem, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, wt, s_wt);
     } else if (p == 2) {
       phase_combine(a, smem);
     } else if (p == 4 || p == 7) {
@@ -968,7 +1022,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
           r.final_step = true;
         }
       }
-      phase_rows(a, r, xreg, s_hrow, s_bin, s_x, smem);
+      phase_rows(a, r, xreg, s_hrow, s_bin, s_x, smem, &s_abort);
       if (r.final_step && k + 1 < a.n_steps) ki = k + 1;  // same workgroup, no wait needed
     } else {
       phase_gemm(a, job, l, wt, smem);
@@ -977,7 +1031,11 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
       const float* ti = a.table + (size_t)(at_t0 ? a.n_steps : ki) * a.R;
       inproj_row(a, ti, ti + W, s_hrow, s_bin, s_x, reinterpret_cast<float*>(smem), crow);
     }
-    if (ph < last_phase) phase_done(a, (u32)(ph + 2));
+    // Completion flags: the row owners poll the split-K slices themselves, so
+    // the slice producers (phases 3, 6) and the workgroups without a row
+    // (row phases) have nothing to signal and go straight on.
+    const bool signal = !(p == 3 || p == 6) && !(rows && !owner);
+    if (ph < last_phase && signal) phase_done(a, (u32)(ph + 2));
     if (ph >= 0) trace_end(a, s_note, ph);
   }
   if (owner && t < A && ia >= 0) a.x[xrow * A + t] = xreg;
@@ -997,9 +1055,12 @@ __global__ void k_frag_order(const u32x4* __restrict__ src, u32x4* __restrict__ 
   }
 }
 
-__global__ void k_persist_reset(u32* flags, int n) {  // n = FLAG_WORDS
+// Before every launch: completion flags to zero, the split-K slice words to
+// EMPTY.
+__global__ void k_persist_reset(u32* flags, int n, u32x4* part, int n_part4) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) flags[i] = 0u;
+  if (i < n) flags[i] = 0u;  // n = FLAG_WORDS
+  for (int j = i; j < n_part4; j += gridDim.x * blockDim.x) part[j] = u32x4{EMPTY, EMPTY, EMPTY, EMPTY};
 }
 
 }  // namespace
@@ -1049,7 +1110,9 @@ hipError_t persist_occupancy(int Dh, int* blocks_per_cu) {
 
 hipError_t launch_persist(const PersistArgs& a, int grid, hipStream_t s) {
   if (grid > MAX_GRID) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_persist_reset, dim3((FLAG_WORDS + 255) / 256), dim3(256), 0, s, a.flags, FLAG_WORDS);
+  const int n_part4 = std::max(a.s_o, a.s_d) * a.M * a.W / 4;  // the slice words start EMPTY
+  hipLaunchKernelGGL(k_persist_reset, dim3(std::max((FLAG_WORDS + 255) / 256, std::min((n_part4 + 255) / 256, 1024))),
+                     dim3(256), 0, s, a.flags, FLAG_WORDS, reinterpret_cast<u32x4*>(a.part), n_part4);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   switch (a.Dh) {
