@@ -419,17 +419,70 @@ __device__ __forceinline__ void phase_gemm(const PersistArgs& a, const GemmJob& 
       hi += red[((v * 4 + wave) * 2 + 1) * 64 + lane];
     }
     __syncthreads();  // red and the tile are reused by the next item
+    // Slices and z leave through LDS (the freed reduction area, a region per
+    // wave) so that each store instruction writes whole lines: a slice row's
+    // 32 columns are one 128-byte line, a wave's 16 x 16 z values one half of
+    // a fragment block (512 contiguous bytes).  Rows >= M are not stored.
+    char* sw = smem + wave * 16 * 144;
+    if (j.kind == EPI_SLICE) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int rl = (lane >> 4) * 4 + e;
+        *reinterpret_cast<u32*>(sw + rl * 144 + fr * 4) = f2u_value(lo[e]);
+        *reinterpret_cast<u32*>(sw + rl * 144 + 64 + fr * 4) = f2u_value(hi[e]);
+      }
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int rl = k * 8 + (lane >> 3), row = wave * 16 + rl;
+        if (row < M)
+          st16(rp, (u32)(((size_t)s * M + row) * Wd + t * 32 + (lane & 7) * 4) * 4u,
+               *reinterpret_cast<const u32x4*>(sw + rl * 144 + (lane & 7) * 16));
+      }
+      continue;
+    }
+    if (j.kind == EPI_GEGLU) {  // gate/up rows interleaved in 16-row groups: z column t * 16 + fr
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const u32 v = bf16_bits(gelu_tanh(lo[e]) * hi[e]);
+        const u32 pair = v | (__shfl_xor(v, 1, 64) << 16);  // columns fr, fr + 1 (fr even)
+        if ((fr & 1) == 0) *reinterpret_cast<u32*>(sw + ((lane >> 4) * 4 + e) * 48 + fr * 2) = pair;
+      }
+      const int rl = lane & 15, row = wave * 16 + rl;
+      if (lane < 32 && row < M)
+        st16(rz, frag_off(row, t * 16 + (lane >> 4) * 8, a.F / 32) * 2u,
+             *reinterpret_cast<const u32x4*>(sw + rl * 48 + (lane >> 4) * 16));
+      continue;
+    }
+    // q columns: the tile holds 16 RoPE pairs (d, d + Dh/2), d = 16 jq + fr.
+    // When the wave's 16 rows are rows of one rollout starting at a multiple
+    // of 16 (one rollout, or H % 16 == 0) they form two half fragment blocks
+    // of that rollout's q, stored whole through LDS.
+    if (qkv && hn >= 0 && (a.B == 1 || (H & 15) == 0)) {
+      const int jq = (within >> 5);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float r_lo = lo[e] * cs[e].x - hi[e] * cs[e].y;
+        const float r_hi = lo[e] * cs[e].y + hi[e] * cs[e].x;
+        const u32 vl = bf16_bits(r_lo), vh = bf16_bits(r_hi);
+        const u32 pl2 = vl | (__shfl_xor(vl, 1, 64) << 16), ph2 = vh | (__shfl_xor(vh, 1, 64) << 16);
+        char* rowp = sw + ((lane >> 4) * 4 + e) * 80;
+        if ((fr & 1) == 0) {
+          *reinterpret_cast<u32*>(rowp + fr * 2) = pl2;
+          *reinterpret_cast<u32*>(rowp + 32 + fr * 2) = ph2;
+        }
+      }
+      const int part = lane >> 5, r = lane & 15, cc = (lane >> 4) & 1;
+      const int row = wave * 16 + r, b = row / H, i = row - b * H;
+      if (row < M)
+        st16(rq, ((u32)(((size_t)b * nH + hn) * 64 * Dh) + frag_off(i, 16 * jq + part * half + cc * 8, Dh / 32)) * 2u,
+             *reinterpret_cast<const u32x4*>(sw + r * 80 + part * 32 + cc * 16));
+      continue;
+    }
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int row = wave * 16 + (lane >> 4) * 4 + e;
       if (row >= M) continue;
-      if (j.kind == EPI_SLICE) {
-        const u32 base = (u32)(((size_t)s * M + row) * Wd + col) * 4u;
-        st4(rp, base, f2u_value(lo[e]));
-        st4(rp, base + 64u, f2u_value(hi[e]));
-      } else if (j.kind == EPI_GEGLU) {  // gate/up rows interleaved in 16-row groups
-        st_bf16(rz, frag_off(row, t * 16 + fr, a.F / 32) * 2u, gelu_tanh(lo[e]) * hi[e]);
-      } else {
+      {
         const int b = row / H, i = row - b * H;
         if (roped) {
           const float r_lo = lo[e] * cs[e].x - hi[e] * cs[e].y;
