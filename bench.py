@@ -47,10 +47,11 @@ METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roof
 # sha256 of the kernel source they were measured on; the byte counts are the
 # counter readings times the copy calibration factor.
 MEASURED_TRAFFIC = {
-    # pi0.5 shape, batch 1: FETCH_SIZE 5270106.8 KiB x 1.99980 (a 256 MiB copy
-    # reads back 131085.29 KiB) + WRITE_SIZE 2007096.2 KiB x 1.00000 (the copy's
+    # pi0.5 shape, batch 1: FETCH_SIZE 5214537.3 KiB x 1.99980 (a 256 MiB copy
+    # reads back 131085.25 KiB) + WRITE_SIZE 2469905.2 KiB x 1.00000 (the copy's
     # 262144 KiB), mean over 4 dispatches
-    ("45e2bd4af4a0eb666973075f8b37bdb789e79c606dce307d6db7823c9ff94ffb", "pi05-b1"): 12847350883,
+    ("c86bc9ca8a00a2eae6bdb2c53629e1cb8b58b770f01cf941ada4e2fac149e9a4", "pi05-b1"):
+        round(5214537.28125 * 1024 * 1.999797841481021 + 2469905.1875 * 1024),
 }
 
 
