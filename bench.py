@@ -47,11 +47,11 @@ METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roof
 # sha256 of the kernel source they were measured on; the byte counts are the
 # counter readings times the copy calibration factor.
 MEASURED_TRAFFIC = {
-    # pi0.5 shape, batch 1: FETCH_SIZE 5214537.3 KiB x 1.99980 (a 256 MiB copy
-    # reads back 131085.25 KiB) + WRITE_SIZE 2469905.2 KiB x 1.00000 (the copy's
+    # pi0.5 shape, batch 1: FETCH_SIZE 5211972.6 KiB x 1.99980 (a 256 MiB copy
+    # reads back 131085.125 KiB) + WRITE_SIZE 2469905.2 KiB x 1.00000 (the copy's
     # 262144 KiB), mean over 4 dispatches
-    ("c86bc9ca8a00a2eae6bdb2c53629e1cb8b58b770f01cf941ada4e2fac149e9a4", "pi05-b1"):
-        round(5214537.28125 * 1024 * 1.999797841481021 + 2469905.1875 * 1024),
+    ("ddd2c3cf9a09c60c8b934a97fc655d9d4e8b2290b75b5576700d12f60b661aaf", "pi05-b1"):
+        round(5211972.640625 * 1024 * 1.999799748445905 + 2469905.1875 * 1024),
 }
 
 

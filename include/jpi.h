@@ -301,6 +301,19 @@ jpi_status jpi_debug_prefix_vt(jpi_ctx* ctx, void** vt_out, int* ld_out);
 jpi_status jpi_debug_persist_trace(jpi_ctx* ctx, uint64_t* host_out, int64_t cap, int* n_workgroups, int* n_slots,
                                    double* ticks_per_us);
 
+/* Test hook for the single-launch kernel's failure path.  That kernel's waits
+ * for its producers' completion flags give up after `polls` unsuccessful
+ * polls (its waits for split-K slice data keep the default bound and stop as
+ * soon as their workgroup gave up elsewhere); a workgroup that gave up
+ * records an error word and waits no more, so a launch always ends, jpi_sync
+ * reports JPI_ERR_HIP ("... timed out") and the call's output is invalid.
+ * polls = 0 restores the default bound (2^21 polls, seconds).  A tiny bound
+ * forces the failure from the host while every kernel still exits normally.
+ * Synchronises the device and drops the captured graphs (the bound is a
+ * launch argument).
+ * Errors: JPI_ERR_ARG (NULL ctx), JPI_ERR_HIP. */
+jpi_status jpi_debug_set_spin_limit(jpi_ctx* ctx, uint32_t polls);
+
 /* Kernel kinds of one denoise step, in launch order per layer. */
 typedef enum {
   JPI_KERNEL_NONE = -1,

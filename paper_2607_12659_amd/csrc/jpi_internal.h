@@ -153,6 +153,7 @@ struct PersistArgs {
   void* z;                  // fragment-ordered [64][F]
   unsigned* flags;          // [grid][32] completion flags: the last phase index + 2 each workgroup finished
   unsigned* err;            // set to 1 if a wait for producers timed out
+  unsigned spin_limit;      // unsuccessful polls after which a wait gives up (>= 1)
   hipEvent_t ev_start, ev_stop;
   unsigned long long* trace;  // trace build only: [grid][trace_slots] real-time stamps (else null)
   int trace_slots;            // 1 + phases recorded per workgroup
@@ -161,6 +162,7 @@ bool persist_supported(jpi_dtype dt, int M, int W, int nH, int Dh, int F, int H,
 int persist_chunks(int P, int H);
 int persist_pick_split(int tiles, int K, int grid);
 int persist_block_threads();
+unsigned persist_default_spin();  // polls a wait makes before it gives up
 int persist_max_grid();    // largest grid the completion flags support
 int persist_flag_words();  // size of the completion flag buffer in 32-bit words
 bool persist_trace_build(); // the kernel was compiled with JPI_PERSIST_TRACE (phase timestamps)

@@ -56,9 +56,12 @@
 // table and the RoPE table are read-only during the launch and use plain
 // loads.
 //
-// Every wait is bounded: after SPIN_LIMIT polls the workgroup records
-// an error word and stops waiting, so a launch always terminates; the host
-// reports the error from jpi_sync.
+// Every wait is bounded: a flag wait gives up after a.spin_limit unsuccessful
+// polls (default SPIN_LIMIT), a row owner's slice wait after SPIN_LIMIT polls
+// or as soon as its workgroup gave up elsewhere. Giving up records an error
+// word and stops all later waits of the workgroup, so a launch always
+// terminates; the host reports the error from jpi_sync. (A variable bound in
+// the slice wait costs the kernel register spills; the fixed one does not.)
 #include <algorithm>
 
 #include "jpi_device.h"
@@ -258,7 +261,7 @@ __device__ __forceinline__ Deps deps_items(int i0, int i1) {
 // Wave 0 polls the producers' flags (lane l covers the l-th, l+64-th, ...
 // workgroup of the two ranges) until all reach `value`; waves 1..3 meanwhile
 // start the direct-to-LDS loads of the first weight tile of a GEMM phase.
-// Every wait is bounded: past SPIN_LIMIT polls the workgroup records an error
+// Every wait is bounded: past a.spin_limit polls the workgroup records an error
 // word and stops waiting, so the launch always terminates.
 __device__ __forceinline__ void wait_producers(const PersistArgs& a, const Deps& d, u32 value, u32* s_abort,
                                                bool tile, const GemmJob& j, lds_t* wt) {
@@ -288,7 +291,7 @@ __device__ __forceinline__ void wait_producers(const PersistArgs& a, const Deps&
       for (int u = 0; u < 4; ++u)
         if (f[u] >= value) pend &= ~(1u << u);
       if (__all(pend == 0u)) break;
-      if (spins > SPIN_LIMIT) {
+      if (spins + 1 >= s_abort[1]) {
         if (threadIdx.x == 0) {
           *s_abort = 1u;
           st4(rsrc(a.err), 0, 1u);
@@ -1009,7 +1012,8 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
   __shared__ __attribute__((aligned(16))) float s_hrow[MAX_W];  // residual row of the owned action row
   __shared__ __attribute__((aligned(16))) float s_bin[MAX_W];
   __shared__ float s_x[64];
-  __shared__ u32 s_abort;
+  __shared__ u32 s_ctl[2];  // [0]: a wait gave up (stop waiting); [1]: polls per wait (read where tested,
+                            // so that the bound occupies no register across the kernel)
   const int t = threadIdx.x, m = blockIdx.x;
   const int L = a.L, W = a.W, A = a.A;
   const bool owner = m < a.M;
@@ -1021,7 +1025,10 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
                               : nullptr;
   const bool at_t0 = ia >= 0 && ia < a.n_t0;  // a committed row modulated at t = 0 (table row n_steps)
   float xreg = 0.f;
-  if (t == 0) s_abort = 0u;
+  if (t == 0) {
+    s_ctl[0] = 0u;
+    s_ctl[1] = a.spin_limit;
+  }
   if (owner) {
     for (int k4 = 4 * t; k4 < W; k4 += 4 * PT)
       *reinterpret_cast<f32x4*>(s_bin + k4) = *reinterpret_cast<const f32x4*>(a.b_in + k4);
@@ -1048,10 +1055,10 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
     // producers of this phase's inputs finished phase ph - 1 (attention waits
     // inside, after loading the prefix part of its chunk)
     const bool rows = p == 4 || p == 7;
-    if (ph >= 0 && p != 1 && !rows) wait_producers(a, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, gemm, job, wt);
+    if (ph >= 0 && p != 1 && !rows) wait_producers(a, phase_deps(a, p, job), (u32)(ph + 1), s_ctl, gemm, job, wt);
     if (p < 0) {
     } else if (p == 1) {
-      phase_attn<DH>(a, l, smem, phase_deps(a, p, job), (u32)(ph + 1), &s_abort, wt, s_wt);
+      phase_attn<DH>(a, l, smem, phase_deps(a, p, job), (u32)(ph + 1), s_ctl, wt, s_wt);
     } else if (p == 2) {
       phase_combine(a, smem);
     } else if (p == 4 || p == 7) {
@@ -1075,7 +1082,7 @@ __global__ __launch_bounds__(PT) void k_persist(PersistArgs a) {
           r.final_step = true;
         }
       }
-      phase_rows(a, r, xreg, s_hrow, s_bin, s_x, smem, &s_abort);
+      phase_rows(a, r, xreg, s_hrow, s_bin, s_x, smem, s_ctl);
       if (r.final_step && k + 1 < a.n_steps) ki = k + 1;  // same workgroup, no wait needed
     } else {
       phase_gemm(a, job, l, wt, smem);
@@ -1136,6 +1143,8 @@ int persist_pick_split(int tiles, int K, int grid) {
 }
 
 int persist_block_threads() { return PT; }
+
+unsigned persist_default_spin() { return SPIN_LIMIT; }
 
 int persist_max_grid() { return MAX_GRID; }
 

@@ -138,6 +138,7 @@ struct jpi_ctx {
   hipStream_t cap_stream = nullptr;
   // single-launch (persistent) path
   unsigned* pflags = nullptr;  // completion flag lines of the single-launch kernel (one per workgroup)
+  unsigned persist_spin = 0;   // bound of the single-launch kernel's waits in polls (0: the default)
   unsigned* perr = nullptr;    // set when a wait for producers timed out
   unsigned long long* ptrace = nullptr;  // trace build only: [max grid][trace_slots] phase timestamps
   int trace_slots = 0, trace_grid = 0, trace_used = 0;
@@ -1067,6 +1068,7 @@ hipError_t enqueue_steps(jpi_ctx* c, const float* table, int n_steps, hipStream_
     pa.z = c->zsw;
     pa.flags = c->pflags;
     pa.err = c->perr;
+    pa.spin_limit = c->persist_spin ? c->persist_spin : persist_default_spin();
     pa.trace = c->ptrace;
     pa.trace_slots = c->trace_slots;
     c->trace_used = std::min(c->trace_slots, 1 + 3 * n_steps * L * 8);
@@ -1314,6 +1316,15 @@ jpi_status jpi_sync(jpi_ctx* c, void* stream) {
     HIPCHK(c, hipMemset(c->perr, 0, sizeof(perr)));
     return fail(c, JPI_ERR_HIP, "single-launch denoise: a wait for producer workgroups timed out; the output is invalid");
   }
+  return JPI_OK;
+}
+
+jpi_status jpi_debug_set_spin_limit(jpi_ctx* c, uint32_t polls) {
+  if (!c) return fail(nullptr, JPI_ERR_ARG, "jpi_debug_set_spin_limit: ctx is NULL");
+  HIPCHK(c, hipSetDevice(c->device));
+  HIPCHK(c, hipDeviceSynchronize());
+  c->persist_spin = polls;
+  drop_graphs(c);  // the bound is an argument of the captured launch
   return JPI_OK;
 }
 

@@ -26,6 +26,7 @@ EXPORTED = ["jpi_abi_version", "jpi_status_str", "jpi_last_error", "jpi_create",
             "jpi_bind_prefix", "jpi_bind_state", "jpi_denoise",
             "jpi_sync", "jpi_debug_gemm", "jpi_gemm_noalloc", "jpi_gemm_noalloc_scratch_bytes",
             "jpi_gemm_noalloc_last_error", "jpi_debug_attention", "jpi_debug_time_kernel", "jpi_debug_kernel_time",
+            "jpi_debug_set_spin_limit",
             "jpi_sched_run", "jpi_sched_sim_hooks", "jpi_vlm_create", "jpi_vlm_destroy", "jpi_vlm_set_weight",
             "jpi_vlm_finalize_weights", "jpi_vlm_prefill", "jpi_vlm_last_error", "jpi_set_committed_t0", "jpi_bind_robot_state", "jpi_corr_create",
             "jpi_corr_destroy", "jpi_corr_set_weight", "jpi_corr_finalize_weights", "jpi_corr_compress",
@@ -130,6 +131,7 @@ _sig = {
     "jpi_gemm_noalloc_last_error": (ctypes.c_char_p, []),
     "jpi_debug_attention": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
     "jpi_debug_time_kernel": (_i, [_vp, _i]),
+    "jpi_debug_set_spin_limit": (_i, [_vp, ctypes.c_uint32]),
     "jpi_debug_kernel_time": (_i, [_vp, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_i)]),
     "jpi_sched_run": (_i, [ctypes.POINTER(jpi_sched_config), ctypes.POINTER(jpi_sched_hooks),
                            ctypes.POINTER(jpi_sched_stats), ctypes.POINTER(jpi_sched_event), _i64]),
@@ -281,6 +283,11 @@ def jpi_debug_attention(q, ks, vs, kp, vp, prefix_len_host, batch, n_heads, H, P
     lens = _i32_host(prefix_len_host)
     return _lib.jpi_debug_attention(addr(q), addr(ks), addr(vs), addr(kp), addr(vp), lens.ctypes.data, batch, n_heads,
                                     H, P, Dh, dtype, addr(out), stream_handle(stream))
+
+
+def jpi_debug_set_spin_limit(ctx, polls: int) -> int:
+    """Bound of the single-launch kernel's waits in polls (0: the default); a test hook for its failure path."""
+    return _lib.jpi_debug_set_spin_limit(ctx, polls)
 
 
 def jpi_debug_time_kernel(ctx, kind: int) -> int:

@@ -338,3 +338,34 @@ def test_persistent_tiny_bf16_repeated_calls_bitwise():
             assert np.array_equal(out.cpu().numpy().astype(np.float64), ref), "call %d differs" % i
     finally:
         ae.close()
+
+
+def test_persistent_wait_timeout_is_reported_and_recovers():
+    """Failure path of the single-launch kernel, forced from the host: with a
+    bound of one poll its waits give up at once (the producers cannot have
+    finished), the launch still ends, jpi_sync reports the timeout, and with
+    the default bound restored the next call is exact again."""
+    torch = torch_cuda()
+    from paper_2607_12659_amd import jpi
+    from paper_2607_12659_amd.expert import to_device
+    wl = synth.WORKLOADS["tiny-fp32"].with_(dtype="bf16", batch=3, n_fixed=2, prefix_len=(64, 5, 41),
+                                            name="tiny-bf16-b3")
+    inp = Inputs(wl)
+    ae = make_expert(wl, inp.weights)
+    try:
+        ref = run(ae, inp.K, inp.V, inp.noise, wl.n_steps, prefix_len=inp.prefix_len,
+                  committed=inp.committed, n_fixed=2)
+        d = to_device(np.ascontiguousarray(inp.noise, np.float32))
+        print("case tiny-bf16-b3 with a one-poll wait bound", flush=True)
+        assert jpi.jpi_debug_set_spin_limit(ae.ctx, 1) == jpi.JPI_OK
+        ae.denoise(d, wl.n_steps)
+        with pytest.raises(jpi.JpiError, match="timed out"):
+            ae.sync()
+        torch.cuda.synchronize()
+        assert jpi.jpi_debug_set_spin_limit(ae.ctx, 0) == jpi.JPI_OK
+        out = ae.denoise(d, wl.n_steps)
+        ae.sync()
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy().astype(np.float64), ref)
+    finally:
+        ae.close()
