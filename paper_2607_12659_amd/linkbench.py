@@ -41,14 +41,18 @@ def main():
     out = subprocess.run([EXE, str(args.phases)], stdout=subprocess.PIPE, text=True, check=True).stdout
     lines = ["| link | activation KiB | producers | consumers | background KiB per CU | us per phase | check |",
              "|---|---:|---:|---:|---:|---:|---|"]
+    notes = []
     for row in out.splitlines():
-        if row.startswith("#"):
+        if row.startswith("# CUs"):
             lines.insert(0, row[2:] + "\n")
+            continue
+        if row.startswith("#"):
+            notes.append(row[2:])
             continue
         mode, kb, prod, cons, bg, us, err, bad = row.split()
         ok = "ok" if err == "0" and bad == "0" else "ERROR (err %s, mismatches %s)" % (err, bad)
         lines.append("| %s | %s | %s | %s | %s | %s | %s |" % (mode, kb, prod, cons, bg, us, ok))
-    text = "\n".join(lines) + "\n"
+    text = "\n".join(lines) + "\n" + "".join("\n" + n + "\n" for n in notes)
     print(text)
     if args.out:
         with open(args.out, "w") as f:
