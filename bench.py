@@ -47,22 +47,25 @@ METRIC = "action chunks/sec (10-step flow denoise, pi0.5 shape, B=1); % HBM roof
 # sha256 of the kernel source they were measured on; the byte counts are the
 # counter readings times the copy calibration factor.
 MEASURED_TRAFFIC = {
-    # pi0.5 shape, batch 1: FETCH_SIZE 5211972.6 KiB x 1.99980 (a 256 MiB copy
-    # reads back 131085.125 KiB) + WRITE_SIZE 2469905.2 KiB x 1.00000 (the copy's
+    # pi0.5 shape, batch 1: FETCH_SIZE 5213836.7 KiB x 1.99980 (a 256 MiB copy
+    # reads back 131085.1875 KiB) + WRITE_SIZE 2469905.2 KiB x 1.00000 (the copy's
     # 262144 KiB), mean over 4 dispatches
-    ("ddd2c3cf9a09c60c8b934a97fc655d9d4e8b2290b75b5576700d12f60b661aaf", "pi05-b1"):
-        round(5211972.640625 * 1024 * 1.999799748445905 + 2469905.1875 * 1024),
+    ("56f8be3ce3d539a631ccde8da1389902a25e5adb47a067af137615c17ce43316", "pi05-b1"):
+        round(5213836.671875 * 1024 * 1.9997987949630083 + 2469905.1875 * 1024),
 }
 
 
 def kernel_source_hash():
-    """sha256 of the single-launch kernel's code: the source with its comments
-    and whitespace removed, so that the recorded traffic stays attached to the
-    code it was measured on and nothing else."""
+    """sha256 of the single-launch kernel's code: its source and the device
+    headers it includes, with comments and whitespace removed, so that the
+    recorded traffic stays attached to the code it was measured on and nothing
+    else."""
     import hashlib
     import re
-    with open(os.path.join(ROOT, "paper_2607_12659_amd", "csrc", "jpi_persist.hip")) as f:
-        src = f.read()
+    src = ""
+    for name in ("jpi_persist.hip", "jpi_device.h", "jpi_internal.h"):
+        with open(os.path.join(ROOT, "paper_2607_12659_amd", "csrc", name)) as f:
+            src += f.read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     src = re.sub(r"//[^\n]*", "", src)
     return hashlib.sha256("".join(src.split()).encode()).hexdigest()

@@ -26,17 +26,6 @@ namespace jpi {
 // then writes slice z's partial sums to out_f32 + z*M*N; a separate row kernel
 // sums the slices in order (no cross-workgroup signalling inside a GEMM).
 // ===========================================================================
-// GELU (tanh form) through the identity 0.5 z (1 + tanh(u)) = z / (1 + 2^(-2u
-// log2 e)): one exp2 and one reciprocal instead of the library tanh (which
-// made the GeGLU epilogue of a 256 x 256 tile cost more than its last K
-// slices); relative error about 2e-6, below the bf16 rounding of its result.
-// Saturates correctly: the exponential overflows to inf (result -0) for large
-// negative z and underflows to 0 (result z) for large positive z.
-__device__ __forceinline__ float gelu_tanh_fast(float z) {
-  const float u2 = 2.f * 0.7978845608028654f * (z + 0.044715f * z * z * z);
-  return z * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-1.4426950408889634f * u2));
-}
-
 template <typename T, EpiKind EPI>
 __device__ __forceinline__ void epilogue_pair(const EpiParams& ep, float* out_f32, int M, int N, int row, int col_lo,
                                               float lo, float hi) {
@@ -52,7 +41,7 @@ __device__ __forceinline__ void epilogue_pair(const EpiParams& ep, float* out_f3
   } else if constexpr (EPI == EPI_GEGLU) {
     // packed group t of 32 columns: [gate f = 16t + c | up f = 16t + c]
     const int f = (col_lo >> 5) * 16 + (col_lo & 15);
-    reinterpret_cast<T*>(ep.z)[(size_t)row * ep.mlp_dim + f] = from_f32<T>(gelu_tanh_fast(lo) * hi);
+    reinterpret_cast<T*>(ep.z)[(size_t)row * ep.mlp_dim + f] = from_f32<T>(gelu_tanh(lo) * hi);
   } else if constexpr (EPI == EPI_QKV) {
     const int Dh = ep.head_dim, half = Dh >> 1, H = ep.horizon;
     const int b = row / H, i = row - b * H;
