@@ -99,8 +99,11 @@ struct FlashSrc {
 // st * 32 + 8g .. + 8; g = lane / 16, g' and e from lane % 16), the next VFR
 // are V^T fragments nt (dim nt * 16 + lane % 16, keys 8g .. + 8).  The
 // per-lane part of each address (koff, vaoff, vpoff) is fixed for the
-// launch; the per-fragment part and the block's first key go in the scalar
-// offset.  Returns the block's valid key count (>= 1).
+// launch; the per-fragment part and the block's first key are added to it,
+// so that the whole offset is range-checked (an offset in the scalar
+// operand is not part of the buffer's range check): K rows past the last
+// valid key read as zero and nothing past the source is touched.  Returns
+// the block's valid key count (>= 1).
 template <int DH>
 __device__ __forceinline__ int flash_issue(lds_t* stage, const FlashSrc& src, int jb, u32 koff, u32 vaoff, u32 vpoff,
                                            int vst_ld, int vpt_ld) {
@@ -117,12 +120,12 @@ __device__ __forceinline__ int flash_issue(lds_t* stage, const FlashSrc& src, in
     const int fi = w + FS::NW * u;
     if (FS::is_k(w, u)) {
       const int kt = fi / FS::NST, st = fi - kt * FS::NST;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, stage + fi * 1024, 16, koff,
-                                               (u32)(((key0 + 4 * kt) * DH + st * 32) * 2), 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, stage + fi * 1024, 16,
+                                               koff + (u32)(((key0 + 4 * kt) * DH + st * 32) * 2), 0, 0, 0);
     } else {
       const int nt = fi - FS::KFR;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, stage + fi * 1024, 16, voff, (u32)((nt * 16 * vld + key0) * 2),
-                                               0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, stage + fi * 1024, 16, voff + (u32)((nt * 16 * vld + key0) * 2),
+                                               0, 0, 0);
     }
   }
   const int n = (act ? src.H : src.pl) - key0;
