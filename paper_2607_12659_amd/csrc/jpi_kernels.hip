@@ -69,6 +69,45 @@ __device__ __forceinline__ void epilogue_pair(const EpiParams& ep, float* out_f3
   }
 }
 
+// Rotation factors of an EPI_QKV result pair (row, col_lo), or (1, 0) where
+// none applies (V columns, rows past M).  They do not depend on the product,
+// so a kernel can load them before its K loop and pass them to the epilogue.
+__device__ __forceinline__ float2 qkv_rope_factor(const EpiParams& ep, int M, int N, int row, int col_lo) {
+  const int Dh = ep.head_dim, qcols = ep.n_heads * Dh;
+  if (row >= M || col_lo >= N || col_lo >= qcols + Dh) return float2{1.f, 0.f};
+  const int hn = col_lo < qcols ? col_lo / Dh : -1;
+  const int within = col_lo < qcols ? col_lo - hn * Dh : col_lo - qcols;
+  const int d = (within >> 5) * 16 + (within & 15);
+  return ep.rope[(size_t)row * (Dh >> 1) + d];  // row = b * H + i
+}
+
+// EPI_QKV epilogue with the rotation factors already in hand
+template <typename T>
+__device__ __forceinline__ void epilogue_qkv_pre(const EpiParams& ep, int M, int N, int row, int col_lo, float lo,
+                                                 float hi, float2 cs) {
+  if (row >= M || col_lo >= N) return;
+  const int Dh = ep.head_dim, half = Dh >> 1, H = ep.horizon;
+  const int b = row / H, i = row - b * H;
+  const int qcols = ep.n_heads * Dh;
+  if (col_lo < qcols + Dh) {
+    const int hn = col_lo < qcols ? col_lo / Dh : -1;
+    const int within = col_lo < qcols ? col_lo - hn * Dh : col_lo - qcols;
+    const int d = (within >> 5) * 16 + (within & 15);
+    const float r_lo = lo * cs.x - hi * cs.y;
+    const float r_hi = lo * cs.y + hi * cs.x;
+    const size_t kbs = ep.ks_bstride ? (size_t)ep.ks_bstride : (size_t)H * Dh;
+    T* dst = hn >= 0 ? reinterpret_cast<T*>(ep.q) + (((size_t)b * ep.n_heads + hn) * H + i) * Dh
+                     : reinterpret_cast<T*>(ep.ks) + b * kbs + (size_t)i * Dh;
+    dst[d] = from_f32<T>(r_lo);
+    dst[d + half] = from_f32<T>(r_hi);
+  } else {
+    const int within = col_lo - qcols - Dh;
+    T* dst = reinterpret_cast<T*>(ep.vst) + (size_t)b * Dh * ep.vst_ld + i;
+    dst[(size_t)within * ep.vst_ld] = from_f32<T>(lo);
+    dst[(size_t)(within + 16) * ep.vst_ld] = from_f32<T>(hi);
+  }
+}
+
 // ---- tiled GEMM for M > 64: workgroup tile BM x BN, 4 waves in 2 x 2, K
 // staged through LDS in BK slices with register double buffering.  An LDS
 // row is one 128-byte slice row (8 chunks of 16 bytes); chunk c of row r is
@@ -187,16 +226,18 @@ __global__ __launch_bounds__(256) void k_gemm(GemmLaunch g) {
 // (wave tile 128 x 64), the same swizzled 128-byte LDS rows and register
 // double buffering as k_gemm.  A K slice moves 64 KB for four times the
 // products of a 128 x 128 tile, half the bytes per product. ------------------
+template <int BM_, int BN_>
 struct BigShape {
-  static constexpr int BM = 256, BN = 256, BK = 64, VEC = 8, CPR = 8, NT = 512;
-  static constexpr int WM = 128, WN = 64, TM = WM / 16, TN = WN / 16;
+  static constexpr int BM = BM_, BN = BN_, BK = 64, VEC = 8, CPR = 8, NT = 512;
+  static constexpr int WM = BM / 2, WN = BN / 4, TM = WM / 16, TN = WN / 16;
   static constexpr int A_CH = BM * CPR / NT, W_CH = BN * CPR / NT;  // 16-byte chunks per thread
+  static_assert(A_CH >= 1 && W_CH >= 1 && TN % 2 == 0, "tile shape");
   static __device__ __forceinline__ int at(int r, int c) { return r * BK + ((c ^ ((r >> 1) & 7)) * VEC); }
 };
+typedef BigShape<256, 256> Big256;
 
-template <EpiKind EPI>
+template <typename S, EpiKind EPI>
 __global__ __launch_bounds__(512) void k_gemm_big(GemmLaunch g) {
-  using S = BigShape;
   using MF = Mfma<bf16>;
   __shared__ __attribute__((aligned(16))) bf16 As[2][S::BM * S::BK];
   __shared__ __attribute__((aligned(16))) bf16 Ws[2][S::BN * S::BK];
@@ -363,6 +404,20 @@ __global__ __launch_bounds__(S::NT) void k_gemm_dma(GemmLaunch g) {
 #pragma unroll
     for (int b = 0; b < S::TN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int fr = lane & 15, fc = lane >> 4;  // fragment row, 16-byte K chunk within a 32-deep step
+  const int rbase = m0 + wm * S::WM + (lane >> 4) * 4;
+  const int cbase = n0 + wn * S::WN + fr;
+  // QKV: the rotation factors of every result pair, loaded before the K loop
+  // (where they fit in registers: up to 16 result tiles per wave)
+  constexpr bool PRE = EPI == EPI_QKV && S::TM * S::TN <= 16;
+  float2 rope[PRE ? S::TM : 1][PRE ? S::TN / 2 : 1][4];
+  if constexpr (PRE) {
+#pragma unroll
+    for (int a = 0; a < S::TM; ++a)
+#pragma unroll
+      for (int b = 0; b < S::TN; b += 2)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rope[a][b / 2][i] = qkv_rope_factor(g.ep, M, N, rbase + a * 16 + i, cbase + b * 16);
+  }
 
 #pragma unroll
   for (int s = 0; s < S::NS - 1; ++s)
@@ -398,22 +453,28 @@ __global__ __launch_bounds__(S::NT) void k_gemm_dma(GemmLaunch g) {
     }
   }
 
-  const int rbase = m0 + wm * S::WM + (lane >> 4) * 4;
-  const int cbase = n0 + wn * S::WN + fr;
   float* out = g.ep.out_f32 ? g.ep.out_f32 + (size_t)blockIdx.z * M * N : nullptr;
 #pragma unroll
   for (int a = 0; a < S::TM; ++a)
 #pragma unroll
     for (int b = 0; b < S::TN; b += 2)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        epilogue_pair<bf16, EPI>(g.ep, out, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i], acc[a][b + 1][i]);
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (PRE)
+          epilogue_qkv_pre<bf16>(g.ep, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i], acc[a][b + 1][i],
+                                 rope[a][b / 2][i]);
+        else
+          epilogue_pair<bf16, EPI>(g.ep, out, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i],
+                                   acc[a][b + 1][i]);
+      }
 }
 
 typedef DmaShape<128, 128, 4, 64> DmaMid;   // one slice: 32 KB; ring 128 KB (a 256 x 256, 8-wave, 32-deep
                                             // shape fits the same ring; slower at M = 3200 than two
                                             // register-staged workgroups per unit)
 typedef DmaShape<64, 64, 4, 64> DmaSmall;   // one slice: 16 KB; ring 64 KB (two workgroups per unit)
+typedef DmaShape<128, 256, 8, 32> DmaWide;  // one slice: 24 KB; ring 96 KB
+typedef DmaShape<256, 256, 8, 32> DmaBig;   // one slice: 32 KB; ring 128 KB
 
 template <typename S>
 static hipError_t launch_dma(const GemmLaunch& g, hipStream_t s) {
@@ -434,12 +495,13 @@ static bool gemm_pipe_enabled() {
   return on != 0;
 }
 
+template <typename S>
 static hipError_t launch_big(const GemmLaunch& g, hipStream_t s) {
-  dim3 grid((g.N + BigShape::BN - 1) / BigShape::BN, (g.M + BigShape::BM - 1) / BigShape::BM, g.splitk);
+  dim3 grid((g.N + S::BN - 1) / S::BN, (g.M + S::BM - 1) / S::BM, g.splitk);
   switch (g.epi) {
-    case EPI_STORE_F32: JPI_LAUNCH((k_gemm_big<EPI_STORE_F32>), grid, dim3(512), 0, s, g.ev_start, g.ev_stop, g); break;
-    case EPI_QKV: JPI_LAUNCH((k_gemm_big<EPI_QKV>), grid, dim3(512), 0, s, g.ev_start, g.ev_stop, g); break;
-    case EPI_GEGLU: JPI_LAUNCH((k_gemm_big<EPI_GEGLU>), grid, dim3(512), 0, s, g.ev_start, g.ev_stop, g); break;
+    case EPI_STORE_F32: JPI_LAUNCH((k_gemm_big<S, EPI_STORE_F32>), grid, dim3(512), 0, s, g.ev_start, g.ev_stop, g); break;
+    case EPI_QKV: JPI_LAUNCH((k_gemm_big<S, EPI_QKV>), grid, dim3(512), 0, s, g.ev_start, g.ev_stop, g); break;
+    case EPI_GEGLU: JPI_LAUNCH((k_gemm_big<S, EPI_GEGLU>), grid, dim3(512), 0, s, g.ev_start, g.ev_stop, g); break;
   }
   return hipGetLastError();
 }
@@ -602,7 +664,16 @@ hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s) {
     if (gemm_pipe_enabled() && g.M <= 512 && tiles(128, 128) < n_cu && g.splitk == 1 && g.K % DmaSmall::BK == 0 &&
         (size_t)g.N * g.K * 2 < (1u << 31))
       return launch_dma<DmaSmall>(g, s);
-    if (tiles(256, 256) >= n_cu) return launch_big(g, s);
+    // Larger M: 256 x 256 tiles on the direct-to-LDS ring (three 32-deep slices in flight) when such
+    // tiles alone cover the units (GateUp at M = 3200: 71.5 -> 68.1 us against the register-staged
+    // k_gemm_big), else one round of 128 x 256 ring tiles when they fill at least three quarters of the
+    // units (M = 3200: QKV 39.6 -> 38.1, split-K O-proj 29.0 -> 25.6 and Down 48.6 -> 42.8 us against two
+    // register-staged 128 x 128 workgroups per unit; register-staged 128 x 256 tiles were slower than both)
+    const bool fits = (size_t)g.N * g.K * 2 < (1u << 31) && (size_t)g.M * g.K * 2 < (1u << 31) &&
+                      (g.K / g.splitk) % 32 == 0;
+    if (fits && tiles(256, 256) >= n_cu) return launch_dma<DmaBig>(g, s);
+    if (tiles(256, 256) >= n_cu) return launch_big<Big256>(g, s);
+    if (fits && tiles(128, 256) <= n_cu && 4 * tiles(128, 256) >= 3 * n_cu) return launch_dma<DmaWide>(g, s);
     if (tiles(128, 128) >= n_cu || g.epi == EPI_STORE_F32) return launch_gemm_t<bf16, 128, 128>(g, s);
     if (tiles(128, 64) >= n_cu) return launch_gemm_t<bf16, 128, 64>(g, s);
     return launch_gemm_t<bf16, 64, 64>(g, s);

@@ -56,7 +56,8 @@ def test_gemm_bf16(M, N, K, splitk):
 
 
 @pytest.mark.parametrize("M,N,K,splitk", [(50, 1024, 4096, 16), (50, 2560, 1024, 4), (3200, 8192, 1024, 1),
-                                          (200, 200, 192, 3)])
+                                          (200, 200, 192, 3), (3200, 2560, 1024, 1), (3200, 1024, 4096, 2),
+                                          (816, 2048, 2048, 4)])
 def test_gemm_bf16_more_shapes(M, N, K, splitk):
     from paper_2607_12659_amd import jpi
     rng = np.random.default_rng(M + N + K)
