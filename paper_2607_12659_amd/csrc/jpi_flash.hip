@@ -260,7 +260,7 @@ __device__ __forceinline__ void flash_compute(const char* cur, int n_valid,
 // hands workgroup i to XCD i % 8, so item (i % 8) * (grid / 8) + i / 8 puts
 // consecutive items, which share a rollout's keys and values, in one XCD's L2.
 template <int DH>
-__global__ __launch_bounds__(512) void k_flash(AttnLaunch a, int S, int nqt, void* part, float2* ml) {
+__global__ __launch_bounds__(512) void k_flash(AttnLaunch a, int S, int nqt, int qrows, void* part, float2* ml) {
   using FS = Flash<DH>;
   using MF = Mfma<bf16>;
   constexpr int NST = FS::NST, NT = FS::NT, RT = FS::RT, NS = FS::NS, LDW = FS::LDW;
@@ -283,13 +283,14 @@ __global__ __launch_bounds__(512) void k_flash(AttnLaunch a, int S, int nqt, voi
   const int nb = src.nbs + (pl + FS::KB - 1) / FS::KB;
   const int jb0 = (int)((int64_t)split * nb / S), jb1 = (int)((int64_t)(split + 1) * nb / S);
   const int nblk = jb1 - jb0;
-  const int row0 = qt * FS::QT + w * 16 * RT;  // this wave's first query row
+  // this wave's first query row; tile qt holds rows [qt * qrows, (qt + 1) * qrows)
+  const int row0 = qt * qrows + w * 16 * RT;
 
   // each split writes its (max, sum) even when it has no keys
   if (nblk == 0) {
     if (S > 1) {
-      for (int t = threadIdx.x; t < FS::QT; t += FS::NW * 64) {
-        const int r = qt * FS::QT + t;
+      for (int t = threadIdx.x; t < qrows; t += FS::NW * 64) {
+        const int r = qt * qrows + t;
         if (r < R) ml[((size_t)split * a.B + b) * R + r] = float2{-INFINITY, 0.f};
       }
     }
@@ -314,7 +315,7 @@ __global__ __launch_bounds__(512) void k_flash(AttnLaunch a, int S, int nqt, voi
 #pragma unroll
     for (int st = 0; st < NST; ++st) qf[rt][st] = r < R ? MF::load(qb + (size_t)r * DH + st * 32 + 8 * g) : MF::frag{};
   }
-  const bool active = row0 < R;  // wave has query rows (uniform per wave)
+  const bool active = row0 < R && 16 * RT * w < qrows;  // wave has query rows of this tile (uniform per wave)
 
   lds_t* ring = (lds_t*)lds;
   // valid keys of the blocks in the ring, by stage.  The first NS - 1 blocks
@@ -463,14 +464,18 @@ int flash_splits(int B, int nH, int H, int P, int n_cu) {
 
 template <int DH>
 static hipError_t launch_flash_t(const AttnLaunch& a, int S, hipStream_t s) {
-  const int nqt = (a.nH * a.H + Flash<DH>::QT - 1) / Flash<DH>::QT;
+  // ceil(rows / 128) tiles per rollout, the rows spread evenly in whole 16-row wave tiles (400 rows: four
+  // tiles of 112 instead of 128 + 128 + 128 + 16, so that the critical tiles keep seven waves busy)
+  const int R = a.nH * a.H;
+  const int nqt = (R + Flash<DH>::QT - 1) / Flash<DH>::QT;
+  const int qrows = ((R + nqt - 1) / nqt + 15) / 16 * 16;
   const size_t rows = (size_t)a.B * a.nH * a.H;
   // partial outputs (bf16) then (max, sum) pairs, inside the opart scratch
   void* part = a.opart;
   float2* ml = reinterpret_cast<float2*>(reinterpret_cast<char*>(a.opart) + (size_t)S * rows * DH * 2);
   const int items = a.B * nqt * S;
   JPI_LAUNCH((k_flash<DH>), dim3((items + 7) / 8 * 8), dim3(Flash<DH>::NW * 64), 0, s, a.ev_start,
-             S == 1 ? a.ev_stop : (hipEvent_t) nullptr, a, S, nqt, part, ml);
+             S == 1 ? a.ev_stop : (hipEvent_t) nullptr, a, S, nqt, qrows, part, ml);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || S == 1) return e;
   constexpr int RPB = 256 / (DH / 4);
