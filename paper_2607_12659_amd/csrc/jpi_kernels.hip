@@ -934,14 +934,21 @@ __global__ __launch_bounds__(256) void k_resid_norm_row(RowLaunch r) {
 // Non-final residual + norm with one wave per row (four rows per workgroup):
 // the row's sum of squares is a wave reduction, so no workgroup barrier.
 // Same per-element arithmetic as k_resid_norm (slices summed in order).
-template <typename T>
+template <typename T, int NJ>
 __global__ __launch_bounds__(256) void k_resid_norm_wave(RowLaunch r) {
-  constexpr int NJ = ROW_MAX_W / 256;  // four columns per lane per pass
+  // A wave per row, W <= 256 NJ.  Every load of the row (up to RW_SLICES
+  // split-K slices, the residual and the gate) is issued before any
+  // arithmetic or store: written pass by pass, with the slice count and the
+  // row end as runtime loop bounds, each 256-column pass waited a memory
+  // round trip for the previous one.  y leaves as 4 packed values per lane.
+  constexpr int RW_SLICES = 4;
   const int lane = threadIdx.x & 63, m = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (m >= r.M) return;
   const int W = r.W, S = r.S;
   const size_t MW = (size_t)r.M * W;
-  const float *gate = r.gate, *scale = r.scale, *shift = r.shift;
+  const float* __restrict__ gate = r.gate;
+  const float* __restrict__ scale = r.scale;
+  const float* __restrict__ shift = r.shift;
   if (r.n_t0 > 0) {  // committed rows at t = 0: the t = 0 table row
     const int ia = m % (r.n_lead + r.horizon) - r.n_lead;
     if (ia >= 0 && ia < r.n_t0) {
@@ -950,30 +957,52 @@ __global__ __launch_bounds__(256) void k_resid_norm_wave(RowLaunch r) {
       shift += r.t0_delta;
     }
   }
-  float* hr = r.h + (size_t)m * W;
-  const float* pr = r.part + (size_t)m * W;
-  f32x4 hv[NJ];
+  float* __restrict__ hr = r.h + (size_t)m * W;
+  const float* __restrict__ pr = r.part + (size_t)m * W;
+  // columns past W read column 0 (in range) and are then ignored
+  int kk[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) kk[j] = 4 * lane + 256 * j < W ? 4 * lane + 256 * j : 0;
+  f32x4 pv[RW_SLICES][NJ], hv[NJ], gv[NJ];
+#pragma unroll
+  for (int z = 0; z < RW_SLICES; ++z)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      pv[z][j] = z < S ? *reinterpret_cast<const f32x4*>(pr + z * MW + kk[j]) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    hv[j] = *reinterpret_cast<const f32x4*>(hr + kk[j]);
+    gv[j] = *reinterpret_cast<const f32x4*>(gate + kk[j]);
+  }
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
-    const int k = 4 * lane + 256 * j;
-    if (k >= W) break;
-    f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int z = 0; z < S; ++z) sum += *reinterpret_cast<const f32x4*>(pr + z * MW + k);
-    const f32x4 h2 = *reinterpret_cast<const f32x4*>(hr + k) + *reinterpret_cast<const f32x4*>(gate + k) * sum;
-    *reinterpret_cast<f32x4*>(hr + k) = h2;
-    hv[j] = h2;
-    ss += h2[0] * h2[0] + h2[1] * h2[1] + h2[2] * h2[2] + h2[3] * h2[3];
+    f32x4 sum = pv[0][j];
+#pragma unroll
+    for (int z = 1; z < RW_SLICES; ++z) sum += pv[z][j];  // zero past S: the same sum in the same order
+    for (int z = RW_SLICES; z < S; ++z) sum += *reinterpret_cast<const f32x4*>(pr + z * MW + kk[j]);
+    hv[j] += gv[j] * sum;
+    if (4 * lane + 256 * j < W) ss += hv[j][0] * hv[j][0] + hv[j][1] * hv[j][1] + hv[j][2] * hv[j][2] + hv[j][3] * hv[j][3];
   }
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    if (4 * lane + 256 * j < W) *reinterpret_cast<f32x4*>(hr + kk[j]) = hv[j];
   const float rs = 1.0f / sqrtf(wave_sum(ss) / (float)W + r.eps);
-  T* yr = reinterpret_cast<T*>(r.y) + (size_t)m * W;
+  T* __restrict__ yr = reinterpret_cast<T*>(r.y) + (size_t)m * W;
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
-    const int k = 4 * lane + 256 * j;
-    if (k >= W) break;
+    if (4 * lane + 256 * j >= W) continue;
+    const int k = kk[j];
     const f32x4 sc = *reinterpret_cast<const f32x4*>(scale + k), sh = *reinterpret_cast<const f32x4*>(shift + k);
+    T v4[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) yr[k + e] = from_f32<T>(hv[j][e] * rs * (1.0f + sc[e]) + sh[e]);
+    for (int e = 0; e < 4; ++e) v4[e] = from_f32<T>(hv[j][e] * rs * (1.0f + sc[e]) + sh[e]);
+    if constexpr (sizeof(T) == 2) {
+      typedef T t4 __attribute__((ext_vector_type(4)));
+      *reinterpret_cast<t4*>(yr + k) = t4{v4[0], v4[1], v4[2], v4[3]};
+    } else {
+      *reinterpret_cast<f32x4*>(yr + k) = f32x4{v4[0], v4[1], v4[2], v4[3]};
+    }
   }
 }
 
@@ -1003,11 +1032,15 @@ hipError_t launch_resid_norm(jpi_dtype dt, const RowLaunch& r, bool final_step, 
   const dim3 wave_grid((r.M + 3) / 4);
   if (dt == JPI_BF16) {
     if (final_step) hipLaunchKernelGGL((k_resid_norm<bf16, true>), dim3(r.M), dim3(256), 0, s, r);
-    else if (wave_rows) hipLaunchKernelGGL(k_resid_norm_wave<bf16>, wave_grid, dim3(256), 0, s, r);
+    else if (wave_rows && r.W <= 1024) hipLaunchKernelGGL((k_resid_norm_wave<bf16, 4>), wave_grid, dim3(256), 0, s, r);
+    else if (wave_rows && r.W <= 2048) hipLaunchKernelGGL((k_resid_norm_wave<bf16, 8>), wave_grid, dim3(256), 0, s, r);
+    else if (wave_rows) hipLaunchKernelGGL((k_resid_norm_wave<bf16, 16>), wave_grid, dim3(256), 0, s, r);
     else hipLaunchKernelGGL(k_resid_norm_row<bf16>, dim3(r.M), dim3(256), 0, s, r);
   } else {
     if (final_step) hipLaunchKernelGGL((k_resid_norm<float, true>), dim3(r.M), dim3(256), 0, s, r);
-    else if (wave_rows) hipLaunchKernelGGL(k_resid_norm_wave<float>, wave_grid, dim3(256), 0, s, r);
+    else if (wave_rows && r.W <= 1024) hipLaunchKernelGGL((k_resid_norm_wave<float, 4>), wave_grid, dim3(256), 0, s, r);
+    else if (wave_rows && r.W <= 2048) hipLaunchKernelGGL((k_resid_norm_wave<float, 8>), wave_grid, dim3(256), 0, s, r);
+    else if (wave_rows) hipLaunchKernelGGL((k_resid_norm_wave<float, 16>), wave_grid, dim3(256), 0, s, r);
     else hipLaunchKernelGGL(k_resid_norm_row<float>, dim3(r.M), dim3(256), 0, s, r);
   }
   return hipGetLastError();
