@@ -45,7 +45,12 @@ def build_all(verbose: bool = False):
     sys.path.insert(0, ROOT)
     import synth
     synth.build_lib(force=True)
-    return build_libjpi(verbose)
+    lib = build_libjpi(verbose)
+    # the two standalone microbenchmarks (link chains, L2 / HBM read rates)
+    from paper_2607_12659_amd import l2bench, linkbench
+    linkbench.build()
+    l2bench.build()
+    return lib
 
 
 if __name__ == "__main__":

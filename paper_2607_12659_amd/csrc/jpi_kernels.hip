@@ -333,18 +333,15 @@ __global__ __launch_bounds__(512) void k_gemm_big(GemmLaunch g) {
 // the bank swizzle is applied through the global addresses: LDS slot s of
 // tile row r holds K chunk s ^ f(r).  Rows past M (or N) lie outside the
 // buffer range and load as zero. ----------------------------------------------
-template <int BM_, int BN_, int NW_, int BK_, int NS_ = 4, bool M32_ = false>
+template <int BM_, int BN_, int NW_, int BK_, int NS_ = 4, int WGM_ = 2>
 struct DmaShape {
   static constexpr int BM = BM_, BN = BN_, NW = NW_, BK = BK_, NS = NS_;
-  // products on 32 x 32 x 16 instead of 16 x 16 x 32 MFMAs (with one wave per SIMD the former sustain
-  // about 33 clocks per instruction, twice the work of a 16 x 16 x 32 one at about 47 clocks)
-  static constexpr bool M32 = M32_;
   static constexpr int NT = 64 * NW;
   static constexpr int VEC = 8;                       // bf16 per 16-byte chunk
   static constexpr int CPR = BK / VEC;                // chunks per tile row: 8 (BK 64) or 4 (BK 32)
   static constexpr int RPI = 64 / CPR;                // tile rows per 1 KB load instruction
-  static constexpr int WGN = NW / 2;                  // wave grid 2 x WGN
-  static constexpr int WM = BM / 2, WN = BN / WGN;
+  static constexpr int WGM = WGM_, WGN = NW / WGM;    // wave grid WGM x WGN
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int TM = WM / 16, TN = WN / 16;
   static constexpr int A_INS = BM / RPI, W_INS = BN / RPI;
   static constexpr int INS = (A_INS + W_INS) / NW;    // load instructions per wave per stage
@@ -352,8 +349,6 @@ struct DmaShape {
   static_assert((A_INS + W_INS) % NW == 0, "load instructions split evenly over the waves");
   static_assert(CPR == 8 || CPR == 4, "swizzle defined for 64- and 32-deep slices");
   static_assert(TN % 2 == 0, "epilogues pair n-subtiles 2t and 2t+1");
-  static_assert(!M32 || (WM % 32 == 0 && WN % 64 == 0), "32 x 32 tiles in pairs along n");
-  static constexpr int TM32 = WM / 32, TN32 = WN / 32;
   // LDS slot of chunk c in row r (an involution: also the chunk held by slot c)
   static __device__ __forceinline__ int swz(int r, int c) {
     // 64-byte rows (32-deep slices): the row pairs of a 128-byte bank window share the permutation.
@@ -426,38 +421,25 @@ __global__ __launch_bounds__(S::NT) void k_gemm_dma(GemmLaunch g) {
   const int M = g.M, N = g.N, K = g.K;
   const int kper = K / g.splitk, kbeg = blockIdx.z * kper, nkt = kper / S::BK;
   const int lr = lane / S::CPR, ls = lane % S::CPR;
-  // Result tiles per wave: AT x BT of 16 x 16 (4 values per lane) or of 32 x 32 (16 values per lane).
-  // 16 x 16: lane l holds column l % 16 of rows 4 (l / 16) + i.  32 x 32: lane l holds MFMA column
-  // l % 32 of rows 8 (i / 4) + 4 (l / 32) + i % 4; tile pair (2t, 2t + 1) covers 64 output columns and
-  // its MFMA column j stands for output column 64t + 16h + (j < 16 ? j : j + 16) (h = tile parity), so
-  // a lane holds the two columns 16 apart that the epilogues combine.
-  constexpr bool W32 = S::M32;
-  constexpr int AT = W32 ? S::TM32 : S::TM, BT = W32 ? S::TN32 : S::TN, NR = W32 ? 16 : 4;
-  typedef float accv __attribute__((ext_vector_type(NR)));
-  accv acc[AT][BT];
+  f32x4 acc[S::TM][S::TN];
 #pragma unroll
-  for (int a = 0; a < AT; ++a)
+  for (int a = 0; a < S::TM; ++a)
 #pragma unroll
-    for (int b = 0; b < BT; ++b)
-#pragma unroll
-      for (int i = 0; i < NR; ++i) acc[a][b][i] = 0.f;
-  const int pc = W32 ? ((lane & 31) < 16 ? (lane & 31) : (lane & 31) + 16) : (lane & 15);
-  auto res_row = [&](int a, int i) -> int {
-    if constexpr (W32) return m0 + wm * S::WM + a * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-    else return m0 + wm * S::WM + a * 16 + 4 * (lane >> 4) + i;
-  };
-  auto res_col = [&](int t) -> int { return n0 + wn * S::WN + (W32 ? 64 : 32) * t + pc; };
+    for (int b = 0; b < S::TN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int fr = lane & 15, fc = lane >> 4;  // fragment row, 16-byte K chunk within a 32-deep step
+  const int rbase = m0 + wm * S::WM + (lane >> 4) * 4;
+  const int cbase = n0 + wn * S::WN + fr;
   // QKV: the rotation factors of every result pair, loaded before the K loop
-  // (where they fit in registers: up to 64 result values per lane)
-  constexpr bool PRE = EPI == EPI_QKV && AT * BT * NR <= 64;
-  float2 rope[PRE ? AT : 1][PRE ? BT / 2 : 1][PRE ? NR : 1];
+  // (where they fit in registers: up to 16 result tiles per wave)
+  constexpr bool PRE = EPI == EPI_QKV && S::TM * S::TN <= 16;
+  float2 rope[PRE ? S::TM : 1][PRE ? S::TN / 2 : 1][4];
   if constexpr (PRE) {
 #pragma unroll
-    for (int a = 0; a < AT; ++a)
+    for (int a = 0; a < S::TM; ++a)
 #pragma unroll
-      for (int t = 0; t < BT / 2; ++t)
+      for (int b = 0; b < S::TN; b += 2)
 #pragma unroll
-        for (int i = 0; i < NR; ++i) rope[a][t][i] = qkv_rope_factor(g.ep, M, N, res_row(a, i), res_col(t));
+        for (int i = 0; i < 4; ++i) rope[a][b / 2][i] = qkv_rope_factor(g.ep, M, N, rbase + a * 16 + i, cbase + b * 16);
   }
 
 #pragma unroll
@@ -470,71 +452,48 @@ __global__ __launch_bounds__(S::NT) void k_gemm_dma(GemmLaunch g) {
     if (kt + S::NS - 1 < nkt) dma_issue<S>(g, ring, wave, lr, ls, m0, n0, kbeg, kt + S::NS - 1);
     const lds_t* As = (const lds_t*)ring + (kt % S::NS) * (S::STAGE * 2);
     const lds_t* Ws = As + S::BM * S::BK * 2;
-    if constexpr (W32) {
 #pragma unroll
-      for (int kk = 0; kk < S::BK; kk += 16) {
-        const int c = kk / S::VEC + (lane >> 5);  // 16-byte K chunk of this lane
-        MF::frag af[AT], bfr[BT];
+    for (int kk = 0; kk < S::BK; kk += MF::KSUB) {
+      const int c = kk / S::VEC + fc;
+      MF::frag af[S::TM], bfr[S::TN];
 #pragma unroll
-        for (int a = 0; a < AT; ++a) {
-          const int r = wm * S::WM + a * 32 + (lane & 31);
-          af[a] = *(lds_frag*)(As + (r * S::BK + S::swz(r, c) * S::VEC) * 2);
-        }
-#pragma unroll
-        for (int b = 0; b < BT; ++b) {
-          const int r = wn * S::WN + (b >> 1) * 64 + (b & 1) * 16 + pc;
-          bfr[b] = *(lds_frag*)(Ws + (r * S::BK + S::swz(r, c) * S::VEC) * 2);
-        }
-#pragma unroll
-        for (int a = 0; a < AT; ++a)
-#pragma unroll
-          for (int b = 0; b < BT; ++b)
-            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
+      for (int a = 0; a < S::TM; ++a) {
+        const int r = wm * S::WM + a * 16 + fr;
+        af[a] = *(lds_frag*)(As + (r * S::BK + S::swz(r, c) * S::VEC) * 2);
       }
-    } else {
-      const int fr = lane & 15, fc = lane >> 4;  // fragment row, 16-byte K chunk within a 32-deep step
 #pragma unroll
-      for (int kk = 0; kk < S::BK; kk += MF::KSUB) {
-        const int c = kk / S::VEC + fc;
-        MF::frag af[AT], bfr[BT];
-#pragma unroll
-        for (int a = 0; a < AT; ++a) {
-          const int r = wm * S::WM + a * 16 + fr;
-          af[a] = *(lds_frag*)(As + (r * S::BK + S::swz(r, c) * S::VEC) * 2);
-        }
-#pragma unroll
-        for (int b = 0; b < BT; ++b) {
-          const int r = wn * S::WN + b * 16 + fr;
-          bfr[b] = *(lds_frag*)(Ws + (r * S::BK + S::swz(r, c) * S::VEC) * 2);
-        }
-#pragma unroll
-        for (int a = 0; a < AT; ++a)
-#pragma unroll
-          for (int b = 0; b < BT; ++b) acc[a][b] = MF::run(af[a], bfr[b], acc[a][b]);
+      for (int b = 0; b < S::TN; ++b) {
+        const int r = wn * S::WN + b * 16 + fr;
+        bfr[b] = *(lds_frag*)(Ws + (r * S::BK + S::swz(r, c) * S::VEC) * 2);
       }
+#pragma unroll
+      for (int a = 0; a < S::TM; ++a)
+#pragma unroll
+        for (int b = 0; b < S::TN; ++b) acc[a][b] = MF::run(af[a], bfr[b], acc[a][b]);
     }
   }
 
   float* out = g.ep.out_f32 ? g.ep.out_f32 + (size_t)blockIdx.z * M * N : nullptr;
 #pragma unroll
-  for (int a = 0; a < AT; ++a)
+  for (int a = 0; a < S::TM; ++a)
 #pragma unroll
-    for (int t = 0; t < BT / 2; ++t)
+    for (int b = 0; b < S::TN; b += 2)
 #pragma unroll
-      for (int i = 0; i < NR; ++i) {
+      for (int i = 0; i < 4; ++i) {
         if constexpr (PRE)
-          epilogue_qkv_pre<bf16>(g.ep, M, N, res_row(a, i), res_col(t), acc[a][2 * t][i], acc[a][2 * t + 1][i],
-                                 rope[a][t][i]);
+          epilogue_qkv_pre<bf16>(g.ep, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i], acc[a][b + 1][i],
+                                 rope[a][b / 2][i]);
         else
-          epilogue_pair<bf16, EPI>(g.ep, out, M, N, res_row(a, i), res_col(t), acc[a][2 * t][i],
-                                   acc[a][2 * t + 1][i]);
+          epilogue_pair<bf16, EPI>(g.ep, out, M, N, rbase + a * 16 + i, cbase + b * 16, acc[a][b][i],
+                                   acc[a][b + 1][i]);
       }
 }
 
-typedef DmaShape<128, 128, 4, 64, 4, true> DmaMid;   // one slice: 32 KB; ring 128 KB (a 256 x 256, 8-wave, 32-deep
-                                            // shape fits the same ring; slower at M = 3200 than two
-                                            // register-staged workgroups per unit)
-typedef DmaShape<64, 64, 4, 64> DmaSmall;   // one slice: 16 KB; ring 64 KB (two workgroups per unit)
+// Every ring runs two waves per SIMD: with one, a wave's LDS reads and its MFMAs take turns (batch 8:
+// four waves on 128 x 128 tiles 14.23 ms per call, eight 13.51 ms; eight waves on 64 x 64 tiles 13.18 ms).
+typedef DmaShape<128, 128, 8, 64> DmaMid;          // one slice: 32 KB; ring 128 KB; waves 2 x 4 of 64 x 32
+typedef DmaShape<64, 64, 8, 64, 4, 4> DmaSmall;    // one slice: 16 KB; ring 64 KB (two workgroups per unit);
+                                                   // waves 4 x 2 of 16 x 32
 typedef DmaShape<128, 256, 8, 32> DmaWide;  // one slice: 24 KB; ring 96 KB
 typedef DmaShape<256, 256, 8, 32> DmaBig;   // one slice: 32 KB; ring 128 KB
 
