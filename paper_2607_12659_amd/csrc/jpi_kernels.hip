@@ -430,8 +430,9 @@ __global__ __launch_bounds__(S::NT) void k_gemm_dma(GemmLaunch g) {
   const int rbase = m0 + wm * S::WM + (lane >> 4) * 4;
   const int cbase = n0 + wn * S::WN + fr;
   // QKV: the rotation factors of every result pair, loaded before the K loop
-  // (where they fit in registers: up to 16 result tiles per wave)
-  constexpr bool PRE = EPI == EPI_QKV && S::TM * S::TN <= 16;
+  // where they fit in registers beside the accumulators (as many again: up to
+  // 16 result tiles per wave at eight waves per workgroup, 8 at sixteen)
+  constexpr bool PRE = EPI == EPI_QKV && S::TM * S::TN * S::NW <= 128;
   float2 rope[PRE ? S::TM : 1][PRE ? S::TN / 2 : 1][4];
   if constexpr (PRE) {
 #pragma unroll
@@ -489,13 +490,17 @@ __global__ __launch_bounds__(S::NT) void k_gemm_dma(GemmLaunch g) {
       }
 }
 
-// Every ring runs two waves per SIMD: with one, a wave's LDS reads and its MFMAs take turns (batch 8:
-// four waves on 128 x 128 tiles 14.23 ms per call, eight 13.51 ms; eight waves on 64 x 64 tiles 13.18 ms).
+// Every ring runs at least two waves per SIMD: with one, a wave's LDS reads and its MFMAs take turns
+// (batch 8: four waves on 128 x 128 tiles 14.23 ms per call, eight 13.51 ms; eight waves on 64 x 64 tiles
+// 13.18 ms).
 typedef DmaShape<128, 128, 8, 64> DmaMid;          // one slice: 32 KB; ring 128 KB; waves 2 x 4 of 64 x 32
 typedef DmaShape<64, 64, 8, 64, 4, 4> DmaSmall;    // one slice: 16 KB; ring 64 KB (two workgroups per unit);
                                                    // waves 4 x 2 of 16 x 32
-typedef DmaShape<128, 256, 8, 32> DmaWide;  // one slice: 24 KB; ring 96 KB
-typedef DmaShape<256, 256, 8, 32> DmaBig;   // one slice: 32 KB; ring 128 KB
+typedef DmaShape<128, 256, 16, 64, 3, 4> DmaWide;  // one slice: 48 KB; ring 144 KB; waves 4 x 4 of 32 x 64
+                                                  // (batch 64 48.62 -> 45.89 ms against eight waves on
+                                                  // four 32-deep slices)
+typedef DmaShape<256, 256, 16, 32, 4, 4> DmaBig;   // one slice: 32 KB; ring 128 KB; waves 4 x 4 of 64 x 64
+                                                 // (four per SIMD: batch 64 48.28 -> 47.31 ms against eight)
 
 template <typename S>
 static hipError_t launch_dma(const GemmLaunch& g, hipStream_t s) {
@@ -685,20 +690,22 @@ hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s) {
     if (gemm_pipe_enabled() && g.M <= 512 && tiles(128, 128) < n_cu && g.splitk == 1 && g.K % DmaSmall::BK == 0 &&
         (size_t)g.N * g.K * 2 < (1u << 31))
       return launch_dma<DmaSmall>(g, s);
-    // Larger M: 256 x 256 tiles on the direct-to-LDS ring (three 32-deep slices in flight) when such
-    // tiles alone cover the units (GateUp at M = 3200: 71.5 -> 68.1 us against the register-staged
-    // k_gemm_big), else one round of 128 x 256 ring tiles when they fill at least three quarters of the
-    // units (M = 3200: QKV 39.6 -> 38.1, split-K O-proj 29.0 -> 25.6 and Down 48.6 -> 42.8 us against two
+    // Larger M: 256 x 256 tiles on the direct-to-LDS ring (three 32-deep slices in flight, sixteen
+    // waves) when such tiles alone cover the units (GateUp at M = 3200: 71.5 -> 68.1 us against the
+    // register-staged k_gemm_big with eight waves), else one round of 128 x 256 ring tiles (two 64-deep
+    // slices in flight, sixteen waves) when they fill at least three quarters of the units (M = 3200,
+    // eight waves: QKV 39.6 -> 38.1, split-K O-proj 29.0 -> 25.6 and Down 48.6 -> 42.8 us against two
     // register-staged 128 x 128 workgroups per unit; register-staged 128 x 256 tiles were slower than both)
-    const bool fits = (size_t)g.N * g.K * 2 < (1u << 31) && (size_t)g.M * g.K * 2 < (1u << 31) &&
-                      (g.K / g.splitk) % 32 == 0;
-    if (fits && tiles(256, 256) >= n_cu) return launch_dma<DmaBig>(g, s);
+    const bool fits = (size_t)g.N * g.K * 2 < (1u << 31) && (size_t)g.M * g.K * 2 < (1u << 31);
+    auto kfits = [&](int bk) { return (g.K / g.splitk) % bk == 0; };
+    if (fits && kfits(DmaBig::BK) && tiles(256, 256) >= n_cu) return launch_dma<DmaBig>(g, s);
     if (tiles(256, 256) >= n_cu) return launch_big<Big256>(g, s);
-    if (fits && tiles(128, 256) <= n_cu && 4 * tiles(128, 256) >= 3 * n_cu) return launch_dma<DmaWide>(g, s);
+    if (fits && kfits(DmaWide::BK) && tiles(128, 256) <= n_cu && 4 * tiles(128, 256) >= 3 * n_cu)
+      return launch_dma<DmaWide>(g, s);
     if (tiles(128, 128) >= n_cu || g.epi == EPI_STORE_F32) return launch_gemm_t<bf16, 128, 128>(g, s);
     // fewer 128 x 128 tiles than units, no K split, yet enough 64 x 64 tiles to fill them (VLM QKV at
     // M = 816, N = 2560: 520 tiles): the ring at two workgroups per unit (prefill 5.52 -> 5.38 ms)
-    if (gemm_pipe_enabled() && fits && g.splitk == 1 && g.K % DmaSmall::BK == 0 && tiles(64, 64) >= n_cu)
+    if (gemm_pipe_enabled() && fits && g.splitk == 1 && kfits(DmaSmall::BK) && tiles(64, 64) >= n_cu)
       return launch_dma<DmaSmall>(g, s);
     if (tiles(128, 64) >= n_cu) return launch_gemm_t<bf16, 128, 64>(g, s);
     return launch_gemm_t<bf16, 64, 64>(g, s);
