@@ -58,7 +58,8 @@ def test_gemm_bf16(M, N, K, splitk):
 @pytest.mark.parametrize("M,N,K,splitk", [(50, 1024, 4096, 16), (50, 2560, 1024, 4), (3200, 8192, 1024, 1),
                                           (200, 200, 192, 3), (3200, 2560, 1024, 1), (3200, 1024, 4096, 2),
                                           (816, 2048, 2048, 4), (816, 2560, 2048, 1), (700, 1536, 1024, 1),
-                                          (400, 8192, 1024, 1), (400, 1024, 4096, 8), (450, 8100, 320, 1)])
+                                          (400, 8192, 1024, 1), (400, 1024, 4096, 8), (450, 8100, 320, 1),
+                                          (2900, 8000, 512, 1), (3000, 2400, 1024, 1)])
 def test_gemm_bf16_more_shapes(M, N, K, splitk):
     from paper_2607_12659_amd import jpi
     rng = np.random.default_rng(M + N + K)
