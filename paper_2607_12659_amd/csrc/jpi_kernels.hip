@@ -499,8 +499,10 @@ typedef DmaShape<64, 64, 8, 64, 4, 4> DmaSmall;    // one slice: 16 KB; ring 64 
 typedef DmaShape<128, 256, 16, 64, 3, 4> DmaWide;  // one slice: 48 KB; ring 144 KB; waves 4 x 4 of 32 x 64
                                                   // (batch 64 48.62 -> 45.89 ms against eight waves on
                                                   // four 32-deep slices)
-typedef DmaShape<256, 256, 16, 32, 4, 4> DmaBig;   // one slice: 32 KB; ring 128 KB; waves 4 x 4 of 64 x 64
-                                                 // (four per SIMD: batch 64 48.28 -> 47.31 ms against eight)
+typedef DmaShape<256, 256, 16, 64, 2, 4> DmaBig;   // one slice: 64 KB; ring 128 KB (double-buffered);
+                                                   // waves 4 x 4 of 64 x 64 (batch 64: 48.28 -> 47.31 ms
+                                                   // for sixteen waves against eight, 45.74 -> 44.50 ms
+                                                   // for two 64-deep stages against four 32-deep ones)
 
 template <typename S>
 static hipError_t launch_dma(const GemmLaunch& g, hipStream_t s) {
@@ -690,7 +692,7 @@ hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s) {
     if (gemm_pipe_enabled() && g.M <= 512 && tiles(128, 128) < n_cu && g.splitk == 1 && g.K % DmaSmall::BK == 0 &&
         (size_t)g.N * g.K * 2 < (1u << 31))
       return launch_dma<DmaSmall>(g, s);
-    // Larger M: 256 x 256 tiles on the direct-to-LDS ring (three 32-deep slices in flight, sixteen
+    // Larger M: 256 x 256 tiles on the direct-to-LDS ring (64-deep slices, double-buffered, sixteen
     // waves) when such tiles alone cover the units (GateUp at M = 3200: 71.5 -> 68.1 us against the
     // register-staged k_gemm_big with eight waves), else one round of 128 x 256 ring tiles (two 64-deep
     // slices in flight, sixteen waves) when they fill at least three quarters of the units (M = 3200,
