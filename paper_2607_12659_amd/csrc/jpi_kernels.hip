@@ -693,11 +693,12 @@ hipError_t launch_gemm(jpi_dtype dt, const GemmLaunch& g, hipStream_t s) {
         (size_t)g.N * g.K * 2 < (1u << 31))
       return launch_dma<DmaSmall>(g, s);
     // Larger M: 256 x 256 tiles on the direct-to-LDS ring (64-deep slices, double-buffered, sixteen
-    // waves) when such tiles alone cover the units (GateUp at M = 3200: 71.5 -> 68.1 us against the
-    // register-staged k_gemm_big with eight waves), else one round of 128 x 256 ring tiles (two 64-deep
-    // slices in flight, sixteen waves) when they fill at least three quarters of the units (M = 3200,
-    // eight waves: QKV 39.6 -> 38.1, split-K O-proj 29.0 -> 25.6 and Down 48.6 -> 42.8 us against two
-    // register-staged 128 x 128 workgroups per unit; register-staged 128 x 256 tiles were slower than both)
+    // waves) when such tiles alone cover the units (GateUp at M = 3200: 71.5 us on the register-staged
+    // k_gemm_big, 68.1 us on the first, eight-wave version of this ring), else one round of 128 x 256 ring
+    // tiles (two 64-deep slices in flight, sixteen waves) when they fill at least three quarters of the
+    // units (M = 3200, first eight-wave version: QKV 39.6 -> 38.1, split-K O-proj 29.0 -> 25.6 and Down
+    // 48.6 -> 42.8 us against two register-staged 128 x 128 workgroups per unit; register-staged 128 x 256
+    // tiles were slower than both)
     const bool fits = (size_t)g.N * g.K * 2 < (1u << 31) && (size_t)g.M * g.K * 2 < (1u << 31);
     auto kfits = [&](int bk) { return (g.K / g.splitk) % bk == 0; };
     if (fits && kfits(DmaBig::BK) && tiles(256, 256) >= n_cu) return launch_dma<DmaBig>(g, s);
